@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X im2win path on one GPU.
+
+One step is one pass of the whole hot path over the workload's input, which is
+resident in device memory before timing starts:
+  1. workspace size query (host),
+  2. im2win transformation x -> window tensor,
+  3. convolution from the window tensor -> y,
+  4. fused convolution x -> y2 (window strips built on chip).
+The step therefore computes the convolution twice; `value` is the total
+convolution work of a step, 2 * (2*N*K*C*Ho*Wo*Fh*Fw) flops, divided by the
+measured step time.  Per-kernel times come from HIP events recorded on the
+launch stream around every kernel of every timed step.
+
+Prints one JSON line (rank 0, N=1).  `--gpus N` with N > 1 exits: this build
+runs on one GPU.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "conv GFLOP/s + % of MFMA/HBM roofline; im2win workspace bytes vs im2col"
+PEAK = {"f32": 157.3, "bf16": 2500.0}          # dense matrix-core TFLOP/s, MI355X
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = {
+    "transform": ["paper_2306_14320_amd/csrc/transform.hip", "paper_2306_14320_amd/csrc/common.h"],
+    "conv": ["paper_2306_14320_amd/csrc/conv_f32.hip", "paper_2306_14320_amd/csrc/conv_bf16.hip",
+             "paper_2306_14320_amd/csrc/conv_common.h", "paper_2306_14320_amd/csrc/common.h"],
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_hash(kind):
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[kind]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel_kind):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; otherwise None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = t.get(workload, {}).get(kernel_kind)
+    if not entry or entry.get("source_hash") != source_hash(kernel_kind):
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=None, help="workload name (default: the headline one)")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="also print one line per workload (no CPU baseline)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device copy of known size (for counter scaling)")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    nbytes = 256 << 20
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes,
+                      "launches": 5}), flush=True)
+
+
+def run_workload(wl, steps, warmup, with_cpu):
+    import torch
+    import paper_2306_14320_amd as P
+    import workloads
+
+    dev = "cuda:0"
+    d = P.desc_for((wl.n, wl.c, wl.h, wl.w), (wl.k, wl.c, wl.fh, wl.fw), (wl.sh, wl.sw),
+                   (wl.ph, wl.pw), workloads.torch_dtype(wl.dtype))
+    ho, wo = P.im2win_output_shape(d)
+    ws_bytes = P.im2win_workspace_bytes(d)
+    col_bytes = P.im2win_im2col_bytes(d)
+    x = workloads.make_input(wl).to(dev)
+    w = workloads.make_filter(wl).to(dev)
+    ws = torch.empty(P.workspace_shape(d), dtype=x.dtype, device=dev)
+    y = torch.empty((wl.n, wl.k, ho, wo), dtype=torch.float32, device=dev)
+    y2 = torch.empty_like(y)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    xp, wp, wsp, yp, y2p = x.data_ptr(), w.data_ptr(), ws.data_ptr(), y.data_ptr(), y2.data_ptr()
+
+    def step(ev=None):
+        P.im2win_workspace_bytes(d)
+        if ev: ev[0].record(stream)
+        P.im2win_transform(d, xp, wsp, ws_bytes, sp)
+        if ev: ev[1].record(stream)
+        P.im2win_conv2d(d, wsp, ws_bytes, wp, yp, sp)
+        if ev: ev[2].record(stream)
+        P.im2win_conv2d_fused(d, xp, wp, y2p, sp)
+        if ev: ev[3].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_xf = sum(e[0].elapsed_time(e[1]) for e in evs) / steps * 1e-3
+    t_cv = sum(e[1].elapsed_time(e[2]) for e in evs) / steps * 1e-3
+    t_fu = sum(e[2].elapsed_time(e[3]) for e in evs) / steps * 1e-3
+
+    conv_flops = 2 * wl.n * wl.k * wl.c * ho * wo * wl.fh * wl.fw
+    e = x.element_size()
+    xf_bytes = wl.n * wl.c * wl.h * wl.w * e + ws_bytes        # read x once, write the window tensor
+    ms_per_step = wall / steps * 1e3
+    value = 2 * conv_flops / (wall / steps) / 1e9
+    peak = PEAK[wl.dtype]
+    dominant = max([("conv", t_cv), ("fused", t_fu), ("transform", t_xf)], key=lambda kv: kv[1])[0]
+    traffic = measured_traffic(wl.name, "conv")
+    if dominant == "transform":
+        achieved = xf_bytes / t_xf / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name, "transform"),
+                "kernel": "transform"}
+    else:
+        t = t_cv if dominant == "conv" else t_fu
+        achieved = conv_flops / t / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": traffic if dominant == "conv" else None,
+                "kernel": "conv2d" if dominant == "conv" else "conv2d_fused"}
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GFLOP/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic (seeded, distributions of the workload)",
+        "config": {"workload": wl.label(), "global_batch": wl.n, "parallelism": "none (1 GPU)",
+                   "step": "workspace query + transform + conv2d + conv2d_fused"},
+        "roofline": roof,
+        "kernels": {
+            "transform": {"ms": round(t_xf * 1e3, 4), "GB_per_s": round(xf_bytes / t_xf / 1e9, 1),
+                          "hbm_frac": round(xf_bytes / t_xf / 1e9 / HBM_PEAK_GBS, 4),
+                          "algorithmic_bytes": xf_bytes},
+            "conv2d": {"ms": round(t_cv * 1e3, 4), "GFLOP_per_s": round(conv_flops / t_cv / 1e9, 1),
+                       "mfma_frac": round(conv_flops / t_cv / 1e12 / peak, 4)},
+            "conv2d_fused": {"ms": round(t_fu * 1e3, 4), "GFLOP_per_s": round(conv_flops / t_fu / 1e9, 1),
+                             "mfma_frac": round(conv_flops / t_fu / 1e12 / peak, 4)},
+            "transform_plus_conv2d_GFLOP_per_s": round(conv_flops / (t_xf + t_cv) / 1e9, 1),
+        },
+        "workspace": {"im2win_bytes": ws_bytes, "im2col_bytes": col_bytes,
+                      "im2win_over_im2col": round(ws_bytes / col_bytes, 4)},
+        "conv_flops": conv_flops,
+    }
+    if with_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, conv_flops)
+    return out
+
+
+def cpu_baseline(wl, conv_flops):
+    """The oracle (fp64 seven-loop direct convolution, OpenMP) on the host
+    cores, repeated over the full workload until about 10 s have passed."""
+    import oracle
+    from oracle import Shape
+    import workloads
+    s = Shape(wl.n, wl.c, wl.h, wl.w, wl.k, wl.fh, wl.fw, wl.sh, wl.sw, wl.ph, wl.pw)
+    x = workloads.make_input(wl).double().numpy()
+    w = workloads.make_filter(wl).double().numpy()
+    reps, total = 0, 0.0
+    while total < 10.0 and reps < 30:
+        t0 = time.perf_counter()
+        oracle.direct_conv(s, x, w)
+        total += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(conv_flops * reps / total / 1e9, 3), "unit": "GFLOP/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"full workload (N={wl.n}), {reps} run(s), {total:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    import workloads
+    wl = workloads.BY_NAME[args.workload] if args.workload else workloads.HEADLINE
+    if args.all_workloads:
+        for other in workloads.WORKLOADS:
+            if other.name != wl.name:
+                line = run_workload(other, args.steps, args.warmup, False)
+                line["headline"] = False
+                print(json.dumps(line), flush=True)
+    print(json.dumps(run_workload(wl, args.steps, args.warmup, not args.no_cpu_baseline)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+"""MI355X (gfx950) im2win transformation and im2win-based convolution.
+
+Python binding of ``libim2win.so`` (C ABI in ``include/im2win.h``).  The
+functions named ``im2win_*`` mirror the C entry points one to one and only
+marshal arguments; every step of the computation runs in the HIP kernels.
+The tensor helpers below them (``desc_for``, ``transform``, ``conv2d``,
+``conv2d_fused``) use PyTorch only to allocate device memory and to pick the
+current HIP stream.
+
+There is no fallback: if the library is missing or was built for another
+target, loading fails with an error.  Build it with
+``python -m paper_2306_14320_amd.build``.
+
+Method: Lu, Chu, Liu, "Im2win: Memory Efficient Convolution On SIMD
+Architectures", arXiv 2306.14320 (Sec. III, Alg. 1 and Alg. 2).
+"""
+import ctypes
+import os
+
+import torch  # imported first: libim2win then binds to the HIP runtime torch has loaded
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libim2win.so")
+
+IM2WIN_F32, IM2WIN_BF16 = 0, 1
+IM2WIN_OK = 0
+IM2WIN_EINVAL = -1
+IM2WIN_ENULL = -2
+IM2WIN_EWORKSPACE = -3
+IM2WIN_EHIP = -4
+IM2WIN_EOVERFLOW = -5
+IM2WIN_EALIGN = -6
+
+
+class im2win_desc(ctypes.Structure):
+    """Mirror of the C ``im2win_desc``."""
+    _fields_ = [
+        ("n", ctypes.c_int64), ("c", ctypes.c_int64), ("h", ctypes.c_int64), ("w", ctypes.c_int64),
+        ("k", ctypes.c_int64), ("fh", ctypes.c_int64), ("fw", ctypes.c_int64),
+        ("stride_h", ctypes.c_int64), ("stride_w", ctypes.c_int64),
+        ("pad_h", ctypes.c_int64), ("pad_w", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+    ]
+
+    def __repr__(self):
+        return ("im2win_desc(n=%d, c=%d, h=%d, w=%d, k=%d, fh=%d, fw=%d, stride=(%d,%d), "
+                "pad=(%d,%d), dtype=%d)" % (self.n, self.c, self.h, self.w, self.k, self.fh,
+                                            self.fw, self.stride_h, self.stride_w, self.pad_h,
+                                            self.pad_w, self.dtype))
+
+
+class Im2winError(RuntimeError):
+    def __init__(self, code, message):
+        super().__init__(f"im2win error {code}: {message}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library():
+    """Load libim2win.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2306_14320_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, D, SZ, I64P = ctypes.c_void_p, ctypes.POINTER(im2win_desc), ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64)
+    sigs = {
+        "im2win_workspace_bytes": [D, ctypes.POINTER(SZ)],
+        "im2win_im2col_bytes": [D, ctypes.POINTER(SZ)],
+        "im2win_output_shape": [D, I64P, I64P],
+        "im2win_transform": [D, P, P, SZ, P],
+        "im2win_conv2d": [D, P, SZ, P, P, P],
+        "im2win_conv2d_fused": [D, P, P, P, P],
+        "im2win_selftest": [],
+        "im2win_check_plan": [D],
+    }
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.im2win_last_error.argtypes = []
+    lib.im2win_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(rc):
+    if rc != IM2WIN_OK:
+        raise Im2winError(rc, im2win_last_error())
+
+
+# ---------------------------------------------------------------------------
+# C entry points, same names and arguments (raising Im2winError on failure)
+# ---------------------------------------------------------------------------
+
+def im2win_workspace_bytes(desc: im2win_desc) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().im2win_workspace_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def im2win_im2col_bytes(desc: im2win_desc) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().im2win_im2col_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def im2win_output_shape(desc: im2win_desc):
+    ho, wo = ctypes.c_int64(), ctypes.c_int64()
+    _check(load_library().im2win_output_shape(ctypes.byref(desc), ctypes.byref(ho), ctypes.byref(wo)))
+    return ho.value, wo.value
+
+
+def im2win_transform(desc: im2win_desc, x: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _check(load_library().im2win_transform(ctypes.byref(desc), x, ws, ws_bytes, stream))
+
+
+def im2win_conv2d(desc: im2win_desc, ws: int, ws_bytes: int, w: int, y: int, stream: int) -> None:
+    _check(load_library().im2win_conv2d(ctypes.byref(desc), ws, ws_bytes, w, y, stream))
+
+
+def im2win_conv2d_fused(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
+    _check(load_library().im2win_conv2d_fused(ctypes.byref(desc), x, w, y, stream))
+
+
+def im2win_last_error() -> str:
+    return load_library().im2win_last_error().decode()
+
+
+def im2win_selftest() -> int:
+    return load_library().im2win_selftest()
+
+
+def im2win_check_plan(desc: im2win_desc) -> int:
+    """0 if every kernel index for this descriptor stays in bounds, else the
+    number of violations (the first is in im2win_last_error())."""
+    return load_library().im2win_check_plan(ctypes.byref(desc))
+
+
+# ---------------------------------------------------------------------------
+# Tensor helpers (marshalling: shapes -> descriptor, tensors -> pointers)
+# ---------------------------------------------------------------------------
+
+_DTYPES = {torch.float32: IM2WIN_F32, torch.bfloat16: IM2WIN_BF16}
+
+
+def _pair(v):
+    return (v, v) if isinstance(v, int) else tuple(v)
+
+
+def desc_for(x_shape, w_shape, stride=1, padding=0, dtype=torch.float32) -> im2win_desc:
+    """Descriptor for input N x C x H x W, filter K x C x Fh x Fw."""
+    n, c, h, w = x_shape
+    k, c2, fh, fw = w_shape
+    if c2 != c:
+        raise ValueError(f"filter has {c2} input channels, input has {c}")
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    if dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dtype} (float32 or bfloat16)")
+    return im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, _DTYPES[dtype])
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev(t, name):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    return t.data_ptr()
+
+
+def workspace_shape(desc: im2win_desc):
+    ho, _ = im2win_output_shape(desc)
+    return (desc.n, desc.c, ho, (desc.w + 2 * desc.pad_w) * desc.fh)
+
+
+def transform(x: torch.Tensor, desc: im2win_desc, ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Window tensor of x (N x C x Ho x Wp*Fh, dtype of x)."""
+    if ws is None:
+        ws = torch.empty(workspace_shape(desc), dtype=x.dtype, device=x.device)
+    im2win_transform(desc, _dev(x, "x"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+    return ws
+
+
+def conv2d(ws: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
+           stream=None) -> torch.Tensor:
+    """Convolution from a window tensor; returns y (N x K x Ho x Wo, fp32)."""
+    ho, wo = im2win_output_shape(desc)
+    if y is None:
+        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=ws.device)
+    im2win_conv2d(desc, _dev(ws, "ws"), ws.numel() * ws.element_size(), _dev(w, "w"),
+                  _dev(y, "y"), _stream(stream))
+    return y
+
+
+def conv2d_fused(x: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
+                 stream=None) -> torch.Tensor:
+    """Convolution straight from x (window strips built on chip); returns y."""
+    ho, wo = im2win_output_shape(desc)
+    if y is None:
+        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=x.device)
+    im2win_conv2d_fused(desc, _dev(x, "x"), _dev(w, "w"), _dev(y, "y"), _stream(stream))
+    return y

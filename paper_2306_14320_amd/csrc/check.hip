@@ -1,0 +1,169 @@
+// Host-side bounds check of the launch plans.  It replays, with the very
+// functions the kernels call (XformBlock, locate/advance, TileRuns,
+// pixel_base), every workgroup of the transformation and of the convolution
+// for a descriptor and verifies that each LDS and device-memory index the
+// kernels form stays inside its buffer.  No HIP calls.
+#include <cstdarg>
+#include <cstdio>
+
+#include "common.h"
+#include "conv_common.h"
+
+namespace im2win {
+namespace {
+
+struct Report {
+    int64_t violations = 0;
+    char* msg;
+    size_t msglen;
+    void fail(const char* fmt, ...) {
+        if (violations++ == 0) {
+            va_list ap;
+            va_start(ap, fmt);
+            vsnprintf(msg, msglen, fmt, ap);
+            va_end(ap);
+        }
+    }
+};
+
+void check_transform(const Geometry& g, Report& r) {
+    const XformPlan p = plan_transform(g);
+    if (!p.use_lds) return;   // the direct kernel indexes rows only through bounds-checked x
+    const XformArgs a = transform_args(g, p, nullptr, nullptr);
+    const int64_t x_elems = g.n * g.c * g.h * g.w;
+    const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
+    const int64_t lds_elems = p.lds_bytes / g.elem;
+    int64_t next_out = 0;
+    for (int64_t b = 0; b < p.blocks && r.violations < 16; ++b) {
+        XformBlock blk;
+        blk.init(b, a);
+        if (blk.nplanes < 1 || blk.nrows < 1)
+            r.fail("transform block %lld: empty run", (long long)b);
+        if ((int64_t)blk.nplanes * blk.nrin * g.w > lds_elems)
+            r.fail("transform block %lld: stages %lld elements, LDS holds %lld", (long long)b,
+                   (long long)blk.nplanes * blk.nrin * g.w, (long long)lds_elems);
+        const int64_t src_lo = (blk.plane0 * g.h + blk.y_lo) * g.w;
+        const int64_t src_hi = ((blk.plane0 + blk.nplanes - 1) * g.h + blk.y_lo + blk.nrin) * g.w;
+        if (blk.nrin > 0 && (src_lo < 0 || src_hi > x_elems || blk.y_lo + blk.nrin > g.h))
+            r.fail("transform block %lld: reads x[%lld, %lld) of %lld", (long long)b,
+                   (long long)src_lo, (long long)src_hi, (long long)x_elems);
+        if (blk.obase != next_out)
+            r.fail("transform block %lld: output run starts at %lld, expected %lld", (long long)b,
+                   (long long)blk.obase, (long long)next_out);
+        next_out = blk.obase + blk.olen;
+        if (next_out > ws_elems)
+            r.fail("transform block %lld: writes up to %lld of %lld", (long long)b,
+                   (long long)next_out, (long long)ws_elems);
+        Cursor c = locate(0, a);
+        for (int e = 0; e < blk.olen; ++e) {
+            const Cursor d = locate(e, a);
+            if (d.plane != c.plane || d.mrel != c.mrel || d.k != c.k || d.u != c.u) {
+                r.fail("transform block %lld: cursor stepping disagrees at element %d", (long long)b, e);
+                break;
+            }
+            if (c.plane >= blk.nplanes || c.mrel >= blk.nrows) {
+                r.fail("transform block %lld: element %d outside its run", (long long)b, e);
+                break;
+            }
+            const int yy = (blk.m0 + c.mrel) * a.sh + c.u - a.ph;
+            const int xx = c.k - a.pw;
+            if (yy >= 0 && yy < g.h && xx >= 0 && xx < g.w) {
+                const int li = blk.lds_index(c.plane, yy, xx, a.w);
+                if (yy < blk.y_lo || yy >= blk.y_lo + blk.nrin || li < 0 || li >= (int64_t)blk.nplanes * blk.nrin * g.w) {
+                    r.fail("transform block %lld: element %d reads LDS %d (rows [%d,%d))", (long long)b,
+                           e, li, blk.y_lo, blk.y_lo + blk.nrin);
+                    break;
+                }
+            }
+            advance(c, a);
+        }
+    }
+    if (r.violations == 0 && next_out != ws_elems)
+        r.fail("transform: workgroups write %lld of %lld elements", (long long)next_out,
+               (long long)ws_elems);
+}
+
+void check_conv(const Geometry& g, Report& r) {
+    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g) : plan_conv_f32(g);
+    if (p.kind == ConvPlan::kNone) {
+        r.fail("conv: no tile configuration fits in LDS (the launch would be refused)");
+        return;
+    }
+    const bool bf16 = p.kind == ConvPlan::kBf16Lds;
+    const ConvArgs a = bf16 ? conv_args_bf16(g, p, nullptr, nullptr, nullptr)
+                            : conv_args_f32(g, p, nullptr, nullptr, nullptr);
+    if (p.lds_bytes > kConvLdsBudgetBytes)
+        r.fail("conv: plan uses %lld bytes of LDS", (long long)p.lds_bytes);
+    if (!bf16 && a.kpad < p.rc * a.taps + ((p.rc * a.taps) & 1))
+        r.fail("conv: filter tile has %d rows for %d reduction slots", a.kpad, p.rc * a.taps);
+    const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
+    const int64_t y_elems = g.n * g.k * g.ho * g.wo;
+    const int64_t ptiles = (g.npix + p.bn - 1) / p.bn;
+    int64_t covered = 0;
+    for (int64_t t = 0; t < ptiles && r.violations < 16; ++t) {
+        TileRuns tr;
+        tr.init((int)t, p.bn, a);
+        if (tr.strip_len > p.strip_cap || tr.strip_len < 1)
+            r.fail("conv tile %lld: strip of %d positions, LDS holds %lld", (long long)t,
+                   tr.strip_len, (long long)p.strip_cap);
+        int sum = 0;
+        for (int s = 0; s < tr.nseg; ++s) {
+            const int len = tr.seg_len(s);
+            if (len < 1 || tr.seg_off(s) != sum)
+                r.fail("conv tile %lld: segment %d has length %d at offset %d (expected %d)",
+                       (long long)t, s, len, tr.seg_off(s), sum);
+            sum += len;
+            // unfused source run of every channel
+            const int64_t first = (((int64_t)(tr.i0 + s) * g.c + 0) * g.ho + tr.seg_m(s)) * g.row_len + tr.seg_q(s);
+            const int64_t last = (((int64_t)(tr.i0 + s) * g.c + g.c - 1) * g.ho + tr.seg_m(s)) * g.row_len + tr.seg_q(s) + len;
+            if (first < 0 || last > ws_elems)
+                r.fail("conv tile %lld: segment %d reads window tensor [%lld, %lld) of %lld",
+                       (long long)t, s, (long long)first, (long long)last, (long long)ws_elems);
+            // a run must stay inside its plane
+            if ((int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s) + len > g.ho * g.row_len)
+                r.fail("conv tile %lld: segment %d runs past its plane", (long long)t, s);
+        }
+        if (sum != tr.strip_len)
+            r.fail("conv tile %lld: segments cover %d of %d positions", (long long)t, sum, tr.strip_len);
+        for (int q = 0; q < p.bn; ++q) {
+            int px = tr.p0 + q;
+            const bool valid = px <= tr.plast;
+            if (!valid) px = tr.p0;
+            int64_t yoff;
+            const int base = pixel_base(tr, a, px, &yoff);
+            // the window must lie inside its own segment of the strip
+            const int gi = px / (int)g.wo, ii = gi / (int)g.ho;
+            const int s = ii - tr.i0;
+            if (s < 0 || s >= tr.nseg || base < tr.seg_off(s) ||
+                base + (int)g.taps > tr.seg_off(s) + tr.seg_len(s)) {
+                r.fail("conv tile %lld: pixel %d window [%d, %d) outside segment %d", (long long)t,
+                       px, base, base + (int)g.taps, s);
+                break;
+            }
+            if (valid) {
+                ++covered;
+                const int mm = gi - ii * (int)g.ho, nn = px - gi * (int)g.wo;
+                if (yoff != (int64_t)ii * g.k * g.ho * g.wo + (int64_t)mm * g.wo + nn ||
+                    yoff + (g.k - 1) * g.ho * g.wo >= y_elems)
+                    r.fail("conv tile %lld: pixel %d output offset %lld", (long long)t, px,
+                           (long long)yoff);
+            }
+        }
+    }
+    if (r.violations == 0 && covered != g.npix)
+        r.fail("conv: tiles cover %lld of %lld pixels", (long long)covered, (long long)g.npix);
+}
+
+}  // namespace
+
+int64_t check_plans(const Geometry& g, char* msg, size_t msglen) {
+    Report r;
+    r.msg = msg;
+    r.msglen = msglen;
+    if (msglen) msg[0] = '\0';
+    check_transform(g, r);
+    check_conv(g, r);
+    return r.violations;
+}
+
+}  // namespace im2win

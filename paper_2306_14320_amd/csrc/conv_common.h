@@ -1,0 +1,153 @@
+// Tile bookkeeping shared by the fp32 and bf16 convolution kernels.
+// Internal to libim2win.
+#pragma once
+
+#include "common.h"
+
+#include <algorithm>
+
+namespace im2win {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kConvThreads = 256;            // 4 waves of 64 lanes
+constexpr int kConvLdsBudgetBytes = 64 * 1024;
+
+struct ConvArgs {
+    const void* src;   // window tensor (unfused) or input x (fused)
+    const void* w;     // K x C x Fh x Fw
+    float* y;          // N x K x Ho x Wo
+    int c, h, w_in, k, fh, fw, sh, sw, ph, pw;
+    int ho, wo, wp, row_len, used_len, taps;
+    int npix, howo;
+    int rc;            // input channels per chunk
+    int strip_cap;     // LDS strip positions reserved per channel
+    int kpad;          // fp32: filter-tile rows, rc*taps rounded up to even
+    int tc;            // bf16: filter taps staged per pass
+    int num_jtiles;
+    FastDiv div_wo, div_ho, div_kpad, div_taps, div_fw, div_row, div_fh, div_tc2;
+    int d_row, d_k, d_u;   // kConvThreads = d_row*L + d_k*Fh + d_u (fused walk)
+};
+
+// Geometry of the window-tensor runs that one pixel tile reads (per channel).
+struct TileRuns {
+    int p0, plast;
+    int i0, m0, n0;     // first pixel
+    int i1, m1, n1;     // last pixel
+    int nseg;           // images touched
+    int qa0;            // first run starts at this column of row m0
+    int len0, len_mid, len_last, strip_len;
+
+    __host__ __device__ void init(int ptile, int bn, const ConvArgs& a) {
+        p0 = ptile * bn;
+        plast = (p0 + bn < a.npix ? p0 + bn : a.npix) - 1;
+        const int g0 = (int)fast_div((uint32_t)p0, a.div_wo);
+        const int g1 = (int)fast_div((uint32_t)plast, a.div_wo);
+        n0 = p0 - g0 * a.wo;
+        n1 = plast - g1 * a.wo;
+        i0 = (int)fast_div((uint32_t)g0, a.div_ho);
+        i1 = (int)fast_div((uint32_t)g1, a.div_ho);
+        m0 = g0 - i0 * a.ho;
+        m1 = g1 - i1 * a.ho;
+        nseg = i1 - i0 + 1;
+        qa0 = n0 * a.sw * a.fh;
+        const int qb_last = (n1 * a.sw + a.fw) * a.fh;
+        len_mid = (a.ho - 1) * a.row_len + a.used_len;
+        if (nseg == 1) {
+            len0 = (m1 - m0) * a.row_len + qb_last - qa0;
+            len_last = 0;
+            strip_len = len0;
+        } else {
+            len0 = (a.ho - 1 - m0) * a.row_len + a.used_len - qa0;
+            len_last = m1 * a.row_len + qb_last;
+            strip_len = len0 + (nseg - 2) * len_mid + len_last;
+        }
+    }
+    __host__ __device__ int seg_off(int s) const { return s == 0 ? 0 : len0 + (s - 1) * len_mid; }
+    __host__ __device__ int seg_len(int s) const {
+        return s == 0 ? len0 : (s == nseg - 1 ? len_last : len_mid);
+    }
+    __host__ __device__ int seg_m(int s) const { return s == 0 ? m0 : 0; }
+    __host__ __device__ int seg_q(int s) const { return s == 0 ? qa0 : 0; }
+};
+
+// Strip offset of the window of pixel p (its column in the implicit GEMM) and
+// the output offset of its channel-0 element.  Pixels past the end of the
+// tile are clamped to the first pixel of the tile (computed, never stored).
+__host__ __device__ inline int pixel_base(const TileRuns& tr, const ConvArgs& a, int p,
+                                          int64_t* yoff) {
+    const int g = (int)fast_div((uint32_t)p, a.div_wo);
+    const int n = p - g * a.wo;
+    const int i = (int)fast_div((uint32_t)g, a.div_ho);
+    const int m = g - i * a.ho;
+    const int s = i - tr.i0;
+    *yoff = (int64_t)i * a.k * a.howo + m * a.wo + n;
+    return tr.seg_off(s) + (m - tr.seg_m(s)) * a.row_len + n * a.sw * a.fh - tr.seg_q(s);
+}
+
+// Launch plan of a convolution kernel (chosen on the host).
+struct ConvPlan {
+    enum Kind { kNone, kF32Lds, kBf16Lds };
+    Kind kind = kNone;     // fp32 strips (fp32, or bf16 widened) / channel-inner bf16 strips
+    int bm = 0, bn = 0;    // output channels x pixels per workgroup
+    int rc = 0;            // input channels per LDS chunk
+    int tc = 0;            // bf16: taps per filter pass
+    int64_t strip_cap = 0; // LDS strip positions per channel
+    int64_t lds_bytes = 0;
+};
+
+ConvPlan plan_conv_f32(const Geometry& g);
+ConvPlan plan_conv_bf16(const Geometry& g);
+ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
+                       float* y);
+ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
+                        float* y);
+int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
+                         const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
+
+struct TileCfg {
+    int bm, bn;
+};
+
+// Upper bound of the per-channel strip length over all pixel tiles of `bn`
+// pixels: a tile spanning D row boundaries reads D*L + (n1-n0)*sw*Fh + Fw*Fh
+// elements with n1 - n0 = (pixels - 1) - D*Wo; the bound is linear in D.
+inline int64_t strip_bound(const Geometry& g, int bn) {
+    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
+    auto at = [&](int64_t d) {
+        return d * (g.row_len - g.wo * g.sw * g.fh) + (int64_t)(bn - 1) * g.sw * g.fh + g.fw * g.fh;
+    };
+    return std::max<int64_t>(1, std::max(at(0), at(dmax))) + 1;
+}
+
+// Common launch arguments (everything except the per-dtype chunking).
+inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w, float* y,
+                               int bm) {
+    ConvArgs a;
+    a.src = src;
+    a.w = w;
+    a.y = y;
+    a.c = (int)g.c; a.h = (int)g.h; a.w_in = (int)g.w; a.k = (int)g.k;
+    a.fh = (int)g.fh; a.fw = (int)g.fw; a.sh = (int)g.sh; a.sw = (int)g.sw;
+    a.ph = (int)g.ph; a.pw = (int)g.pw;
+    a.ho = (int)g.ho; a.wo = (int)g.wo; a.wp = (int)g.wp;
+    a.row_len = (int)g.row_len; a.used_len = (int)g.used_len; a.taps = (int)g.taps;
+    a.npix = (int)g.npix; a.howo = (int)(g.ho * g.wo);
+    a.rc = 1; a.strip_cap = 1; a.kpad = 2; a.tc = 1;
+    a.num_jtiles = (int)((g.k + bm - 1) / bm);
+    a.div_wo = make_fastdiv((uint32_t)a.wo);
+    a.div_ho = make_fastdiv((uint32_t)a.ho);
+    a.div_taps = make_fastdiv((uint32_t)a.taps);
+    a.div_fw = make_fastdiv((uint32_t)a.fw);
+    a.div_row = make_fastdiv((uint32_t)a.row_len);
+    a.div_fh = make_fastdiv((uint32_t)a.fh);
+    a.div_kpad = make_fastdiv(2);
+    a.div_tc2 = make_fastdiv(2);
+    a.d_row = kConvThreads / a.row_len;
+    const int rem = kConvThreads % a.row_len;
+    a.d_k = rem / a.fh;
+    a.d_u = rem % a.fh;
+    return a;
+}
+
+}  // namespace im2win

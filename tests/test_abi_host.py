@@ -1,0 +1,151 @@
+"""Host-side tests of the C ABI (no GPU needed): the library loads and exports
+every declared symbol, size queries agree with the oracle, invalid arguments
+are rejected before any HIP call, and every launch plan stays in bounds."""
+import ctypes
+import os
+import random
+import re
+
+import pytest
+
+import oracle
+from oracle import Shape
+import workloads
+import paper_2306_14320_amd as P
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "im2win.h")
+
+
+def _desc(s: Shape, dtype=P.IM2WIN_F32):
+    return P.im2win_desc(s.n, s.c, s.h, s.w, s.k, s.fh, s.fw, s.sh, s.sw, s.ph, s.pw, dtype)
+
+
+def _wl_shape(wl):
+    return Shape(wl.n, wl.c, wl.h, wl.w, wl.k, wl.fh, wl.fw, wl.sh, wl.sw, wl.ph, wl.pw)
+
+
+def _wl_dtype(wl):
+    return P.IM2WIN_F32 if wl.dtype == "f32" else P.IM2WIN_BF16
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:int|const char\s*\*)\s*(im2win_\w+)\s*\(", text, re.M))
+    assert {"im2win_workspace_bytes", "im2win_transform", "im2win_conv2d",
+            "im2win_conv2d_fused", "im2win_last_error"} <= declared
+    lib = ctypes.CDLL(P.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+
+
+def test_fastdiv_selftest():
+    assert P.im2win_selftest() == 0
+
+
+SHAPES = [_wl_shape(wl) for wl in workloads.WORKLOADS] + [
+    Shape(1, 1, 4, 4, 2, 2, 2), Shape(2, 3, 9, 11, 3, 3, 5, 2, 2, 1, 2),
+    Shape(1, 2, 9, 9, 2, 2, 2, 3, 3), Shape(1, 1, 3, 3, 1, 3, 3, 1, 1, 2, 2),
+    Shape(128, 3, 227, 227, 96, 11, 11, 4, 4),
+]
+
+
+@pytest.mark.parametrize("s", SHAPES, ids=str)
+@pytest.mark.parametrize("dtype", [P.IM2WIN_F32, P.IM2WIN_BF16])
+def test_sizes_agree_with_oracle(s, dtype):
+    d = _desc(s, dtype)
+    e = 4 if dtype == P.IM2WIN_F32 else 2
+    assert P.im2win_output_shape(d) == (s.ho, s.wo)
+    assert P.im2win_workspace_bytes(d) == oracle.im2win_elems(s) * e
+    assert P.im2win_im2col_bytes(d) == oracle.im2col_elems(s) * e
+    assert P.workspace_shape(d) == s.win_shape
+
+
+def test_workspace_not_larger_than_im2col_on_workloads():
+    for wl in workloads.WORKLOADS:
+        d = _desc(_wl_shape(wl), _wl_dtype(wl))
+        assert P.im2win_workspace_bytes(d) < P.im2win_im2col_bytes(d)
+
+
+def _code(fn, *args):
+    with pytest.raises(P.Im2winError) as ei:
+        fn(*args)
+    return ei.value.code
+
+
+GOOD = Shape(2, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1)
+FAKE = 0x10000   # never dereferenced: every call below is rejected before any HIP call
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n", 0), ("c", 0), ("h", -1), ("w", 0), ("k", 0), ("fh", 0), ("fw", 0),
+    ("stride_h", 0), ("stride_w", -2), ("pad_h", -1), ("pad_w", -1), ("dtype", 7),
+    ("fh", 11), ("fw", 11),  # filter larger than the padded input: Ho or Wo < 1
+])
+def test_invalid_descriptor_rejected(field, value):
+    d = _desc(GOOD)
+    setattr(d, field, value)
+    assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_transform, d, FAKE, FAKE, 1 << 30, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d, d, FAKE, 1 << 30, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert P.im2win_last_error() != ""
+
+
+def test_null_misaligned_and_short_workspace_rejected():
+    d = _desc(GOOD)
+    need = P.im2win_workspace_bytes(d)
+    assert _code(P.im2win_transform, d, 0, FAKE, need, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_transform, d, FAKE, 0, need, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_transform, d, FAKE + 4, FAKE, need, 0) == P.IM2WIN_EALIGN
+    assert _code(P.im2win_transform, d, FAKE, FAKE, need - 1, 0) == P.IM2WIN_EWORKSPACE
+    assert _code(P.im2win_conv2d, d, FAKE, need - 4, FAKE, FAKE, 0) == P.IM2WIN_EWORKSPACE
+    assert _code(P.im2win_conv2d, d, FAKE, need, 0, FAKE, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_conv2d, d, FAKE, need, FAKE, FAKE + 8, 0) == P.IM2WIN_EALIGN
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, 0, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE + 2, FAKE, 0) == P.IM2WIN_EALIGN
+    lib = P.load_library()
+    assert lib.im2win_workspace_bytes(None, None) == P.IM2WIN_ENULL
+    assert lib.im2win_workspace_bytes(ctypes.byref(d), None) == P.IM2WIN_ENULL
+
+
+def test_oversized_problem_rejected():
+    d = _desc(Shape(1 << 20, 4, 1024, 1024, 4, 3, 3, 1, 1, 1, 1))   # N*Ho*Wo >= 2^31
+    assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EOVERFLOW
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
+
+
+@pytest.mark.parametrize("wl", workloads.WORKLOADS, ids=lambda wl: wl.name)
+def test_launch_plans_in_bounds_on_workloads(wl):
+    d = _desc(_wl_shape(wl), _wl_dtype(wl))
+    assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+
+
+def test_launch_plans_in_bounds_on_random_shapes():
+    rng = random.Random(14320)
+    checked = 0
+    while checked < 600:
+        n, c, h, w = rng.randint(1, 4), rng.randint(1, 40), rng.randint(1, 40), rng.randint(1, 64)
+        k, fh, fw = rng.randint(1, 140), rng.randint(1, 9), rng.randint(1, 9)
+        sh, sw, ph, pw = rng.randint(1, 4), rng.randint(1, 4), rng.randint(0, 4), rng.randint(0, 4)
+        if h + 2 * ph < fh or w + 2 * pw < fw:
+            continue
+        for dt in (P.IM2WIN_F32, P.IM2WIN_BF16):
+            d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, dt)
+            assert P.im2win_check_plan(d) == 0, (d, P.im2win_last_error())
+            checked += 1
+
+
+def test_launch_plans_in_bounds_on_paper_layers():
+    """Table 1 layers at batch 2 (the plan depends on the batch only through
+    the number of tiles)."""
+    import json
+    from conftest import GOLDEN
+    t = json.load(open(os.path.join(GOLDEN, "table1.json")))
+    for layer in t["layers"]:
+        ci, hi, wi = layer["input"]
+        co, hf, wf = layer["filter"]
+        st = layer["stride"]
+        for dt in (P.IM2WIN_F32, P.IM2WIN_BF16):
+            d = P.im2win_desc(2, ci, hi, wi, co, hf, wf, st, st, 0, 0, dt)
+            assert P.im2win_check_plan(d) == 0, (layer["name"], P.im2win_last_error())
