@@ -92,10 +92,19 @@ void check_conv(const Geometry& g, Report& r) {
     const bool bf16 = p.kind == ConvPlan::kBf16Lds;
     const ConvArgs a = bf16 ? conv_args_bf16(g, p, nullptr, nullptr, nullptr)
                             : conv_args_f32(g, p, nullptr, nullptr, nullptr);
-    if (p.lds_bytes > kConvLdsBudgetBytes)
+    if (p.lds_bytes > kConvLdsMaxBytes)
         r.fail("conv: plan uses %lld bytes of LDS", (long long)p.lds_bytes);
-    if (!bf16 && a.kpad < p.rc * a.taps + ((p.rc * a.taps) & 1))
-        r.fail("conv: filter tile has %d rows for %d reduction slots", a.kpad, p.rc * a.taps);
+    if (!bf16) {
+        // fp32 layout: S[rc][sc] then F[bm][fp]; a k-slot reads at most
+        // (channel) * T + T - 1 + fw (dead row-split slot) of a filter row and
+        // strip offset strip_len - 1 + fh of a channel strip
+        if (p.sc < p.strip_cap + g.fh || p.fp < p.rc * g.taps + g.fw + 1 ||
+            p.stage < p.rc * p.sc + p.bm * p.fp + g.fw || p.lds_bytes < 4 * 2 * p.stage)
+            r.fail("conv: fp32 LDS layout too small (sc %lld, fp %lld, %lld bytes)", (long long)p.sc,
+                   (long long)p.fp, (long long)p.lds_bytes);
+        if (p.split == 0 && (p.rc & 1))
+            r.fail("conv: channel split with an odd chunk of %d", p.rc);
+    }
     const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
     const int64_t y_elems = g.n * g.k * g.ho * g.wo;
     const int64_t ptiles = (g.npix + p.bn - 1) / p.bn;

@@ -31,13 +31,16 @@ struct alignas(16) U16x8 {
 template <bool FUSED>
 __device__ inline void stage_strips(uint16_t* S, const ConvArgs& a, const TileRuns& tr, int r0) {
     const uint16_t* src = static_cast<const uint16_t*>(a.src);
+    const int nseg = tr.nseg, i0 = tr.i0, len0 = tr.len0, len_mid = tr.len_mid,
+              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0;
     for (int grp = 0; grp < 2; ++grp) {
         const int rbase = r0 + 8 * grp;
-        for (int s = 0; s < tr.nseg; ++s) {
-            const int len = tr.seg_len(s);
-            const int i = tr.i0 + s;
-            const int ma = tr.seg_m(s), qa = tr.seg_q(s);
-            uint16_t* dst = S + (int64_t)tr.seg_off(s) * kRC + 8 * grp;
+        for (int s = 0; s < nseg; ++s) {
+            const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0);
+            const int len = sr.len;
+            const int i = i0 + s;
+            const int ma = sr.m, qa = sr.q;
+            uint16_t* dst = S + (int64_t)sr.off * kRC + 8 * grp;
             int e = threadIdx.x;
             if (e >= len) continue;
             if (!FUSED) {

@@ -11,7 +11,9 @@ namespace im2win {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kConvThreads = 256;            // 4 waves of 64 lanes
-constexpr int kConvLdsBudgetBytes = 64 * 1024;
+constexpr int kConvLdsBudgetBytes = 64 * 1024;    // preferred LDS per workgroup
+constexpr int kConvLdsMaxBytes = 160 * 1024;      // gfx950 LDS per workgroup
+constexpr int kConvLdsPipelinedBytes = 80 * 1024; // two double-buffered workgroups per CU
 
 struct ConvArgs {
     const void* src;   // window tensor (unfused) or input x (fused)
@@ -22,11 +24,17 @@ struct ConvArgs {
     int npix, howo;
     int rc;            // input channels per chunk
     int strip_cap;     // LDS strip positions reserved per channel
+    int sc;            // fp32: LDS stride between channel strips (floats)
+    int fp;            // fp32: LDS stride between filter rows (floats)
+    int bm;            // output channels per workgroup
+    int ksplit;        // fp32: 0 = k-slots split by channel halves, 1 = by filter rows
     int kpad;          // fp32: filter-tile rows, rc*taps rounded up to even
     int tc;            // bf16: filter taps staged per pass
     int num_jtiles;
     FastDiv div_wo, div_ho, div_kpad, div_taps, div_fw, div_row, div_fh, div_tc2;
     int d_row, d_k, d_u;   // kConvThreads = d_row*L + d_k*Fh + d_u (fused walk)
+    int e_row, e_k, e_u;   // 64 (one wave) = e_row*L + e_k*Fh + e_u (fused DMA walk)
+    int stage;             // fp32: LDS floats per pipeline stage
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -71,6 +79,22 @@ struct TileRuns {
     __host__ __device__ int seg_q(int s) const { return s == 0 ? qa0 : 0; }
 };
 
+// One run (image segment) of a tile, computed from values held in registers
+// (a select between struct fields would otherwise be turned into a load).
+struct SegRun {
+    int off, len, m, q;
+};
+
+__host__ __device__ inline SegRun seg_run(int s, int nseg, int len0, int len_mid, int len_last,
+                                          int m0, int qa0) {
+    SegRun r;
+    r.off = s == 0 ? 0 : len0 + (s - 1) * len_mid;
+    r.len = s == 0 ? len0 : (s == nseg - 1 ? len_last : len_mid);
+    r.m = s == 0 ? m0 : 0;
+    r.q = s == 0 ? qa0 : 0;
+    return r;
+}
+
 // Strip offset of the window of pixel p (its column in the implicit GEMM) and
 // the output offset of its channel-0 element.  Pixels past the end of the
 // tile are clamped to the first pixel of the tile (computed, never stored).
@@ -92,7 +116,10 @@ struct ConvPlan {
     int bm = 0, bn = 0;    // output channels x pixels per workgroup
     int rc = 0;            // input channels per LDS chunk
     int tc = 0;            // bf16: taps per filter pass
+    int split = 0;         // fp32: k-slot split (0 channel halves, 1 filter rows)
     int64_t strip_cap = 0; // LDS strip positions per channel
+    int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
+    int64_t stage = 0;       // fp32: LDS floats per pipeline stage
     int64_t lds_bytes = 0;
 };
 
@@ -134,6 +161,7 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.row_len = (int)g.row_len; a.used_len = (int)g.used_len; a.taps = (int)g.taps;
     a.npix = (int)g.npix; a.howo = (int)(g.ho * g.wo);
     a.rc = 1; a.strip_cap = 1; a.kpad = 2; a.tc = 1;
+    a.sc = 1; a.fp = 1; a.bm = bm; a.ksplit = 0;
     a.num_jtiles = (int)((g.k + bm - 1) / bm);
     a.div_wo = make_fastdiv((uint32_t)a.wo);
     a.div_ho = make_fastdiv((uint32_t)a.ho);
@@ -147,6 +175,10 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     const int rem = kConvThreads % a.row_len;
     a.d_k = rem / a.fh;
     a.d_u = rem % a.fh;
+    a.e_row = 64 / a.row_len;
+    a.e_k = (64 % a.row_len) / a.fh;
+    a.e_u = (64 % a.row_len) % a.fh;
+    a.stage = 0;
     return a;
 }
 

@@ -1,112 +1,240 @@
 // fp32 im2win convolution on gfx950 matrix cores (Alg. 2 semantics).
 //
 // The convolution is an implicit GEMM  Y[j][p] = sum_kk F[j][kk] * Win[kk][p]
-// over output channels j, output pixels p = (i, m, n) and the reduction index
-// kk = (r, t), t = v*Fh + u.  Because the window tensor stores each window as
-// the contiguous run [n*sw*Fh, n*sw*Fh + Fw*Fh) of row (i, r, m), the operand
-// Win[(r, t)][p] is  strip_r[base(p) + t]: horizontally adjacent windows
-// overlap inside one strip and are read from the same on-chip copy (the data
-// reuse the paper builds its loop order around, Sec. III-B).
+// over output channels j, output pixels p = (i, m, n) and reduction index
+// kk = (r, u, v).  The window tensor stores the window of pixel p, channel r
+// as the contiguous run [base(p), base(p) + Fw*Fh) of row (i, r, m), tap
+// (u, v) at offset v*Fh + u; horizontally adjacent windows overlap inside
+// one strip and are read from the same on-chip copy (the reuse the paper's
+// loop order is built around, Sec. III-B).
 //
 // Workgroup = 4 waves computing a BM (channels) x BN (pixels) tile of Y.
-// Pixels are tiled in flattened (i, m, n) order, so a tile covers a handful
-// of window-tensor rows, which for one channel are contiguous in memory
-// (one run per image).  Per chunk of `rc` input channels the workgroup:
-//   - copies those runs into LDS (unfused: from the window tensor; fused:
-//     builds them from x, zero padding included, never touching HBM for Win),
-//   - stages the filter chunk as F[kk][j] (kk in window order),
-//   - runs v_mfma_f32_32x32x2f32: A = filter rows (32 channels), B = window
-//     columns (32 pixels), so each accumulator register holds 32 consecutive
-//     pixels of one output channel and the NCHW stores are coalesced.
+// Pixels are tiled in flattened (i, m, n) order, so a tile reads a few
+// window-tensor rows, which for one channel are contiguous in memory (one run
+// per image).  Per chunk of input channels:
+//   - unfused: the runs and the filter rows are copied straight from global
+//     memory into LDS by the global_load_lds DMA path (no register round
+//     trip; a wave issues every copy of the chunk, then waits once);
+//   - fused: the strips are built in LDS from x, zero padding included
+//     (gathers batched eight per thread), the window tensor is never written;
+//   - v_mfma_f32_32x32x2f32 runs with A = filter rows (32 channels) and
+//     B = window columns (32 pixels); each accumulator register then holds 32
+//     consecutive pixels of one output channel, so NCHW stores coalesce.
+// The matrix core's two k-slots (lanes 0-31 / 32-63) take either the two
+// halves of the channel chunk or the top and bottom filter rows, whichever
+// pads the reduction less; either way the second half is the first shifted
+// by a constant, so with the filter size known at compile time every tap
+// offset is an immediate of the LDS read.
 #include "conv_common.h"
 
-#include <algorithm>
 #include <cstdio>
 
 namespace im2win {
 namespace {
 
-// Input elements are fp32, or bf16 bit patterns widened to fp32 when staged
-// (exact; the bf16 fallback path for problems whose channel-inner bf16 tiles
-// do not fit in LDS).
+// Input elements are fp32, or bf16 bit patterns widened to fp32 (exact) for
+// bf16 problems whose channel-inner tiles do not fit in LDS.
 __device__ inline float to_f32(float v) { return v; }
 __device__ inline float to_f32(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 
-// Copy (unfused) or build (fused) the strips of channels [r0, r0+rc_act).
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One wave copies `len` consecutive floats from global memory to LDS (DMA).
+__device__ inline void dma_run(const float* g, float* l, int len, int lane) {
+    for (int e0 = 0; e0 < len; e0 += 64) {
+        if (e0 + lane < len)
+            __builtin_amdgcn_global_load_lds(g + e0 + lane, (lds_void*)(l + e0), 4, 0, 0);
+    }
+}
+
+// Stage one channel chunk [r0, r0 + rc_act) of one tile into S (strips,
+// stride sc per channel) and F (filter rows, stride fp), issuing copies only:
+// fp32 data moves by DMA (global_load_lds) and lands while the previous chunk
+// is being multiplied; the caller's next barrier waits for it.
+//   F[jj][0 .. rc_act*T)   filter rows in natural (r, u, v) order
+//   S[rc][0 .. strip_len)  window-tensor runs (unfused), or the same strip
+//                          positions gathered from x, zero where they fall in
+//                          the padding (fused)
 template <typename TIn, bool FUSED>
-__device__ inline void stage_strips(float* S, const ConvArgs& a, const TileRuns& tr, int r0,
-                                    int rc_act) {
-    for (int rc = 0; rc < rc_act; ++rc) {
-        const int r = r0 + rc;
-        for (int s = 0; s < tr.nseg; ++s) {
-            const int len = tr.seg_len(s);
-            const int i = tr.i0 + s;
-            const int ma = tr.seg_m(s), qa = tr.seg_q(s);
-            float* dst = S + rc * a.strip_cap + tr.seg_off(s);
-            if (!FUSED) {
-                const TIn* src = static_cast<const TIn*>(a.src) +
-                                 (((int64_t)i * a.c + r) * a.ho + ma) * a.row_len + qa;
-                for (int e = threadIdx.x; e < len; e += kConvThreads) dst[e] = to_f32(src[e]);
-            } else {
-                const TIn* plane = static_cast<const TIn*>(a.src) +
-                                   ((int64_t)i * a.c + r) * a.h * a.w_in;
-                int e = threadIdx.x;
-                if (e >= len) continue;
-                const int pos = qa + e;
-                int row = (int)fast_div((uint32_t)pos, a.div_row);
-                const int q = pos - row * a.row_len;
-                int kcol = (int)fast_div((uint32_t)q, a.div_fh);
-                int u = q - kcol * a.fh;
-                for (; e < len; e += kConvThreads) {
-                    const int yy = (ma + row) * a.sh + u - a.ph;
-                    const int xx = kcol - a.pw;
-                    float v = 0.0f;
-                    if ((unsigned)yy < (unsigned)a.h && (unsigned)xx < (unsigned)a.w_in)
-                        v = to_f32(plane[(int64_t)yy * a.w_in + xx]);
-                    dst[e] = v;
-                    u += a.d_u;
-                    if (u >= a.fh) { u -= a.fh; ++kcol; }
-                    kcol += a.d_k;
-                    if (kcol >= a.wp) { kcol -= a.wp; ++row; }
-                    row += a.d_row;
+__device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRuns& tr, int j0,
+                             int r0, int rc_act, int rc_stage) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int kreal = rc_act * a.taps;
+    const int nrows_f = min(a.k - j0, a.bm);
+    constexpr bool kDma = sizeof(TIn) == 4;
+    {
+        const TIn* w = static_cast<const TIn*>(a.w);
+        for (int jj = wave; jj < nrows_f; jj += 4) {
+            const TIn* g = w + ((int64_t)(j0 + jj) * a.c + r0) * a.taps;
+            if (kDma)
+                dma_run(reinterpret_cast<const float*>(g), F + jj * a.fp, kreal, lane);
+            else
+                for (int e = lane; e < kreal; e += 64) F[jj * a.fp + e] = to_f32(g[e]);
+        }
+    }
+    // an odd last chunk under the channel split gets one zero channel
+    if (rc_stage > rc_act) {
+        for (int e = threadIdx.x; e < tr.strip_len; e += kConvThreads) S[rc_act * a.sc + e] = 0.0f;
+        for (int jj = wave; jj < a.bm; jj += 4)
+            for (int e = lane; e < a.taps; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
+    }
+    const TIn* src = static_cast<const TIn*>(a.src);
+    const int nseg = tr.nseg, i0 = tr.i0, len0 = tr.len0, len_mid = tr.len_mid,
+              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0;
+    const int nruns = rc_act * nseg;
+    for (int q = wave; q < nruns; q += 4) {
+        const int rc = q / nseg, s = q - rc * nseg;
+        const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0);
+        float* l = S + rc * a.sc + sr.off;
+        const int len = sr.len;
+        if (!FUSED) {
+            const TIn* g = src + (((int64_t)(i0 + s) * a.c + r0 + rc) * a.ho + sr.m) * a.row_len + sr.q;
+            if (kDma)
+                dma_run(reinterpret_cast<const float*>(g), l, len, lane);
+            else
+                for (int e = lane; e < len; e += 64) l[e] = to_f32(g[e]);
+        } else {
+            // strip position qa + e of this run is x[(ma + row)*sh + u - ph][k - pw]
+            // with (row, k, u) the mixed-radix digits of qa + e over (L, Fh);
+            // each lane walks its position in steps of one wave (64)
+            const TIn* plane = src + ((int64_t)(i0 + s) * a.c + r0 + rc) * a.h * a.w_in;
+            const int pos = sr.q + lane;
+            int row = (int)fast_div((uint32_t)pos, a.div_row);
+            const int qq = pos - row * a.row_len;
+            int kcol = (int)fast_div((uint32_t)qq, a.div_fh);
+            int u = qq - kcol * a.fh;
+            for (int e0 = 0; e0 < len; e0 += 64) {
+                const int e = e0 + lane;
+                const int yy = (sr.m + row) * a.sh + u - a.ph;
+                const int xx = kcol - a.pw;
+                const bool inb = (unsigned)yy < (unsigned)a.h && (unsigned)xx < (unsigned)a.w_in;
+                if (e < len) {
+                    if (!inb)
+                        l[e] = 0.0f;
+                    else if (kDma)
+                        __builtin_amdgcn_global_load_lds(
+                            reinterpret_cast<const float*>(plane) + (int64_t)yy * a.w_in + xx,
+                            (lds_void*)(l + e0), 4, 0, 0);
+                    else
+                        l[e] = to_f32(plane[(int64_t)yy * a.w_in + xx]);
                 }
+                u += a.e_u;
+                if (u >= a.fh) { u -= a.fh; ++kcol; }
+                kcol += a.e_k;
+                if (kcol >= a.wp) { kcol -= a.wp; ++row; }
+                row += a.e_row;
             }
         }
     }
 }
 
-// F[kk][j] for kk = (r - r0)*T + v*Fh + u, zero outside the real filter.
-template <typename TIn, int BM>
-__device__ inline void stage_filter(float* F, const ConvArgs& a, int j0, int r0, int rc_act) {
-    const int kreal = rc_act * a.taps;
-    for (int idx = threadIdx.x; idx < BM * a.kpad; idx += kConvThreads) {
-        const int jj = (int)fast_div((uint32_t)idx, a.div_kpad);
-        const int nat = idx - jj * a.kpad;          // natural (r, u, v) order within the chunk
-        const int j = j0 + jj;
-        int kk = nat;
-        float v = 0.0f;
-        if (nat < kreal && j < a.k) {
-            const int rl = (int)fast_div((uint32_t)nat, a.div_taps);
-            const int tt = nat - rl * a.taps;
-            const int u = (int)fast_div((uint32_t)tt, a.div_fw);
-            const int vv = tt - u * a.fw;
-            kk = rl * a.taps + vv * a.fh + u;
-            v = to_f32(static_cast<const TIn*>(a.w)[((int64_t)j * a.c + r0) * a.taps + nat]);
+template <int NJ, int NP>
+__device__ inline void mfma_step(f32x16 (&acc)[NJ][NP], const float* F, const float* S,
+                                 const int (&fl)[NJ], const int (&sl)[NP], int fo, int so,
+                                 bool dead) {
+    float av[NJ], bv[NP];
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) av[jb] = F[fl[jb] + fo];
+#pragma unroll
+    for (int pb = 0; pb < NP; ++pb) bv[pb] = S[sl[pb] + so];
+    if (dead) {
+#pragma unroll
+        for (int jb = 0; jb < NJ; ++jb) av[jb] = 0.0f;
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb) bv[pb] = 0.0f;
+    }
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb)
+            acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
+}
+
+// Operands of one filter row u of one channel iteration (FW taps) in registers.
+template <int FW, int NJ, int NP>
+struct RowRegs {
+    float a[NJ][FW];
+    float b[NP][FW];
+};
+
+// MFMA over one staged chunk: `iters` channels per k-slot.  FH, FW > 0 fix
+// the filter size at compile time (tap offsets become immediates).  The
+// reduction is walked in groups of one filter row (FW taps); the operands of
+// the next group are read from LDS into a second register set before the
+// matrix-core instructions of the current group are issued, so LDS latency is
+// hidden behind the MFMAs of the same wave.  ROWS: the k-slots are split by
+// filter rows (the second k-slot has no row left when Fh is odd: zeroed).
+template <int FH, int FW, bool ROWS, int NJ, int NP>
+__device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, const float* S,
+                                     const ConvArgs& a, const int (&fl)[NJ], const int (&sl)[NP],
+                                     int kl, int iters) {
+    if constexpr (FH > 0 && FW > 0) {
+        constexpr int T = FH * FW, U0 = (FH + 1) / 2;
+        constexpr int UEND = ROWS ? U0 : FH;
+        const int ng = iters * UEND;
+        const int sc = a.sc;
+        RowRegs<FW, NJ, NP> r0, r1;
+        auto load = [&](RowRegs<FW, NJ, NP>& r, int g) {
+            const int it = g / UEND, u = g - it * UEND;
+            const int fo = it * T + u * FW, so = it * sc + u;
+#pragma unroll
+            for (int v = 0; v < FW; ++v) {
+#pragma unroll
+                for (int jb = 0; jb < NJ; ++jb) r.a[jb][v] = F[fl[jb] + fo + v];
+#pragma unroll
+                for (int pb = 0; pb < NP; ++pb) r.b[pb][v] = S[sl[pb] + so + v * FH];
+            }
+        };
+        auto mma = [&](RowRegs<FW, NJ, NP>& r, int g) {
+            bool dead = false;
+            if constexpr (ROWS && (FH & 1)) dead = kl && (g % UEND == UEND - 1);
+#pragma unroll
+            for (int v = 0; v < FW; ++v) {
+                float av[NJ], bv[NP];
+#pragma unroll
+                for (int jb = 0; jb < NJ; ++jb) av[jb] = dead ? 0.0f : r.a[jb][v];
+#pragma unroll
+                for (int pb = 0; pb < NP; ++pb) bv[pb] = dead ? 0.0f : r.b[pb][v];
+#pragma unroll
+                for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+                    for (int pb = 0; pb < NP; ++pb)
+                        acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
+            }
+        };
+        if (ng <= 0) return;
+        load(r0, 0);
+        int g = 0;
+        for (; g + 2 <= ng; g += 2) {
+            load(r1, g + 1);
+            mma(r0, g);
+            if (g + 2 < ng) load(r0, g + 2);
+            mma(r1, g + 1);
         }
-        F[kk * (BM + 1) + jj] = v;
+        if (g < ng) mma(r0, g);
+    } else {
+        const int fh = a.fh, fw = a.fw, T = fh * fw, u0 = (fh + 1) >> 1;
+        const int uend = ROWS ? u0 : fh;
+        for (int it = 0; it < iters; ++it) {
+            const int fo = it * T, so = it * a.sc;
+            for (int u = 0; u < uend; ++u) {
+                const bool dead = ROWS && kl && (u + u0 >= fh);
+                for (int v = 0; v < fw; ++v)
+                    mfma_step<NJ, NP>(acc, F, S, fl, sl, fo + u * fw + v, so + v * fh + u, dead);
+            }
+        }
     }
 }
 
-template <typename TIn, int BM, int BN, int TJ, int TP, bool FUSED>
+template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, bool FUSED>
 __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    float* S = reinterpret_cast<float*>(smem);
-    float* F = S + a.rc * a.strip_cap;
-    float* Z = F + a.kpad * (BM + 1);   // one zero word for padded reduction slots
+    float* S = reinterpret_cast<float*>(smem);   // stage s: S + s*stage, F + s*stage
+    float* F = S + a.rc * a.sc;
 
     const int jtile = blockIdx.x % a.num_jtiles;
     const int ptile = blockIdx.x / a.num_jtiles;
@@ -120,8 +248,14 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     const int wj = wave / WAVES_P, wp_ = wave % WAVES_P;
     const int l32 = lane & 31, kl = lane >> 5;
 
-    // Per-lane pixel columns: strip offset of the window start and output offset.
-    int pbase[NP];
+    // Per-lane LDS bases.  The second k-slot (kl = 1) is the first shifted by
+    // half a channel chunk, or by the top half of the filter rows.
+    const int fh = FH > 0 ? FH : a.fh, fw = FW > 0 ? FW : a.fw;
+    const int u0 = (fh + 1) >> 1;
+    const int half_full = a.rc >> 1;
+    const int df = ROWS ? u0 * fw : half_full * fh * fw;
+    const int ds = ROWS ? u0 : half_full * a.sc;
+    int sl[NP];
     int64_t yoff[NP];
     bool pvalid[NP];
 #pragma unroll
@@ -129,11 +263,11 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         int p = tr.p0 + wp_ * TP + pb * 32 + l32;
         pvalid[pb] = p <= tr.plast;
         if (!pvalid[pb]) p = tr.p0;
-        pbase[pb] = pixel_base(tr, a, p, &yoff[pb]);
+        sl[pb] = pixel_base(tr, a, p, &yoff[pb]) + kl * ds;
     }
-    int jrow[NJ];
+    int fl[NJ];
 #pragma unroll
-    for (int jb = 0; jb < NJ; ++jb) jrow[jb] = wj * TJ + jb * 32 + l32;
+    for (int jb = 0; jb < NJ; ++jb) fl[jb] = (wj * TJ + jb * 32 + l32) * a.fp + kl * df;
 
     f32x16 acc[NJ][NP];
 #pragma unroll
@@ -143,35 +277,42 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
 
-    if (threadIdx.x == 0) Z[0] = 0.0f;
-    const int zero_off = (int)(Z - S);
-
-    for (int r0 = 0; r0 < a.c; r0 += a.rc) {
+    // Two LDS stages: while chunk c is multiplied out of one, the copies of
+    // chunk c+1 land in the other.  One barrier per chunk: it waits for the
+    // copies of chunk c (vmcnt 0 in every wave) and for every wave to be done
+    // with chunk c-1, whose stage the copies of chunk c+1 then overwrite.
+    const int nchunks = (a.c + a.rc - 1) / a.rc;
+    {
+        const int rc_act = min(a.rc, a.c);
+        stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, ROWS ? rc_act : ((rc_act + 1) & ~1));
+    }
+    for (int ch = 0; ch < nchunks; ++ch) {
+        const int r0 = ch * a.rc;
         const int rc_act = min(a.rc, a.c - r0);
+        const int rc_stage = ROWS ? rc_act : ((rc_act + 1) & ~1);
+        const float* Sc = S + (ch & 1) * a.stage;
+        const float* Fc = F + (ch & 1) * a.stage;
         __syncthreads();
-        stage_strips<TIn, FUSED>(S, a, tr, r0, rc_act);
-        stage_filter<TIn, BM>(F, a, j0, r0, rc_act);
-        __syncthreads();
-
-        const int kreal = rc_act * a.taps;
-        const int ksteps = (kreal + 1) >> 1;
-        int rck = 0, tk = kl;
-        while (tk >= a.taps) { tk -= a.taps; ++rck; }
-        for (int s = 0; s < ksteps; ++s) {
-            const int kk = 2 * s + kl;
-            const int koff = rck * a.strip_cap + tk;
-            float av[NJ], bv[NP];
+        if (ch + 1 < nchunks) {
+            const int r1 = r0 + a.rc;
+            const int rc1 = min(a.rc, a.c - r1);
+            const int off = ((ch + 1) & 1) * a.stage;
+            stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, ROWS ? rc1 : ((rc1 + 1) & ~1));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (ROWS) {
+            compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act);
+        } else if (rc_stage == a.rc) {
+            compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full);
+        } else {
+            // short last chunk: its second half starts at rc_stage/2
+            const int half = rc_stage >> 1;
+            int fl2[NJ], sl2[NP];
 #pragma unroll
-            for (int jb = 0; jb < NJ; ++jb) av[jb] = F[kk * (BM + 1) + jrow[jb]];
+            for (int jb = 0; jb < NJ; ++jb) fl2[jb] = fl[jb] + kl * (half - half_full) * fh * fw;
 #pragma unroll
-            for (int pb = 0; pb < NP; ++pb) bv[pb] = S[kk < kreal ? pbase[pb] + koff : zero_off];
-#pragma unroll
-            for (int jb = 0; jb < NJ; ++jb)
-#pragma unroll
-                for (int pb = 0; pb < NP; ++pb)
-                    acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
-            tk += 2;
-            while (tk >= a.taps) { tk -= a.taps; ++rck; }
+            for (int pb = 0; pb < NP; ++pb) sl2[pb] = sl[pb] + kl * (half - half_full) * a.sc;
+            compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl2, sl2, kl, half);
         }
     }
 
@@ -189,52 +330,89 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         }
 }
 
-template <typename TIn, int BM, int BN, int TJ, int TP>
+template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP>
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipStream_t stream) {
-    if (fused)
-        hipLaunchKernelGGL((conv_f32_kernel<TIn, BM, BN, TJ, TP, true>), dim3((unsigned)blocks),
-                           dim3(kConvThreads), (size_t)lds, stream, a);
-    else
-        hipLaunchKernelGGL((conv_f32_kernel<TIn, BM, BN, TJ, TP, false>), dim3((unsigned)blocks),
-                           dim3(kConvThreads), (size_t)lds, stream, a);
+    auto kern = fused ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, true>
+                      : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, false>;
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
 }
 
-template <typename TIn>
-void launch_plan(const ConvPlan& p, const ConvArgs& a, int64_t blocks, bool fused,
+template <typename TIn, int FH, int FW, bool ROWS>
+void launch_tile_split(const ConvPlan& p, const ConvArgs& a, int64_t blocks, bool fused,
+                       hipStream_t stream) {
+    if (p.bm == 64 && p.bn == 256) launch_cfg<TIn, FH, FW, ROWS, 64, 256, 64, 64>(a, blocks, p.lds_bytes, fused, stream);
+    else if (p.bm == 128) launch_cfg<TIn, FH, FW, ROWS, 128, 128, 64, 64>(a, blocks, p.lds_bytes, fused, stream);
+    else if (p.bn == 128) launch_cfg<TIn, FH, FW, ROWS, 64, 128, 32, 64>(a, blocks, p.lds_bytes, fused, stream);
+    else launch_cfg<TIn, FH, FW, ROWS, 64, 64, 32, 32>(a, blocks, p.lds_bytes, fused, stream);
+}
+
+template <typename TIn, int FH, int FW>
+void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, bool fused,
                  hipStream_t stream) {
-    if (p.bm == 64 && p.bn == 256) launch_cfg<TIn, 64, 256, 64, 64>(a, blocks, p.lds_bytes, fused, stream);
-    else if (p.bm == 128) launch_cfg<TIn, 128, 128, 64, 64>(a, blocks, p.lds_bytes, fused, stream);
-    else if (p.bn == 128) launch_cfg<TIn, 64, 128, 32, 64>(a, blocks, p.lds_bytes, fused, stream);
-    else launch_cfg<TIn, 64, 64, 32, 32>(a, blocks, p.lds_bytes, fused, stream);
+    if (p.split) launch_tile_split<TIn, FH, FW, true>(p, a, blocks, fused, stream);
+    else launch_tile_split<TIn, FH, FW, false>(p, a, blocks, fused, stream);
 }
 
-int64_t lds_bytes_f32(int bm, int rc, int64_t taps, int64_t strip_cap) {
-    const int64_t kpad = (rc * taps + 1) & ~int64_t(1);
-    return ((int64_t)rc * strip_cap + kpad * (bm + 1) + 4) * 4;
+// LDS of one workgroup: two pipeline stages, each holding the strips of rc
+// channels (stride sc) and bm filter rows (stride fp, odd so that 32
+// consecutive rows fall in different banks), with slack for the reads past
+// the last tap that a dead k-slot makes.
+int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, int64_t* sc, int64_t* fp,
+                   int64_t* stage) {
+    *sc = (cap + g.fh + 3) & ~int64_t(3);
+    *fp = (int64_t)rc * g.taps + g.fw + 1;
+    if ((*fp & 1) == 0) ++*fp;
+    *stage = ((int64_t)rc * *sc + (int64_t)bm * *fp + g.fw + 4 + 3) & ~int64_t(3);
+    return 2 * *stage * 4;
+}
+
+// Zero reduction slots each way of splitting the two k-slots adds: one zero
+// channel in total (odd C, channel halves) or one zero filter row per channel
+// (odd Fh, row halves).
+int choose_split(const Geometry& g) {
+    const int64_t chan = (g.c & 1) ? g.taps : 0;
+    const int64_t rows = (g.fh & 1) ? g.c * g.fw : 0;
+    return rows < chan ? 1 : 0;
 }
 
 }  // namespace
 
-// Tile candidates, preferred first; the first whose LDS fits is used, with
-// the largest channel chunk that fits.  The window strips and the filter tile
-// are held in fp32 whatever the input type.
 ConvPlan plan_conv_f32(const Geometry& g) {
-    const TileCfg cfgs_small_k[] = {{64, 256}, {64, 128}, {64, 64}};
-    const TileCfg cfgs_large_k[] = {{128, 128}, {64, 128}, {64, 64}};
-    const TileCfg* cfgs = g.k <= 64 ? cfgs_small_k : cfgs_large_k;
-    ConvPlan p;
-    for (int ci = 0; ci < 3; ++ci) {
-        const int64_t cap = strip_bound(g, cfgs[ci].bn);
-        for (int rc = 1; rc <= std::min<int64_t>(g.c, 32); ++rc) {
-            const int64_t lds = lds_bytes_f32(cfgs[ci].bm, rc, g.taps, cap);
-            if (lds > kConvLdsBudgetBytes) break;
-            p.kind = ConvPlan::kF32Lds;
-            p.bm = cfgs[ci].bm; p.bn = cfgs[ci].bn; p.rc = rc; p.tc = (int)g.taps;
-            p.strip_cap = cap; p.lds_bytes = lds;
+    // Tiles in order of preference; the first that gives every CU two
+    // workgroups is taken, else the one with the most workgroups.  Both
+    // pipeline stages together are sized for 80 KB of LDS (two workgroups per
+    // CU); only shapes that fit nothing there use up to the full 160 KB.
+    const TileCfg small_k[] = {{64, 256}, {64, 128}, {64, 64}};
+    const TileCfg large_k[] = {{128, 128}, {64, 128}, {64, 64}};
+    const TileCfg* cfgs = g.k <= 64 ? small_k : large_k;
+    const int split = choose_split(g);
+    const int step = split ? 1 : 2;
+    const int64_t rc_max = std::min<int64_t>(split ? g.c : ((g.c + 1) & ~int64_t(1)), 32);
+    for (const int64_t budget : {int64_t(kConvLdsPipelinedBytes), int64_t(kConvLdsMaxBytes)}) {
+        ConvPlan best;
+        int64_t best_blocks = 0;
+        for (int ci = 0; ci < 3; ++ci) {
+            const TileCfg t = cfgs[ci];
+            const int64_t cap = strip_bound(g, t.bn);
+            ConvPlan p;
+            for (int rc = step; rc <= rc_max; rc += step) {
+                int64_t sc, fp, st;
+                const int64_t lds = f32_layout(g, t.bm, rc, cap, &sc, &fp, &st);
+                if (lds > budget) break;
+                p.kind = ConvPlan::kF32Lds;
+                p.bm = t.bm; p.bn = t.bn; p.rc = rc; p.tc = (int)g.taps; p.split = split;
+                p.strip_cap = cap; p.sc = sc; p.fp = fp; p.stage = st; p.lds_bytes = lds;
+            }
+            if (p.kind == ConvPlan::kNone) continue;
+            const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
+            if (blocks >= 2 * 256) return p;
+            if (blocks > best_blocks) { best = p; best_blocks = blocks; }
         }
-        if (p.rc > 0) break;
+        if (best.kind != ConvPlan::kNone) return best;
     }
-    return p;
+    return ConvPlan();
 }
 
 ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
@@ -242,8 +420,10 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     ConvArgs a = make_conv_args(g, src, w, y, p.bm);
     a.rc = p.rc;
     a.strip_cap = (int)p.strip_cap;
-    a.kpad = (p.rc * a.taps + 1) & ~1;
-    a.div_kpad = make_fastdiv((uint32_t)a.kpad);
+    a.sc = (int)p.sc;
+    a.fp = (int)p.fp;
+    a.stage = (int)p.stage;
+    a.ksplit = p.split;
     return a;
 }
 
@@ -255,15 +435,19 @@ int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const
         snprintf(err, errlen, "conv: grid of %lld workgroups is too large", (long long)blocks);
         return -5;
     }
-    if (g.elem == 4) launch_plan<float>(p, a, blocks, fused, stream);
-    else launch_plan<uint16_t>(p, a, blocks, fused, stream);
+    if (g.elem == 2) launch_tile<uint16_t, 0, 0>(p, a, blocks, fused, stream);
+    else if (g.fh == 3 && g.fw == 3) launch_tile<float, 3, 3>(p, a, blocks, fused, stream);
+    else if (g.fh == 3 && g.fw == 5) launch_tile<float, 3, 5>(p, a, blocks, fused, stream);
+    else if (g.fh == 7 && g.fw == 7) launch_tile<float, 7, 7>(p, a, blocks, fused, stream);
+    else if (g.fh == 1 && g.fw == 1) launch_tile<float, 1, 1>(p, a, blocks, fused, stream);
+    else launch_tile<float, 0, 0>(p, a, blocks, fused, stream);
     return 0;
 }
 
 int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, float* y,
                     hipStream_t stream, char* err, size_t errlen) {
     const ConvPlan p = plan_conv_f32(g);
-    if (p.rc == 0) {
+    if (p.kind == ConvPlan::kNone) {
         snprintf(err, errlen,
                  "conv: the window strips of one tile (row length %lld) do not fit in LDS; "
                  "this shape is not supported", (long long)g.row_len);
