@@ -83,69 +83,61 @@ void check_transform(const Geometry& g, Report& r) {
                (long long)ws_elems);
 }
 
-void check_conv(const Geometry& g, Report& r) {
-    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g) : plan_conv_f32(g);
-    if (p.kind == ConvPlan::kNone) {
-        r.fail("conv: no tile configuration fits in LDS (the launch would be refused)");
-        return;
-    }
+void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report& r) {
     const bool bf16 = p.kind == ConvPlan::kBf16Lds;
     const ConvArgs a = bf16 ? conv_args_bf16(g, p, nullptr, nullptr, nullptr)
-                            : conv_args_f32(g, p, nullptr, nullptr, nullptr);
-    if (p.lds_bytes > kConvLdsMaxBytes)
-        r.fail("conv: plan uses %lld bytes of LDS", (long long)p.lds_bytes);
-    if (!bf16) {
-        // fp32 layout: S[rc][sc] then F[bm][fp]; a k-slot reads at most
-        // (channel) * T + T - 1 + fw (dead row-split slot) of a filter row and
-        // strip offset strip_len - 1 + fh of a channel strip
-        if (p.sc < p.strip_cap + g.fh || p.fp < p.rc * g.taps + g.fw + 1 ||
-            p.stage < p.rc * p.sc + p.bm * p.fp + g.fw || p.lds_bytes < 4 * 2 * p.stage)
-            r.fail("conv: fp32 LDS layout too small (sc %lld, fp %lld, %lld bytes)", (long long)p.sc,
-                   (long long)p.fp, (long long)p.lds_bytes);
-        if (p.split == 0 && (p.rc & 1))
-            r.fail("conv: channel split with an odd chunk of %d", p.rc);
-    }
+                            : conv_args_f32(g, p, nullptr, nullptr, nullptr, fused);
+    const char* what = fused ? "fused conv" : "conv";
     const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
+    const int64_t plane = g.ho * g.row_len;
     const int64_t y_elems = g.n * g.k * g.ho * g.wo;
     const int64_t ptiles = (g.npix + p.bn - 1) / p.bn;
     int64_t covered = 0;
     for (int64_t t = 0; t < ptiles && r.violations < 16; ++t) {
         TileRuns tr;
         tr.init((int)t, p.bn, a);
-        if (tr.strip_len > p.strip_cap || tr.strip_len < 1)
-            r.fail("conv tile %lld: strip of %d positions, LDS holds %lld", (long long)t,
-                   tr.strip_len, (long long)p.strip_cap);
-        int sum = 0;
+        if (tr.extent > p.strip_cap || tr.strip_len < 1)
+            r.fail("%s tile %lld: strip of %d positions, LDS holds %lld", what, (long long)t,
+                   tr.extent, (long long)p.strip_cap);
+        int prev_end = 0;
         for (int s = 0; s < tr.nseg; ++s) {
             const int len = tr.seg_len(s);
-            if (len < 1 || tr.seg_off(s) != sum)
-                r.fail("conv tile %lld: segment %d has length %d at offset %d (expected %d)",
-                       (long long)t, s, len, tr.seg_off(s), sum);
-            sum += len;
-            // unfused source run of every channel
+            const int off = tr.seg_off(s);
+            if (len < 1 || off < prev_end || off + len > tr.extent)
+                r.fail("%s tile %lld: run %d [%d, %d) overlaps or leaves the strip of %d", what,
+                       (long long)t, s, off, off + len, tr.extent);
+            prev_end = off + len;
+            // window-tensor source of the run, for the first and the last channel
             const int64_t first = (((int64_t)(tr.i0 + s) * g.c + 0) * g.ho + tr.seg_m(s)) * g.row_len + tr.seg_q(s);
             const int64_t last = (((int64_t)(tr.i0 + s) * g.c + g.c - 1) * g.ho + tr.seg_m(s)) * g.row_len + tr.seg_q(s) + len;
             if (first < 0 || last > ws_elems)
-                r.fail("conv tile %lld: segment %d reads window tensor [%lld, %lld) of %lld",
+                r.fail("%s tile %lld: run %d reads window tensor [%lld, %lld) of %lld", what,
                        (long long)t, s, (long long)first, (long long)last, (long long)ws_elems);
-            // a run must stay inside its plane
-            if ((int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s) + len > g.ho * g.row_len)
-                r.fail("conv tile %lld: segment %d runs past its plane", (long long)t, s);
+            if ((int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s) + len > plane)
+                r.fail("%s tile %lld: run %d runs past its plane", what, (long long)t, s);
+            if (a.svec) {
+                // 16-byte copies: aligned start and rounded end stay in the plane,
+                // and the chunks of run s are the LDS chunks [off/4 - shift, ...)
+                const int64_t in_plane = (int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s);
+                const int shift = s == 0 ? tr.shift0 : 0;
+                if ((in_plane & 3) != shift || (plane & 3) != 0 ||
+                    ((in_plane - shift + 4 * (int64_t)((shift + len + 3) / 4)) > plane) ||
+                    ((off - shift) & 3) != 0)
+                    r.fail("%s tile %lld: 16-byte run %d misplaced (shift %d)", what, (long long)t, s, shift);
+            }
         }
-        if (sum != tr.strip_len)
-            r.fail("conv tile %lld: segments cover %d of %d positions", (long long)t, sum, tr.strip_len);
         for (int q = 0; q < p.bn; ++q) {
             int px = tr.p0 + q;
             const bool valid = px <= tr.plast;
             if (!valid) px = tr.p0;
             int64_t yoff;
             const int base = pixel_base(tr, a, px, &yoff);
-            // the window must lie inside its own segment of the strip
+            // the window must lie inside its own run of the strip
             const int gi = px / (int)g.wo, ii = gi / (int)g.ho;
             const int s = ii - tr.i0;
             if (s < 0 || s >= tr.nseg || base < tr.seg_off(s) ||
                 base + (int)g.taps > tr.seg_off(s) + tr.seg_len(s)) {
-                r.fail("conv tile %lld: pixel %d window [%d, %d) outside segment %d", (long long)t,
+                r.fail("%s tile %lld: pixel %d window [%d, %d) outside run %d", what, (long long)t,
                        px, base, base + (int)g.taps, s);
                 break;
             }
@@ -154,13 +146,38 @@ void check_conv(const Geometry& g, Report& r) {
                 const int mm = gi - ii * (int)g.ho, nn = px - gi * (int)g.wo;
                 if (yoff != (int64_t)ii * g.k * g.ho * g.wo + (int64_t)mm * g.wo + nn ||
                     yoff + (g.k - 1) * g.ho * g.wo >= y_elems)
-                    r.fail("conv tile %lld: pixel %d output offset %lld", (long long)t, px,
+                    r.fail("%s tile %lld: pixel %d output offset %lld", what, (long long)t, px,
                            (long long)yoff);
             }
         }
     }
     if (r.violations == 0 && covered != g.npix)
-        r.fail("conv: tiles cover %lld of %lld pixels", (long long)covered, (long long)g.npix);
+        r.fail("%s: tiles cover %lld of %lld pixels", what, (long long)covered, (long long)g.npix);
+}
+
+void check_conv(const Geometry& g, Report& r) {
+    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g) : plan_conv_f32(g);
+    if (p.kind == ConvPlan::kNone) {
+        r.fail("conv: no tile configuration fits in LDS (the launch would be refused)");
+        return;
+    }
+    const bool bf16 = p.kind == ConvPlan::kBf16Lds;
+    if (p.lds_bytes > kConvLdsMaxBytes)
+        r.fail("conv: plan uses %lld bytes of LDS", (long long)p.lds_bytes);
+    if (!bf16) {
+        // fp32 layout: two stages of S[rc][sc] then F[bm][fp]; a k-slot reads
+        // at most T + fw past a channel's first tap of a filter row (dead
+        // row-split slot) and fh past the last strip position
+        if (p.sc < p.strip_cap + g.fh || p.fp < p.rc * g.taps + g.fw + 1 ||
+            p.stage < p.rc * p.sc + p.bm * p.fp + g.fw || p.lds_bytes < 4 * 2 * p.stage ||
+            (p.sc & 3) != 0 || (p.stage & 3) != 0)
+            r.fail("conv: fp32 LDS layout too small (sc %lld, fp %lld, %lld bytes)", (long long)p.sc,
+                   (long long)p.fp, (long long)p.lds_bytes);
+        if (p.split == 0 && (p.rc & 1))
+            r.fail("conv: channel split with an odd chunk of %d", p.rc);
+    }
+    check_conv_variant(g, p, false, r);
+    if (!bf16 && p.svec) check_conv_variant(g, p, true, r);
 }
 
 }  // namespace

@@ -32,11 +32,12 @@ template <bool FUSED>
 __device__ inline void stage_strips(uint16_t* S, const ConvArgs& a, const TileRuns& tr, int r0) {
     const uint16_t* src = static_cast<const uint16_t*>(a.src);
     const int nseg = tr.nseg, i0 = tr.i0, len0 = tr.len0, len_mid = tr.len_mid,
-              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0;
+              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0, d_first = tr.d_first,
+              d_second = tr.d_second, d_stride = tr.d_stride;
     for (int grp = 0; grp < 2; ++grp) {
         const int rbase = r0 + 8 * grp;
         for (int s = 0; s < nseg; ++s) {
-            const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0);
+            const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0, d_first, d_second, d_stride);
             const int len = sr.len;
             const int i = i0 + s;
             const int ma = sr.m, qa = sr.q;

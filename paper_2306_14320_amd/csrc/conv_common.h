@@ -35,6 +35,8 @@ struct ConvArgs {
     int d_row, d_k, d_u;   // kConvThreads = d_row*L + d_k*Fh + d_u (fused walk)
     int e_row, e_k, e_u;   // 64 (one wave) = e_row*L + e_k*Fh + e_u (fused DMA walk)
     int stage;             // fp32: LDS floats per pipeline stage
+    int svec;              // fp32 unfused: strips staged by 16-byte copies (plane % 4 == 0)
+    FastDiv div_fp, div_ckmid;
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -45,6 +47,12 @@ struct TileRuns {
     int nseg;           // images touched
     int qa0;            // first run starts at this column of row m0
     int len0, len_mid, len_last, strip_len;
+    // LDS placement of the runs.  Plain layout: run s starts at seg_off(s),
+    // runs back to back.  16-byte layout (a.svec): every run starts on a
+    // 16-byte boundary and run 0 is shifted by its global misalignment
+    // shift0, so that 16-byte copies land aligned; ck* count 16-byte chunks.
+    int shift0, ck0, ck_mid, ck_last, ck_total;
+    int d_first, d_second, d_stride, extent;   // data start of run 0, of run 1, run pitch, LDS floats used
 
     __host__ __device__ void init(int ptile, int bn, const ConvArgs& a) {
         p0 = ptile * bn;
@@ -70,8 +78,29 @@ struct TileRuns {
             len_last = m1 * a.row_len + qb_last;
             strip_len = len0 + (nseg - 2) * len_mid + len_last;
         }
+        if (a.svec) {
+            shift0 = (m0 * a.row_len + qa0) & 3;
+            ck0 = (shift0 + len0 + 3) >> 2;
+            ck_mid = (len_mid + 3) >> 2;
+            ck_last = (len_last + 3) >> 2;
+            ck_total = nseg == 1 ? ck0 : ck0 + (nseg - 2) * ck_mid + ck_last;
+            d_first = shift0;
+            d_second = 4 * ck0;
+            d_stride = 4 * ck_mid;
+            extent = 4 * ck_total;
+        } else {
+            shift0 = 0;
+            ck0 = ck_mid = ck_last = ck_total = 0;
+            d_first = 0;
+            d_second = len0;
+            d_stride = len_mid;
+            extent = strip_len;
+        }
     }
-    __host__ __device__ int seg_off(int s) const { return s == 0 ? 0 : len0 + (s - 1) * len_mid; }
+    // LDS offset of the first element of run s
+    __host__ __device__ int seg_off(int s) const {
+        return s == 0 ? d_first : d_second + (s - 1) * d_stride;
+    }
     __host__ __device__ int seg_len(int s) const {
         return s == 0 ? len0 : (s == nseg - 1 ? len_last : len_mid);
     }
@@ -86,9 +115,10 @@ struct SegRun {
 };
 
 __host__ __device__ inline SegRun seg_run(int s, int nseg, int len0, int len_mid, int len_last,
-                                          int m0, int qa0) {
+                                          int m0, int qa0, int d_first, int d_second,
+                                          int d_stride) {
     SegRun r;
-    r.off = s == 0 ? 0 : len0 + (s - 1) * len_mid;
+    r.off = s == 0 ? d_first : d_second + (s - 1) * d_stride;
     r.len = s == 0 ? len0 : (s == nseg - 1 ? len_last : len_mid);
     r.m = s == 0 ? m0 : 0;
     r.q = s == 0 ? qa0 : 0;
@@ -120,13 +150,14 @@ struct ConvPlan {
     int64_t strip_cap = 0; // LDS strip positions per channel
     int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
     int64_t stage = 0;       // fp32: LDS floats per pipeline stage
+    int svec = 0;            // fp32 unfused: 16-byte strip copies
     int64_t lds_bytes = 0;
 };
 
 ConvPlan plan_conv_f32(const Geometry& g);
 ConvPlan plan_conv_bf16(const Geometry& g);
 ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
-                       float* y);
+                       float* y, bool fused);
 ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
                         float* y);
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
@@ -179,6 +210,9 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.e_k = (64 % a.row_len) / a.fh;
     a.e_u = (64 % a.row_len) % a.fh;
     a.stage = 0;
+    a.svec = 0;
+    a.div_fp = make_fastdiv(1);
+    a.div_ckmid = make_fastdiv(1);
     return a;
 }
 

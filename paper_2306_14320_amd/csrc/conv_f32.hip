@@ -62,29 +62,67 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
     const int kreal = rc_act * a.taps;
     const int nrows_f = min(a.k - j0, a.bm);
     constexpr bool kDma = sizeof(TIn) == 4;
-    {
+    if (kDma) {
+        // one DMA instruction fills 64 consecutive LDS floats of the row-major
+        // tile (rows of stride fp), lane by lane from the matching filter row
+        const float* w = static_cast<const float*>(a.w) + ((int64_t)j0 * a.c + r0) * a.taps;
+        const int64_t wrow = (int64_t)a.c * a.taps;
+        const int total = nrows_f * a.fp;
+        for (int e0 = wave * 64; e0 < total; e0 += kConvThreads) {
+            const int e = e0 + lane;
+            const int jj = (int)fast_div((uint32_t)e, a.div_fp);
+            const int col = e - jj * a.fp;
+            if (e < total && col < kreal)
+                __builtin_amdgcn_global_load_lds(w + jj * wrow + col, (lds_void*)(F + e0), 4, 0, 0);
+        }
+    } else {
         const TIn* w = static_cast<const TIn*>(a.w);
         for (int jj = wave; jj < nrows_f; jj += 4) {
             const TIn* g = w + ((int64_t)(j0 + jj) * a.c + r0) * a.taps;
-            if (kDma)
-                dma_run(reinterpret_cast<const float*>(g), F + jj * a.fp, kreal, lane);
-            else
-                for (int e = lane; e < kreal; e += 64) F[jj * a.fp + e] = to_f32(g[e]);
+            for (int e = lane; e < kreal; e += 64) F[jj * a.fp + e] = to_f32(g[e]);
         }
     }
     // an odd last chunk under the channel split gets one zero channel
     if (rc_stage > rc_act) {
-        for (int e = threadIdx.x; e < tr.strip_len; e += kConvThreads) S[rc_act * a.sc + e] = 0.0f;
+        for (int e = threadIdx.x; e < tr.extent; e += kConvThreads) S[rc_act * a.sc + e] = 0.0f;
         for (int jj = wave; jj < a.bm; jj += 4)
             for (int e = lane; e < a.taps; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
     }
     const TIn* src = static_cast<const TIn*>(a.src);
     const int nseg = tr.nseg, i0 = tr.i0, len0 = tr.len0, len_mid = tr.len_mid,
-              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0;
+              len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0, d_first = tr.d_first,
+              d_second = tr.d_second, d_stride = tr.d_stride;
+    if (!FUSED && kDma && a.svec) {
+        // 16-byte copies: channel rc's runs fill ck_total consecutive 16-byte
+        // chunks of its strip; chunk c belongs to run s and reads from that
+        // run's 16-byte-aligned start.  Window-tensor planes are multiples of
+        // four elements, so no chunk leaves its plane.
+        const float* srcf = reinterpret_cast<const float*>(src);
+        const int64_t plane_len = (int64_t)a.ho * a.row_len;
+        const int ck0 = tr.ck0, ck_mid = tr.ck_mid, ck_total = tr.ck_total;
+        const int start0 = m0 * a.row_len + qa0 - tr.shift0;
+        for (int rc = wave; rc < rc_act; rc += 4) {
+            float* l = S + rc * a.sc;
+            for (int c0 = 0; c0 < ck_total; c0 += 64) {
+                const int c = c0 + lane;
+                int sgi = 0, cs = c;
+                if (c >= ck0) {
+                    sgi = 1 + (int)fast_div((uint32_t)(c - ck0), a.div_ckmid);
+                    if (sgi > nseg - 1) sgi = nseg - 1;
+                    cs = c - ck0 - (sgi - 1) * ck_mid;
+                }
+                const float* g = srcf + ((int64_t)(i0 + sgi) * a.c + r0 + rc) * plane_len +
+                                 (sgi == 0 ? start0 : 0) + 4 * cs;
+                if (c < ck_total)
+                    __builtin_amdgcn_global_load_lds(g, (lds_void*)(l + 4 * c0), 16, 0, 0);
+            }
+        }
+        return;
+    }
     const int nruns = rc_act * nseg;
     for (int q = wave; q < nruns; q += 4) {
         const int rc = q / nseg, s = q - rc * nseg;
-        const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0);
+        const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0, d_first, d_second, d_stride);
         float* l = S + rc * a.sc + sr.off;
         const int len = sr.len;
         if (!FUSED) {
@@ -368,6 +406,20 @@ int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, int64_t* sc, 
     return 2 * *stage * 4;
 }
 
+// Strips can be staged by 16-byte copies when a window-tensor plane is a
+// whole number of 16-byte chunks (fp32: Ho*Wp*Fh divisible by 4).
+bool strips_vec(const Geometry& g) { return g.elem == 4 && ((g.ho * g.row_len) & 3) == 0; }
+
+// Strip capacity: the plain bound plus, for 16-byte runs, the shift of run 0
+// and the rounding of every run to whole chunks.
+int64_t strip_capacity(const Geometry& g, int bn, bool vec) {
+    const int64_t cap = strip_bound(g, bn);
+    if (!vec) return cap;
+    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
+    const int64_t nseg = std::min<int64_t>(dmax + 1, (bn - 1) / (g.ho * g.wo) + 2);
+    return cap + 3 + 3 * nseg;
+}
+
 // Zero reduction slots each way of splitting the two k-slots adds: one zero
 // channel in total (odd C, channel halves) or one zero filter row per channel
 // (odd Fh, row halves).
@@ -395,7 +447,8 @@ ConvPlan plan_conv_f32(const Geometry& g) {
         int64_t best_blocks = 0;
         for (int ci = 0; ci < 3; ++ci) {
             const TileCfg t = cfgs[ci];
-            const int64_t cap = strip_bound(g, t.bn);
+            const bool vec = strips_vec(g);
+            const int64_t cap = strip_capacity(g, t.bn, vec);
             ConvPlan p;
             for (int rc = step; rc <= rc_max; rc += step) {
                 int64_t sc, fp, st;
@@ -404,6 +457,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
                 p.kind = ConvPlan::kF32Lds;
                 p.bm = t.bm; p.bn = t.bn; p.rc = rc; p.tc = (int)g.taps; p.split = split;
                 p.strip_cap = cap; p.sc = sc; p.fp = fp; p.stage = st; p.lds_bytes = lds;
+                p.svec = vec ? 1 : 0;
             }
             if (p.kind == ConvPlan::kNone) continue;
             const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
@@ -416,20 +470,23 @@ ConvPlan plan_conv_f32(const Geometry& g) {
 }
 
 ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
-                       float* y) {
+                       float* y, bool fused) {
     ConvArgs a = make_conv_args(g, src, w, y, p.bm);
+    a.svec = (!fused && p.svec) ? 1 : 0;
     a.rc = p.rc;
     a.strip_cap = (int)p.strip_cap;
     a.sc = (int)p.sc;
     a.fp = (int)p.fp;
     a.stage = (int)p.stage;
     a.ksplit = p.split;
+    a.div_fp = make_fastdiv((uint32_t)p.fp);
+    a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 3) >> 2));
     return a;
 }
 
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen) {
-    const ConvArgs a = conv_args_f32(g, p, src, w, y);
+    const ConvArgs a = conv_args_f32(g, p, src, w, y, fused);
     const int64_t blocks = ((g.npix + p.bn - 1) / p.bn) * a.num_jtiles;
     if (blocks > 0x7fffffff) {
         snprintf(err, errlen, "conv: grid of %lld workgroups is too large", (long long)blocks);
