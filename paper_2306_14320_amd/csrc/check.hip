@@ -1,10 +1,11 @@
 // Host-side bounds check of the launch plans.  It replays, with the very
-// functions the kernels call (XformBlock, locate/advance, TileRuns,
+// functions the kernels call (XformBlock, TileRuns,
 // pixel_base), every workgroup of the transformation and of the convolution
 // for a descriptor and verifies that each LDS and device-memory index the
 // kernels form stays inside its buffer.  No HIP calls.
 #include <cstdarg>
 #include <cstdio>
+#include <vector>
 
 #include "common.h"
 #include "conv_common.h"
@@ -33,20 +34,16 @@ void check_transform(const Geometry& g, Report& r) {
     const int64_t x_elems = g.n * g.c * g.h * g.w;
     const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
     const int64_t lds_elems = p.lds_bytes / g.elem;
+    std::vector<uint8_t> hits;
     int64_t next_out = 0;
     for (int64_t b = 0; b < p.blocks && r.violations < 16; ++b) {
         XformBlock blk;
         blk.init(b, a);
         if (blk.nplanes < 1 || blk.nrows < 1)
             r.fail("transform block %lld: empty run", (long long)b);
-        if ((int64_t)blk.nplanes * blk.nrin * g.w > lds_elems)
-            r.fail("transform block %lld: stages %lld elements, LDS holds %lld", (long long)b,
-                   (long long)blk.nplanes * blk.nrin * g.w, (long long)lds_elems);
-        const int64_t src_lo = (blk.plane0 * g.h + blk.y_lo) * g.w;
-        const int64_t src_hi = ((blk.plane0 + blk.nplanes - 1) * g.h + blk.y_lo + blk.nrin) * g.w;
-        if (blk.nrin > 0 && (src_lo < 0 || src_hi > x_elems || blk.y_lo + blk.nrin > g.h))
-            r.fail("transform block %lld: reads x[%lld, %lld) of %lld", (long long)b,
-                   (long long)src_lo, (long long)src_hi, (long long)x_elems);
+        if (blk.shift + blk.olen + a.vec > lds_elems || (blk.obase - blk.shift) % a.vec != 0)
+            r.fail("transform block %lld: run of %d (+%d) elements, LDS holds %lld", (long long)b,
+                   blk.olen, blk.shift, (long long)lds_elems);
         if (blk.obase != next_out)
             r.fail("transform block %lld: output run starts at %lld, expected %lld", (long long)b,
                    (long long)blk.obase, (long long)next_out);
@@ -54,28 +51,48 @@ void check_transform(const Geometry& g, Report& r) {
         if (next_out > ws_elems)
             r.fail("transform block %lld: writes up to %lld of %lld", (long long)b,
                    (long long)next_out, (long long)ws_elems);
-        Cursor c = locate(0, a);
-        for (int e = 0; e < blk.olen; ++e) {
-            const Cursor d = locate(e, a);
-            if (d.plane != c.plane || d.mrel != c.mrel || d.k != c.k || d.u != c.u) {
-                r.fail("transform block %lld: cursor stepping disagrees at element %d", (long long)b, e);
+        if (a.g > 1 && (int64_t)blk.nrin * g.w != (int64_t)a.div_plane.d)
+            r.fail("transform block %lld: footprint per plane %lld, divisor %u", (long long)b,
+                   (long long)blk.nrin * g.w, a.div_plane.d);
+        // replay the scatter: every LDS write inside the run, each element of
+        // the run written once if it has a source in x and never if padding
+        hits.assign(blk.olen, 0);
+        const int per_plane = blk.nrin * a.w;
+        const int total = blk.nplanes * per_plane;
+        for (int f = 0; f < total && r.violations < 16; ++f) {
+            const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
+            const int rem = f - pj * per_plane;
+            const int rr = (int)fast_div((uint32_t)rem, a.div_w);
+            const int yy = blk.y_lo + rr, xx = rem - rr * a.w;
+            const int64_t src = (blk.plane0 + pj) * (int64_t)g.h * g.w + (int64_t)yy * g.w + xx;
+            if (pj >= blk.nplanes || yy < 0 || yy >= g.h || src < 0 || src >= x_elems) {
+                r.fail("transform block %lld: footprint element %d reads x[%lld]", (long long)b, f,
+                       (long long)src);
                 break;
             }
-            if (c.plane >= blk.nplanes || c.mrel >= blk.nrows) {
-                r.fail("transform block %lld: element %d outside its run", (long long)b, e);
-                break;
-            }
-            const int yy = (blk.m0 + c.mrel) * a.sh + c.u - a.ph;
-            const int xx = c.k - a.pw;
-            if (yy >= 0 && yy < g.h && xx >= 0 && xx < g.w) {
-                const int li = blk.lds_index(c.plane, yy, xx, a.w);
-                if (yy < blk.y_lo || yy >= blk.y_lo + blk.nrin || li < 0 || li >= (int64_t)blk.nplanes * blk.nrin * g.w) {
-                    r.fail("transform block %lld: element %d reads LDS %d (rows [%d,%d))", (long long)b,
-                           e, li, blk.y_lo, blk.y_lo + blk.nrin);
+            int mf, ml;
+            blk.rows_of(yy, a, &mf, &ml);
+            for (int m = mf; m <= ml; ++m) {
+                const int u = yy + a.ph - m * a.sh;
+                const int li = blk.lds_index(pj, m, xx + a.pw, u, a) - blk.shift;
+                if (u < 0 || u >= a.fh || li < 0 || li >= blk.olen) {
+                    r.fail("transform block %lld: scatter to %d outside the run", (long long)b, li);
                     break;
                 }
+                ++hits[li];
             }
-            advance(c, a);
+        }
+        for (int e = 0; e < blk.olen && r.violations < 16; ++e) {
+            const int q = e % a.row_len, row = e / a.row_len;
+            const int k = q / a.fh, u = q % a.fh;
+            const int m = blk.m0 + row % blk.nrows;
+            const int yy = m * a.sh + u - a.ph, xx = k - a.pw;
+            const bool has_src = yy >= 0 && yy < g.h && xx >= 0 && xx < g.w;
+            if (hits[e] != (has_src ? 1 : 0)) {
+                r.fail("transform block %lld: element %d written %d times (source %d)", (long long)b,
+                       e, hits[e], (int)has_src);
+                break;
+            }
         }
     }
     if (r.violations == 0 && next_out != ws_elems)

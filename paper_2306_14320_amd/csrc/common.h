@@ -66,17 +66,22 @@ struct XformArgs {
     int g;               // planes per workgroup (>1 only when tm == ho)
     int tm;              // window-tensor rows per plane per workgroup
     int tiles_per_plane; // ceil(ho / tm)
-    FastDiv div_row, div_fh, div_tm;
+    int vec;             // elements per 16 bytes
+    int vec_in;          // planes and rows of x are whole 16-byte vectors
+    FastDiv div_plane, div_w, div_sh;   // by H*W, W, sh
 };
 
 // The run of window-tensor rows one workgroup of the LDS kernel produces.
+// The workgroup builds the run in LDS (index 0 = global element obase - shift,
+// so that 16-byte LDS reads and global stores line up) and copies it out.
 struct XformBlock {
     int64_t plane0;   // first image plane (i*C + r)
     int nplanes;      // planes in this workgroup
     int m0, nrows;    // window-tensor rows [m0, m0 + nrows) of each plane
-    int y_lo, nrin;   // input rows [y_lo, y_lo + nrin) of each plane, staged in LDS
+    int y_lo, nrin;   // input rows [y_lo, y_lo + nrin) of each plane that the run uses
     int64_t obase;    // first output element
     int olen;         // output elements (one contiguous run)
+    int shift;        // obase mod (16 bytes / element size)
 
     __host__ __device__ void init(int64_t b, const XformArgs& a) {
         const int64_t grp = b / a.tiles_per_plane;
@@ -92,42 +97,23 @@ struct XformBlock {
         nrin = y_hi - y_lo > 0 ? y_hi - y_lo : 0;
         obase = (plane0 * a.ho + m0) * (int64_t)a.row_len;
         olen = nplanes * nrows * a.row_len;
+        shift = (int)(obase % a.vec);
     }
-    // LDS index of input element (plane p of this run, row yy, column xx);
-    // valid when 0 <= yy < H and 0 <= xx < W.
-    __host__ __device__ int lds_index(int p, int yy, int xx, int w) const {
-        return (p * nrin + (yy - y_lo)) * w + xx;
+    // Window-tensor rows [*m_first, *m_last] of this run that use input row
+    // yy (each at row-in-window u = yy + ph - m*sh); empty when first > last.
+    __host__ __device__ void rows_of(int yy, const XformArgs& a, int* m_first, int* m_last) const {
+        const int t = yy + a.ph;                       // >= 0
+        const int hi = (int)fast_div((uint32_t)t, a.div_sh);
+        const int lo_num = t - a.fh + a.sh;            // ceil((t - fh + 1) / sh)
+        const int lo = lo_num > 0 ? (int)fast_div((uint32_t)lo_num, a.div_sh) : 0;
+        *m_first = lo > m0 ? lo : m0;
+        *m_last = hi < m0 + nrows - 1 ? hi : m0 + nrows - 1;
+    }
+    // LDS index of window-tensor element (plane p of the run, row m, column k, u)
+    __host__ __device__ int lds_index(int p, int m, int k, int u, const XformArgs& a) const {
+        return shift + (p * nrows + (m - m0)) * a.row_len + k * a.fh + u;
     }
 };
-
-// Position of local output element e inside this workgroup's run.
-struct Cursor {
-    int plane, mrel, k, u;
-};
-
-__host__ __device__ inline Cursor locate(int e, const XformArgs& a) {
-    Cursor c;
-    const int row = (int)fast_div((uint32_t)e, a.div_row);
-    const int q = e - row * a.row_len;
-    c.k = (int)fast_div((uint32_t)q, a.div_fh);
-    c.u = q - c.k * a.fh;
-    c.plane = (a.g > 1) ? (int)fast_div((uint32_t)row, a.div_tm) : 0;
-    c.mrel = row - c.plane * a.tm;
-    return c;
-}
-
-__host__ __device__ inline void advance(Cursor& c, const XformArgs& a) {
-    if (++c.u == a.fh) {
-        c.u = 0;
-        if (++c.k == a.wp) {
-            c.k = 0;
-            if (++c.mrel == a.tm) {
-                c.mrel = 0;
-                ++c.plane;
-            }
-        }
-    }
-}
 
 struct XformPlan {
     bool use_lds = false;     // LDS-staged kernel, else the direct fallback

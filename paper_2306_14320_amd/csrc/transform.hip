@@ -4,13 +4,15 @@
 // Pure data movement, bound by HBM bandwidth.  Each workgroup owns one
 // contiguous run of window-tensor rows: either a tile of `tm` rows of one
 // image plane (large planes) or `g` whole image planes (small planes).  It
-//   1. copies the input rows that run needs into LDS with coalesced loads
-//      (rows of one plane are contiguous in x, so this is one linear copy),
-//   2. writes its output run with 16-byte stores in address order, reading the
-//      column-major strip values back from LDS.
-// Every input element is read from HBM once per workgroup; the Fh/sh-fold
-// duplication of the window tensor happens on chip.  Elements are moved as
-// raw bits (uint32 for fp32, uint16 for bf16), so the copy is exact.
+//   1. clears the run in LDS (padding positions stay zero),
+//   2. reads the input rows the run uses once, coalesced, eight loads in
+//      flight per thread, and writes every element to the ceil(Fh/sh)
+//      positions of the run that hold it (the Fh/sh-fold duplication of the
+//      window tensor happens on chip),
+//   3. copies the finished run to global memory with 16-byte LDS reads and
+//      16-byte stores in address order.
+// Elements move as raw bits (uint32 for fp32, uint16 for bf16): the copy is
+// exact.
 #include "common.h"
 
 #include <algorithm>
@@ -21,39 +23,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kOutTargetBytes = 32 * 1024;   // output bytes per workgroup (target)
-constexpr int kLdsBudgetBytes = 48 * 1024;   // LDS per workgroup (cap)
+constexpr int kLdsBudgetBytes = 64 * 1024;   // LDS per workgroup (cap)
 
 template <typename T, int V>
 struct alignas(16) Vec {
     T v[V];
 };
-
-template <typename T>
-__device__ inline void stage_rows(T* lds, const T* __restrict__ x, const XformArgs& a,
-                                  int64_t plane0, int nplanes, int y_lo, int nrin) {
-    const int per_plane = nrin * a.w;
-    if (nrin == a.h) {
-        // whole planes: one contiguous run of nplanes*H*W elements
-        const T* src = x + plane0 * (int64_t)a.h * a.w;
-        const int total = nplanes * per_plane;
-        for (int e = threadIdx.x; e < total; e += kThreads) lds[e] = src[e];
-    } else {
-        for (int p = 0; p < nplanes; ++p) {
-            const T* src = x + ((plane0 + p) * (int64_t)a.h + y_lo) * a.w;
-            T* dst = lds + p * per_plane;
-            for (int e = threadIdx.x; e < per_plane; e += kThreads) dst[e] = src[e];
-        }
-    }
-}
-
-template <typename T>
-__device__ inline T fetch(const T* lds, const Cursor& c, const XformArgs& a, const XformBlock& b) {
-    const int yy = (b.m0 + c.mrel) * a.sh + c.u - a.ph;
-    const int xx = c.k - a.pw;
-    if ((unsigned)yy < (unsigned)a.h && (unsigned)xx < (unsigned)a.w)
-        return lds[b.lds_index(c.plane, yy, xx, a.w)];
-    return T(0);
-}
 
 template <typename T, int V>
 __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
@@ -64,37 +39,89 @@ __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
 
     XformBlock blk;
     blk.init(blockIdx.x, a);
-    stage_rows<T>(lds, x, a, blk.plane0, blk.nplanes, blk.y_lo, blk.nrin);
+    const int span = blk.shift + blk.olen;             // LDS elements in use
+    const int nvec_lds = (span + V - 1) / V;
+
+    // 1. clear
+    Vec<T, V> zero;
+#pragma unroll
+    for (int j = 0; j < V; ++j) zero.v[j] = T(0);
+    for (int i = threadIdx.x; i < nvec_lds; i += kThreads) reinterpret_cast<Vec<T, V>*>(lds)[i] = zero;
     __syncthreads();
 
-    // This workgroup's output: one contiguous run [obase, obase + olen).
-    const int64_t obase = blk.obase;
-    const int olen = blk.olen;
-    const int head = (int)min<int64_t>((V - (obase % V)) % V, olen);
-    const int nvec = (olen - head) / V;
-    const int tail0 = head + nvec * V;
-
-    for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
-        const int e0 = head + vi * V;
-        Cursor c = locate(e0, a);
-        Vec<T, V> out;
+    // 2. scatter the input rows [y_lo, y_lo + nrin) of each plane.  When the
+    // footprint of a plane starts and ends on 16-byte boundaries each thread
+    // loads whole 16-byte vectors (V elements), else single elements; either
+    // way eight loads are in flight per thread before any value is placed.
+    const int per_plane = blk.nrin * a.w;
+    const int total = blk.nplanes * per_plane;
+    const int64_t plane_len = (int64_t)a.h * a.w;
+    const bool vec_in = a.vec_in && ((int64_t)blk.y_lo * a.w) % V == 0;
+    auto place = [&](T v, int f) {
+        const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
+        const int rem = f - pj * per_plane;
+        const int r = (int)fast_div((uint32_t)rem, a.div_w);
+        const int yy = blk.y_lo + r, xx = rem - r * a.w;
+        int mf, ml;
+        blk.rows_of(yy, a, &mf, &ml);
+        for (int m = mf; m <= ml; ++m)
+            lds[blk.lds_index(pj, m, xx + a.pw, yy + a.ph - m * a.sh, a)] = v;
+    };
+    if (vec_in) {
+        // footprint vectors; plane starts, row y_lo and per_plane are multiples of V
+        const int nv = total / V;
+        for (int i0 = threadIdx.x; i0 < nv; i0 += 8 * kThreads) {
+            Vec<T, V> v[8];
 #pragma unroll
-        for (int j = 0; j < V; ++j) {
-            out.v[j] = fetch<T>(lds, c, a, blk);
-            advance(c, a);
+            for (int j = 0; j < 8; ++j) {
+                const int i = i0 + j * kThreads;
+                const int f = i * V;
+                const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
+                const int64_t src = (blk.plane0 + pj) * plane_len + (int64_t)blk.y_lo * a.w + (f - pj * per_plane);
+                if (i < nv) v[j] = *reinterpret_cast<const Vec<T, V>*>(x + src);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int i = i0 + j * kThreads;
+                if (i < nv)
+#pragma unroll
+                    for (int t = 0; t < V; ++t) place(v[j].v[t], i * V + t);
+            }
         }
-        *reinterpret_cast<Vec<T, V>*>(ws + obase + e0) = out;
+    } else {
+        for (int f0 = threadIdx.x; f0 < total; f0 += 8 * kThreads) {
+            T v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int f = f0 + j * kThreads;
+                const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
+                const int64_t src = (blk.plane0 + pj) * plane_len + (int64_t)blk.y_lo * a.w + (f - pj * per_plane);
+                v[j] = f < total ? x[src] : T(0);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (f0 + j * kThreads < total) place(v[j], f0 + j * kThreads);
+        }
     }
-    // unaligned head and tail, one element per thread
-    const int nscalar = head + (olen - tail0);
-    for (int s = threadIdx.x; s < nscalar; s += kThreads) {
-        const int e = (s < head) ? s : tail0 + (s - head);
-        Cursor c = locate(e, a);
-        ws[obase + e] = fetch<T>(lds, c, a, blk);
-    }
+    __syncthreads();
+
+    // 3. copy out; LDS index i is global element obase - shift + i
+    const int64_t gbase = blk.obase - blk.shift;
+    const int first_vec = blk.shift ? 1 : 0;
+    const int last_vec = span / V;                      // vectors [first_vec, last_vec) are whole
+    // (plain stores: the convolution that follows reads the window tensor
+    // back, and finds much of it still in the caches)
+    for (int i = first_vec + threadIdx.x; i < last_vec; i += kThreads)
+        *reinterpret_cast<Vec<T, V>*>(ws + gbase + (int64_t)i * V) =
+            reinterpret_cast<const Vec<T, V>*>(lds)[i];
+    // partial head (before the first whole vector) and tail
+    const int head_end = min(first_vec ? V : 0, span);
+    for (int i = blk.shift + threadIdx.x; i < head_end; i += kThreads) ws[gbase + i] = lds[i];
+    for (int i = max(last_vec * V, head_end) + threadIdx.x; i < span; i += kThreads)
+        ws[gbase + i] = lds[i];
 }
 
-// Fallback for input rows too wide to stage in LDS: one workgroup per
+// Fallback for rows too long to build in LDS: one workgroup per
 // window-tensor row, reading x directly (loads stay coalesced along k).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void transform_direct_kernel(XformArgs a, int64_t nrows_total) {
@@ -129,28 +156,28 @@ void launch(const XformArgs& a, const XformPlan& p, int64_t nrows_total, hipStre
 
 }  // namespace
 
-// Work split of the transformation (chosen on the host, checked by the plan
-// checker with the same arithmetic).
+// Work split of the transformation (chosen on the host, replayed by the plan
+// checker with the same arithmetic): about kOutTargetBytes of output per
+// workgroup, the whole run held in LDS.
 XformPlan plan_transform(const Geometry& g) {
     XformPlan p;
     const int64_t e = g.elem;
+    const int64_t vec = 16 / e;
     const int64_t nc = g.n * g.c;
     const int64_t row_bytes = g.row_len * e;
     const int64_t plane_out = g.ho * row_bytes;
-    auto rows_in = [&](int64_t tm) { return std::min<int64_t>(g.h, (tm - 1) * g.sh + g.fh); };
     int64_t tm, gp;
     if (plane_out >= kOutTargetBytes / 2) {
         gp = 1;
         tm = std::max<int64_t>(1, std::min<int64_t>(g.ho, kOutTargetBytes / row_bytes));
-        while (tm > 1 && rows_in(tm) * g.w * e > kLdsBudgetBytes) --tm;
     } else {
         tm = g.ho;
         gp = std::max<int64_t>(1, std::min<int64_t>(nc, kOutTargetBytes / plane_out));
-        while (gp > 1 && gp * rows_in(tm) * g.w * e > kLdsBudgetBytes) --gp;
     }
-    p.lds_bytes = gp * rows_in(tm) * g.w * e;
-    // the LDS path indexes a workgroup's output run with 32-bit integers
-    p.use_lds = p.lds_bytes <= kLdsBudgetBytes && gp * tm * g.row_len < (int64_t(1) << 30);
+    p.lds_bytes = (gp * tm * g.row_len + 2 * vec) * e;
+    // the LDS kernel indexes a workgroup's run and footprint with 32-bit integers
+    p.use_lds = p.lds_bytes <= kLdsBudgetBytes && gp * tm * g.row_len < (int64_t(1) << 30) &&
+                gp * g.h * g.w < (int64_t(1) << 30);
     if (p.use_lds) {
         p.g = gp;
         p.tm = tm;
@@ -183,9 +210,14 @@ XformArgs transform_args(const Geometry& g, const XformPlan& p, const void* x, v
     a.g = (int)p.g;
     a.tm = (int)p.tm;
     a.tiles_per_plane = (int)p.tiles_per_plane;
-    a.div_row = make_fastdiv((uint32_t)a.row_len);
-    a.div_fh = make_fastdiv((uint32_t)a.fh);
-    a.div_tm = make_fastdiv((uint32_t)a.tm);
+    a.vec = 16 / g.elem;
+    a.vec_in = ((g.h * g.w) % a.vec == 0 && g.w % a.vec == 0) ? 1 : 0;
+    // with several planes per workgroup (tm == ho) every workgroup uses the
+    // same input rows of each plane: [max(0, -ph), min(h, (ho-1)*sh - ph + fh))
+    const int64_t rows = std::min<int64_t>(g.h, (g.ho - 1) * g.sh - g.ph + g.fh) - std::max<int64_t>(0, -g.ph);
+    a.div_plane = make_fastdiv((uint32_t)std::max<int64_t>(1, std::min<int64_t>(rows * g.w, 0x7fffffff)));
+    a.div_w = make_fastdiv((uint32_t)a.w);
+    a.div_sh = make_fastdiv((uint32_t)a.sh);
     return a;
 }
 
