@@ -192,6 +192,8 @@ void check_conv(const Geometry& g, Report& r) {
                    (long long)p.fp, (long long)p.lds_bytes);
         if (p.split == 0 && (p.rc & 1))
             r.fail("conv: channel split with an odd chunk of %d", p.rc);
+        if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
+            r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
     }
     check_conv_variant(g, p, false, r);
     if (!bf16 && p.svec) check_conv_variant(g, p, true, r);

@@ -36,6 +36,7 @@ struct ConvArgs {
     int e_row, e_k, e_u;   // 64 (one wave) = e_row*L + e_k*Fh + e_u (fused DMA walk)
     int stage;             // fp32: LDS floats per pipeline stage
     int svec;              // fp32 unfused: strips staged by 16-byte copies (plane % 4 == 0)
+    int fvec;              // fp32: filter rows staged by 16-byte copies
     FastDiv div_fp, div_ckmid;
 };
 
@@ -151,6 +152,7 @@ struct ConvPlan {
     int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
     int64_t stage = 0;       // fp32: LDS floats per pipeline stage
     int svec = 0;            // fp32 unfused: 16-byte strip copies
+    int fvec = 0;            // fp32: 16-byte filter-row copies
     int64_t lds_bytes = 0;
 };
 
@@ -211,6 +213,7 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.e_u = (64 % a.row_len) % a.fh;
     a.stage = 0;
     a.svec = 0;
+    a.fvec = 0;
     a.div_fp = make_fastdiv(1);
     a.div_ckmid = make_fastdiv(1);
     return a;

@@ -62,7 +62,22 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
     const int kreal = rc_act * a.taps;
     const int nrows_f = min(a.k - j0, a.bm);
     constexpr bool kDma = sizeof(TIn) == 4;
-    if (kDma) {
+    if (kDma && a.fvec) {
+        // filter rows are whole 16-byte chunks (C*T and the chunk's rc*T are
+        // multiples of 4): one DMA instruction fills 64 consecutive 16-byte
+        // chunks of the row-major tile (rows of stride fp, a multiple of 4)
+        const float* w = static_cast<const float*>(a.w) + ((int64_t)j0 * a.c + r0) * a.taps;
+        const int64_t wrow = (int64_t)a.c * a.taps;
+        const int cpr = a.fp >> 2, creal = kreal >> 2;
+        const int total = nrows_f * cpr;
+        for (int c0 = wave * 64; c0 < total; c0 += kConvThreads) {
+            const int c = c0 + lane;
+            const int jj = (int)fast_div((uint32_t)c, a.div_fp);
+            const int col = c - jj * cpr;
+            if (c < total && col < creal)
+                __builtin_amdgcn_global_load_lds(w + jj * wrow + 4 * col, (lds_void*)(F + 4 * c0), 16, 0, 0);
+        }
+    } else if (kDma) {
         // one DMA instruction fills 64 consecutive LDS floats of the row-major
         // tile (rows of stride fp), lane by lane from the matching filter row
         const float* w = static_cast<const float*>(a.w) + ((int64_t)j0 * a.c + r0) * a.taps;
@@ -397,13 +412,26 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, bool fuse
 // channels (stride sc) and bm filter rows (stride fp, odd so that 32
 // consecutive rows fall in different banks), with slack for the reads past
 // the last tap that a dead k-slot makes.
-int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, int64_t* sc, int64_t* fp,
-                   int64_t* stage) {
+int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, bool fvec, int64_t* sc,
+                   int64_t* fp, int64_t* stage) {
     *sc = (cap + g.fh + 3) & ~int64_t(3);
     *fp = (int64_t)rc * g.taps + g.fw + 1;
-    if ((*fp & 1) == 0) ++*fp;
+    if (fvec) {
+        // 16-byte rows: a multiple of 4 floats, and not of 8, so that 32
+        // consecutive rows spread over 8 banks (4-way, not 8-way, conflicts)
+        *fp = (*fp + 3) & ~int64_t(3);
+        if ((*fp & 7) == 0) *fp += 4;
+    } else if ((*fp & 1) == 0) {
+        ++*fp;   // odd stride: 32 consecutive rows fall in 32 banks
+    }
     *stage = ((int64_t)rc * *sc + (int64_t)bm * *fp + g.fw + 4 + 3) & ~int64_t(3);
     return 2 * *stage * 4;
+}
+
+// Filter rows can be staged by 16-byte copies when every row of every
+// channel chunk starts on a 16-byte boundary.
+bool filter_vec(const Geometry& g, int rc) {
+    return g.elem == 4 && ((g.c * g.taps) & 3) == 0 && ((rc * g.taps) & 3) == 0;
 }
 
 // Strips can be staged by 16-byte copies when a window-tensor plane is a
@@ -449,16 +477,24 @@ ConvPlan plan_conv_f32(const Geometry& g) {
             const TileCfg t = cfgs[ci];
             const bool vec = strips_vec(g);
             const int64_t cap = strip_capacity(g, t.bn, vec);
-            ConvPlan p;
+            // largest chunk that fits; among those that keep the filter rows
+            // 16-byte aligned, the largest of those if one fits
+            ConvPlan p, pv;
             for (int rc = step; rc <= rc_max; rc += step) {
                 int64_t sc, fp, st;
-                const int64_t lds = f32_layout(g, t.bm, rc, cap, &sc, &fp, &st);
-                if (lds > budget) break;
-                p.kind = ConvPlan::kF32Lds;
-                p.bm = t.bm; p.bn = t.bn; p.rc = rc; p.tc = (int)g.taps; p.split = split;
-                p.strip_cap = cap; p.sc = sc; p.fp = fp; p.stage = st; p.lds_bytes = lds;
-                p.svec = vec ? 1 : 0;
+                const bool fv = filter_vec(g, rc);
+                const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, &sc, &fp, &st);
+                if (lds > budget) continue;
+                ConvPlan q;
+                q.kind = ConvPlan::kF32Lds;
+                q.bm = t.bm; q.bn = t.bn; q.rc = rc; q.tc = (int)g.taps; q.split = split;
+                q.strip_cap = cap; q.sc = sc; q.fp = fp; q.stage = st; q.lds_bytes = lds;
+                q.svec = vec ? 1 : 0;
+                q.fvec = fv ? 1 : 0;
+                p = q;
+                if (fv) pv = q;
             }
+            if (pv.kind != ConvPlan::kNone) p = pv;
             if (p.kind == ConvPlan::kNone) continue;
             const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
             if (blocks >= 2 * 256) return p;
@@ -479,7 +515,8 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     a.fp = (int)p.fp;
     a.stage = (int)p.stage;
     a.ksplit = p.split;
-    a.div_fp = make_fastdiv((uint32_t)p.fp);
+    a.fvec = p.fvec;
+    a.div_fp = make_fastdiv((uint32_t)(p.fvec ? p.fp / 4 : p.fp));
     a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 3) >> 2));
     return a;
 }
