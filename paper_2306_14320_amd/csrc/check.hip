@@ -102,7 +102,7 @@ void check_transform(const Geometry& g, Report& r) {
 
 void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report& r) {
     const bool bf16 = p.kind == ConvPlan::kBf16Lds;
-    const ConvArgs a = bf16 ? conv_args_bf16(g, p, nullptr, nullptr, nullptr)
+    const ConvArgs a = bf16 ? conv_args_bf16(g, p, nullptr, nullptr, nullptr, fused)
                             : conv_args_f32(g, p, nullptr, nullptr, nullptr, fused);
     const char* what = fused ? "fused conv" : "conv";
     const int64_t ws_elems = g.n * g.c * g.ho * g.row_len;
@@ -133,15 +133,25 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
             if ((int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s) + len > plane)
                 r.fail("%s tile %lld: run %d runs past its plane", what, (long long)t, s);
             if (a.svec) {
-                // 16-byte copies: aligned start and rounded end stay in the plane,
-                // and the chunks of run s are the LDS chunks [off/4 - shift, ...)
+                // 16-byte copies of vc elements: aligned start and rounded end
+                // stay in the plane, and the chunks of run s are the LDS
+                // chunks [(off - shift)/vc, ...)
+                const int vc = a.vchunk;
                 const int64_t in_plane = (int64_t)tr.seg_m(s) * g.row_len + tr.seg_q(s);
                 const int shift = s == 0 ? tr.shift0 : 0;
-                if ((in_plane & 3) != shift || (plane & 3) != 0 ||
-                    ((in_plane - shift + 4 * (int64_t)((shift + len + 3) / 4)) > plane) ||
-                    ((off - shift) & 3) != 0)
+                if (vc * g.elem != 16 || (in_plane % vc) != shift || (plane % vc) != 0 ||
+                    ((in_plane - shift + vc * (int64_t)((shift + len + vc - 1) / vc)) > plane) ||
+                    ((off - shift) % vc) != 0)
                     r.fail("%s tile %lld: 16-byte run %d misplaced (shift %d)", what, (long long)t, s, shift);
             }
+        }
+        if (bf16) {
+            // per-thread staging items of this tile (16-byte chunks, or positions)
+            const int64_t items = a.svec ? 2 * (int64_t)tr.ck_total : 2 * (int64_t)tr.extent;
+            const int64_t cap_items = (int64_t)kConvThreads * (a.svec ? kBf16StripVecItems : kBf16StripScalarItems);
+            if (items > cap_items)
+                r.fail("%s tile %lld: %lld strip items, registers hold %lld", what, (long long)t,
+                       (long long)items, (long long)cap_items);
         }
         for (int q = 0; q < p.bn; ++q) {
             int px = tr.p0 + q;
@@ -195,8 +205,20 @@ void check_conv(const Geometry& g, Report& r) {
         if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
     }
+    if (bf16) {
+        // two stages of S[cap][16] then F[taps][bm][16] (bf16 elements)
+        if (p.rc != kBf16Chunk || p.tc != g.taps || p.stage < (p.strip_cap + g.taps * p.bm) * kBf16Chunk ||
+            p.lds_bytes < 2 * 2 * p.stage || (p.bm & (p.bm - 1)) != 0)
+            r.fail("conv: bf16 LDS layout too small (stage %lld, %lld bytes)", (long long)p.stage,
+                   (long long)p.lds_bytes);
+        if (p.fvec && ((g.c * g.taps) & 7))
+            r.fail("conv: 16-byte bf16 filter rows with C*T = %lld", (long long)(g.c * g.taps));
+        if (!p.fvec && 2 * g.taps * p.bm > (int64_t)kConvThreads * kBf16FilterScalarItems)
+            r.fail("conv: %lld bf16 filter items exceed the staging registers",
+                   (long long)(2 * g.taps * p.bm));
+    }
     check_conv_variant(g, p, false, r);
-    if (!bf16 && p.svec) check_conv_variant(g, p, true, r);
+    if (bf16 || p.svec) check_conv_variant(g, p, true, r);
 }
 
 }  // namespace

@@ -34,10 +34,12 @@ struct ConvArgs {
     FastDiv div_wo, div_ho, div_kpad, div_taps, div_fw, div_row, div_fh, div_tc2;
     int d_row, d_k, d_u;   // kConvThreads = d_row*L + d_k*Fh + d_u (fused walk)
     int e_row, e_k, e_u;   // 64 (one wave) = e_row*L + e_k*Fh + e_u (fused DMA walk)
-    int stage;             // fp32: LDS floats per pipeline stage
-    int svec;              // fp32 unfused: strips staged by 16-byte copies (plane % 4 == 0)
-    int fvec;              // fp32: filter rows staged by 16-byte copies
+    int stage;             // LDS elements per pipeline stage
+    int svec;              // unfused: strips staged by 16-byte copies (plane % vchunk == 0)
+    int vchunk;            // elements per 16 bytes (4 fp32, 8 bf16)
+    int fvec;              // filter rows staged by 16-byte copies
     FastDiv div_fp, div_ckmid;
+    FastDiv div_lenmid;    // by len_mid, the run length of a whole image (plain layout)
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -80,15 +82,16 @@ struct TileRuns {
             strip_len = len0 + (nseg - 2) * len_mid + len_last;
         }
         if (a.svec) {
-            shift0 = (m0 * a.row_len + qa0) & 3;
-            ck0 = (shift0 + len0 + 3) >> 2;
-            ck_mid = (len_mid + 3) >> 2;
-            ck_last = (len_last + 3) >> 2;
+            const int vc = a.vchunk;   // elements per 16-byte chunk (4 fp32, 8 bf16)
+            shift0 = (m0 * a.row_len + qa0) & (vc - 1);
+            ck0 = (shift0 + len0 + vc - 1) / vc;
+            ck_mid = (len_mid + vc - 1) / vc;
+            ck_last = (len_last + vc - 1) / vc;
             ck_total = nseg == 1 ? ck0 : ck0 + (nseg - 2) * ck_mid + ck_last;
             d_first = shift0;
-            d_second = 4 * ck0;
-            d_stride = 4 * ck_mid;
-            extent = 4 * ck_total;
+            d_second = vc * ck0;
+            d_stride = vc * ck_mid;
+            extent = vc * ck_total;
         } else {
             shift0 = 0;
             ck0 = ck_mid = ck_last = ck_total = 0;
@@ -150,9 +153,9 @@ struct ConvPlan {
     int split = 0;         // fp32: k-slot split (0 channel halves, 1 filter rows)
     int64_t strip_cap = 0; // LDS strip positions per channel
     int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
-    int64_t stage = 0;       // fp32: LDS floats per pipeline stage
-    int svec = 0;            // fp32 unfused: 16-byte strip copies
-    int fvec = 0;            // fp32: 16-byte filter-row copies
+    int64_t stage = 0;       // LDS elements per pipeline stage
+    int svec = 0;            // unfused: 16-byte strip copies
+    int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
 };
 
@@ -161,7 +164,13 @@ ConvPlan plan_conv_bf16(const Geometry& g);
 ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
                        float* y, bool fused);
 ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
-                        float* y);
+                        float* y, bool fused);
+
+// bf16 kernel: channels per chunk and per-thread staging registers (items)
+constexpr int kBf16Chunk = 16;
+constexpr int kBf16StripVecItems = 2;
+constexpr int kBf16StripScalarItems = 8;
+constexpr int kBf16FilterScalarItems = 16;
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
 
@@ -178,6 +187,17 @@ inline int64_t strip_bound(const Geometry& g, int bn) {
         return d * (g.row_len - g.wo * g.sw * g.fh) + (int64_t)(bn - 1) * g.sw * g.fh + g.fw * g.fh;
     };
     return std::max<int64_t>(1, std::max(at(0), at(dmax))) + 1;
+}
+
+// Strip capacity: the plain bound plus, for runs of 16-byte chunks of `vc`
+// elements (vc = 0: plain layout), the shift of run 0 and the rounding of
+// every run to whole chunks.
+inline int64_t strip_capacity(const Geometry& g, int bn, int vc) {
+    const int64_t cap = strip_bound(g, bn);
+    if (vc == 0) return cap;
+    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
+    const int64_t nseg = std::min<int64_t>(dmax + 1, (bn - 1) / (g.ho * g.wo) + 2);
+    return cap + (vc - 1) * (1 + nseg);
 }
 
 // Common launch arguments (everything except the per-dtype chunking).
@@ -213,9 +233,11 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.e_u = (64 % a.row_len) % a.fh;
     a.stage = 0;
     a.svec = 0;
+    a.vchunk = 16 / g.elem;
     a.fvec = 0;
     a.div_fp = make_fastdiv(1);
     a.div_ckmid = make_fastdiv(1);
+    a.div_lenmid = make_fastdiv((uint32_t)((g.ho - 1) * g.row_len + g.used_len));
     return a;
 }
 

@@ -438,16 +438,6 @@ bool filter_vec(const Geometry& g, int rc) {
 // whole number of 16-byte chunks (fp32: Ho*Wp*Fh divisible by 4).
 bool strips_vec(const Geometry& g) { return g.elem == 4 && ((g.ho * g.row_len) & 3) == 0; }
 
-// Strip capacity: the plain bound plus, for 16-byte runs, the shift of run 0
-// and the rounding of every run to whole chunks.
-int64_t strip_capacity(const Geometry& g, int bn, bool vec) {
-    const int64_t cap = strip_bound(g, bn);
-    if (!vec) return cap;
-    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
-    const int64_t nseg = std::min<int64_t>(dmax + 1, (bn - 1) / (g.ho * g.wo) + 2);
-    return cap + 3 + 3 * nseg;
-}
-
 // Zero reduction slots each way of splitting the two k-slots adds: one zero
 // channel in total (odd C, channel halves) or one zero filter row per channel
 // (odd Fh, row halves).
@@ -476,7 +466,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
         for (int ci = 0; ci < 3; ++ci) {
             const TileCfg t = cfgs[ci];
             const bool vec = strips_vec(g);
-            const int64_t cap = strip_capacity(g, t.bn, vec);
+            const int64_t cap = strip_capacity(g, t.bn, vec ? 4 : 0);
             // largest chunk that fits; among those that keep the filter rows
             // 16-byte aligned, the largest of those if one fits
             ConvPlan p, pv;
