@@ -9,8 +9,11 @@ resident in device memory before timing starts:
   4. fused convolution x -> y2 (window strips built on chip).
 The step therefore computes the convolution twice; `value` is the total
 convolution work of a step, 2 * (2*N*K*C*Ho*Wo*Fh*Fw) flops, divided by the
-measured step time.  Per-kernel times come from HIP events recorded on the
-launch stream around every kernel of every timed step.
+measured step time (host clock around the synchronised timed steps; the GPU
+time between two events around them is reported beside it).  Per-kernel
+launch durations, from which the roofline fractions are computed, come from a
+second timed region per kernel: as many back-to-back launches as timed steps,
+on the same stream, between two HIP events.
 
 Prints one JSON line (rank 0, N=1).  `--gpus N` with N > 1 exits: this build
 runs on one GPU.
@@ -45,15 +48,17 @@ def source_hash(kind):
 
 
 def measured_traffic(workload, kernel_kind):
-    """HBM bytes per launch from the committed counter summary, if it was taken
-    on the current kernel source; otherwise None."""
+    """HBM bytes per launch of a kernel ("transform", "conv" or "fused") from the
+    committed counter summary, if it was taken on the current kernel source;
+    otherwise None."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
     entry = t.get(workload, {}).get(kernel_kind)
-    if not entry or entry.get("source_hash") != source_hash(kernel_kind):
+    src = "transform" if kernel_kind == "transform" else "conv"
+    if not entry or entry.get("source_hash") != source_hash(src):
         return None
     return entry.get("bytes_per_launch")
 
@@ -105,38 +110,51 @@ def run_workload(wl, steps, warmup, with_cpu):
     sp = stream.cuda_stream
     xp, wp, wsp, yp, y2p = x.data_ptr(), w.data_ptr(), ws.data_ptr(), y.data_ptr(), y2.data_ptr()
 
-    def step(ev=None):
+    launch = {
+        "transform": lambda: P.im2win_transform(d, xp, wsp, ws_bytes, sp),
+        "conv2d": lambda: P.im2win_conv2d(d, wsp, ws_bytes, wp, yp, sp),
+        "conv2d_fused": lambda: P.im2win_conv2d_fused(d, xp, wp, y2p, sp),
+    }
+
+    def step():
         P.im2win_workspace_bytes(d)
-        if ev: ev[0].record(stream)
-        P.im2win_transform(d, xp, wsp, ws_bytes, sp)
-        if ev: ev[1].record(stream)
-        P.im2win_conv2d(d, wsp, ws_bytes, wp, yp, sp)
-        if ev: ev[2].record(stream)
-        P.im2win_conv2d_fused(d, xp, wp, y2p, sp)
-        if ev: ev[3].record(stream)
+        launch["transform"]()
+        launch["conv2d"]()
+        launch["conv2d_fused"]()
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
-    torch.cuda.synchronize()
+    # the timed steps: one event pair around all of them
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    e0.record(stream)
     for i in range(steps):
-        step(evs[i])
+        step()
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    t_xf = sum(e[0].elapsed_time(e[1]) for e in evs) / steps * 1e-3
-    t_cv = sum(e[1].elapsed_time(e[2]) for e in evs) / steps * 1e-3
-    t_fu = sum(e[2].elapsed_time(e[3]) for e in evs) / steps * 1e-3
+    gpu_step = e0.elapsed_time(e1) * 1e-3 / steps
+    # per-kernel launch duration: the same number of launches of each kernel
+    # back to back on the same stream, one event pair around them
+    per = {}
+    for name, fn in launch.items():
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        per[name] = a.elapsed_time(b) * 1e-3 / steps
+    t_xf, t_cv, t_fu = per["transform"], per["conv2d"], per["conv2d_fused"]
 
     conv_flops = 2 * wl.n * wl.k * wl.c * ho * wo * wl.fh * wl.fw
     e = x.element_size()
     xf_bytes = wl.n * wl.c * wl.h * wl.w * e + ws_bytes        # read x once, write the window tensor
     ms_per_step = wall / steps * 1e3
-    value = 2 * conv_flops / (wall / steps) / 1e9
+    value = 2 * conv_flops / (wall / steps) / 1e9   # host clock around the synchronised steps
     peak = PEAK[wl.dtype]
     dominant = max([("conv", t_cv), ("fused", t_fu), ("transform", t_xf)], key=lambda kv: kv[1])[0]
-    traffic = measured_traffic(wl.name, "conv")
     if dominant == "transform":
         achieved = xf_bytes / t_xf / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -146,11 +164,12 @@ def run_workload(wl, steps, warmup, with_cpu):
         t = t_cv if dominant == "conv" else t_fu
         achieved = conv_flops / t / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic if dominant == "conv" else None,
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(wl.name, dominant),
                 "kernel": "conv2d" if dominant == "conv" else "conv2d_fused"}
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4),
+        "gpu_ms_per_step": round(gpu_step * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic (seeded, distributions of the workload)",
         "config": {"workload": wl.label(), "global_batch": wl.n, "parallelism": "none (1 GPU)",
