@@ -145,6 +145,52 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                     r.fail("%s tile %lld: 16-byte run %d misplaced (shift %d)", what, (long long)t, s, shift);
             }
         }
+        if (fused && !bf16 && g.elem == 4) {
+            // raw input rows: inside x and inside their LDS area; their
+            // expansion writes each strip position once if it has a source
+            // in x, never if it lies in the padding
+            const RawRows rw = raw_rows(tr, a);
+            if ((int64_t)rw.rtot * g.w > a.raw_pitch || (a.raw_pitch & 3) || (a.raw_off & 3))
+                r.fail("fused conv tile %lld: %d raw rows of %lld, LDS pitch %d", (long long)t, rw.rtot,
+                       (long long)g.w, a.raw_pitch);
+            std::vector<uint8_t> hit(tr.extent > 0 ? tr.extent : 1, 0);
+            for (int rr = 0; rr < rw.rtot && r.violations < 16; ++rr) {
+                int yy, sg;
+                if (rr < rw.r0) { sg = 0; yy = rw.ylo0 + rr; }
+                else {
+                    sg = 1 + (rr - rw.r0) / std::max(a.rmid, 1);
+                    if (sg > tr.nseg - 1) sg = tr.nseg - 1;
+                    yy = a.ylo_mid + (rr - rw.r0 - (sg - 1) * a.rmid);
+                }
+                if (yy < 0 || yy >= g.h || tr.i0 + sg >= g.n) {
+                    r.fail("fused conv tile %lld: raw row %d reads x row %d of image %d", (long long)t, rr, yy, tr.i0 + sg);
+                    break;
+                }
+                const int m_st = tr.seg_m(sg), q_st = tr.seg_q(sg), len = tr.seg_len(sg), off = tr.seg_off(sg);
+                const int m_end = sg == tr.nseg - 1 ? tr.m1 : (int)g.ho - 1;
+                for (int xx = 0; xx < g.w; ++xx)
+                    for (int m = m_st; m <= m_end; ++m) {
+                        const int u = yy + (int)g.ph - m * (int)g.sh;
+                        if (u < 0 || u >= g.fh) continue;
+                        const int rel = (m - m_st) * (int)g.row_len + (xx + (int)g.pw) * (int)g.fh + u - q_st;
+                        if (rel >= 0 && rel < len) ++hit[off + rel];
+                    }
+            }
+            for (int sg = 0; sg < tr.nseg && r.violations < 16; ++sg) {
+                const int m_st = tr.seg_m(sg), q_st = tr.seg_q(sg), len = tr.seg_len(sg), off = tr.seg_off(sg);
+                for (int e = 0; e < len; ++e) {
+                    const int pos = m_st * (int)g.row_len + q_st + e;
+                    const int m = pos / (int)g.row_len, qq = pos % (int)g.row_len;
+                    const int yy = m * (int)g.sh + qq % (int)g.fh - (int)g.ph, xx = qq / (int)g.fh - (int)g.pw;
+                    const bool src = yy >= 0 && yy < g.h && xx >= 0 && xx < g.w;
+                    if (hit[off + e] != (src ? 1 : 0)) {
+                        r.fail("fused conv tile %lld: strip position %d written %d times (source %d)",
+                               (long long)t, off + e, hit[off + e], (int)src);
+                        break;
+                    }
+                }
+            }
+        }
         if (bf16) {
             // per-thread staging items of this tile (16-byte chunks, or positions)
             const int64_t items = a.svec ? 2 * (int64_t)tr.ck_total : 2 * (int64_t)tr.extent;
@@ -204,6 +250,8 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: channel split with an odd chunk of %d", p.rc);
         if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
+        if (g.elem == 4 && p.lds_bytes + 4 * p.rc * p.raw_pitch > kConvLdsMaxBytes)
+            r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * p.rc * p.raw_pitch));
     }
     if (bf16) {
         // two stages of S[cap][16] then F[taps][bm][16] (bf16 elements)

@@ -40,6 +40,14 @@ struct ConvArgs {
     int fvec;              // filter rows staged by 16-byte copies
     FastDiv div_fp, div_ckmid;
     FastDiv div_lenmid;    // by len_mid, the run length of a whole image (plain layout)
+    // fused fp32: the tile's input rows are copied to LDS (raw rows), then
+    // expanded on chip into the strip layout
+    int xvec;              // rows of x are whole 16-byte vectors (W % 4 == 0)
+    int raw_pitch;         // LDS floats per channel of the raw rows
+    int raw_off;           // LDS float offset of the raw rows
+    int rmid;              // input rows that the windows of a whole image use
+    int ylo_mid;           // first of them
+    FastDiv div_w, div_sh, div_rmid;   // by W, sh, max(rmid, 1)
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -143,6 +151,29 @@ __host__ __device__ inline int pixel_base(const TileRuns& tr, const ConvArgs& a,
     return tr.seg_off(s) + (m - tr.seg_m(s)) * a.row_len + n * a.sw * a.fh - tr.seg_q(s);
 }
 
+// Input rows of x that one pixel tile uses, per image segment of its runs:
+// segment 0 reads rows [ylo0, ylo0 + r0), the middle segments (whole images)
+// [ylo_mid, ylo_mid + rmid) and the last [ylo_mid, ylo_mid + rlast).  In LDS
+// they are stored back to back, segment after segment (rtot rows).
+struct RawRows {
+    int ylo0, r0, rlast, rtot;
+};
+
+__host__ __device__ inline int clamp_rows(int lo, int hi) { return hi > lo ? hi - lo : 0; }
+
+__host__ __device__ inline RawRows raw_rows(const TileRuns& tr, const ConvArgs& a) {
+    RawRows r;
+    const int m_end0 = tr.nseg == 1 ? tr.m1 : a.ho - 1;
+    const int lo0 = tr.m0 * a.sh - a.ph;
+    r.ylo0 = lo0 > 0 ? lo0 : 0;
+    const int hi0 = m_end0 * a.sh - a.ph + a.fh;
+    r.r0 = clamp_rows(r.ylo0, hi0 < a.h ? hi0 : a.h);
+    const int hil = tr.m1 * a.sh - a.ph + a.fh;
+    r.rlast = tr.nseg == 1 ? 0 : clamp_rows(a.ylo_mid, hil < a.h ? hil : a.h);
+    r.rtot = tr.nseg == 1 ? r.r0 : r.r0 + (tr.nseg - 2) * a.rmid + r.rlast;
+    return r;
+}
+
 // Launch plan of a convolution kernel (chosen on the host).
 struct ConvPlan {
     enum Kind { kNone, kF32Lds, kBf16Lds };
@@ -154,6 +185,7 @@ struct ConvPlan {
     int64_t strip_cap = 0; // LDS strip positions per channel
     int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
     int64_t stage = 0;       // LDS elements per pipeline stage
+    int64_t raw_pitch = 0;   // fused fp32: LDS floats per channel of the raw input rows
     int svec = 0;            // unfused: 16-byte strip copies
     int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
@@ -200,6 +232,21 @@ inline int64_t strip_capacity(const Geometry& g, int bn, int vc) {
     return cap + (vc - 1) * (1 + nseg);
 }
 
+// Upper bound of RawRows::rtot over all tiles of `bn` pixels: the window
+// rows a tile spans, each segment adding the filter height.
+// Upper bound of RawRows::rtot over all tiles of `bn` pixels.  A segment of
+// q window rows uses (q - 1)*sh + Fh input rows, and at most H; a tile spans
+// at most dmax + 1 window rows in ns segments, so at most
+// min(ns*H, (dmax + 1 - ns)*sh + ns*Fh) input rows.
+inline int64_t raw_rows_bound(const Geometry& g, int bn) {
+    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;   // row boundaries crossed
+    const int64_t nseg = std::min<int64_t>(dmax + 1, (bn - 1) / (g.ho * g.wo) + 2);
+    int64_t best = 0;
+    for (int64_t ns = 1; ns <= nseg; ++ns)
+        best = std::max(best, std::min<int64_t>(ns * g.h, (dmax + 1 - ns) * g.sh + ns * g.fh));
+    return best;
+}
+
 // Common launch arguments (everything except the per-dtype chunking).
 inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w, float* y,
                                int bm) {
@@ -238,6 +285,14 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.div_fp = make_fastdiv(1);
     a.div_ckmid = make_fastdiv(1);
     a.div_lenmid = make_fastdiv((uint32_t)((g.ho - 1) * g.row_len + g.used_len));
+    a.xvec = (g.w & 3) == 0 ? 1 : 0;
+    a.raw_pitch = 0;
+    a.raw_off = 0;
+    a.ylo_mid = (int)std::max<int64_t>(0, -g.ph);
+    a.rmid = (int)std::max<int64_t>(0, std::min<int64_t>(g.h, (g.ho - 1) * g.sh - g.ph + g.fh) - a.ylo_mid);
+    a.div_w = make_fastdiv((uint32_t)g.w);
+    a.div_sh = make_fastdiv((uint32_t)g.sh);
+    a.div_rmid = make_fastdiv((uint32_t)std::max(a.rmid, 1));
     return a;
 }
 

@@ -47,6 +47,12 @@ __device__ inline void dma_run(const float* g, float* l, int len, int lane) {
     }
 }
 
+// Zero the strips of channel slots [c0, c1) over the tile's extent.
+__device__ inline void zero_channels(float* S, const ConvArgs& a, const TileRuns& tr, int c0, int c1) {
+    for (int c = c0; c < c1; ++c)
+        for (int e = threadIdx.x; e < tr.extent; e += kConvThreads) S[c * a.sc + e] = 0.0f;
+}
+
 // Stage one channel chunk [r0, r0 + rc_act) of one tile into S (strips,
 // stride sc per channel) and F (filter rows, stride fp), issuing copies only:
 // fp32 data moves by DMA (global_load_lds) and lands while the previous chunk
@@ -55,7 +61,7 @@ __device__ inline void dma_run(const float* g, float* l, int len, int lane) {
 //   S[rc][0 .. strip_len)  window-tensor runs (unfused), or the same strip
 //                          positions gathered from x, zero where they fall in
 //                          the padding (fused)
-template <typename TIn, bool FUSED>
+template <typename TIn, bool FUSED, bool FILTER_ONLY = false>
 __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRuns& tr, int j0,
                              int r0, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -97,12 +103,15 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
             for (int e = lane; e < kreal; e += 64) F[jj * a.fp + e] = to_f32(g[e]);
         }
     }
-    // an odd last chunk under the channel split gets one zero channel
+    // a short last chunk under the channel split is padded with zero channels
+    // up to a whole chunk, so that every chunk runs the same MFMA sequence
     if (rc_stage > rc_act) {
-        for (int e = threadIdx.x; e < tr.extent; e += kConvThreads) S[rc_act * a.sc + e] = 0.0f;
+        if (!FILTER_ONLY) zero_channels(S, a, tr, rc_act, rc_stage);
+        const int nz = (rc_stage - rc_act) * a.taps;
         for (int jj = wave; jj < a.bm; jj += 4)
-            for (int e = lane; e < a.taps; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
+            for (int e = lane; e < nz; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
     }
+    if (FILTER_ONLY) return;
     const TIn* src = static_cast<const TIn*>(a.src);
     const int nseg = tr.nseg, i0 = tr.i0, len0 = tr.len0, len_mid = tr.len_mid,
               len_last = tr.len_last, m0 = tr.m0, qa0 = tr.qa0, d_first = tr.d_first,
@@ -179,6 +188,178 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
             }
         }
     }
+}
+
+// Segment of raw row r of a tile and the input row y it holds.
+__device__ inline int raw_segment(int r, const RawRows& rr, int nseg, const ConvArgs& a, int* yy) {
+    if (r < rr.r0) {
+        *yy = rr.ylo0 + r;
+        return 0;
+    }
+    int s = 1 + (int)fast_div((uint32_t)(r - rr.r0), a.div_rmid);
+    if (s > nseg - 1) s = nseg - 1;
+    *yy = a.ylo_mid + (r - rr.r0 - (s - 1) * a.rmid);
+    return s;
+}
+
+// Fused fp32: copy the input rows that channels [r0, r0 + rc_act) of the
+// tile use into X[rc][0 .. rtot*W), segment after segment (DMA; the rows of
+// one segment are contiguous in x).  16-byte copies when rows are whole
+// vectors, else one float per lane.
+__device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr, const RawRows& rr,
+                                 int r0, int rc_act) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float* x = static_cast<const float*>(a.src);
+    const int64_t plane = (int64_t)a.h * a.w_in;
+    const int n = rr.rtot * a.w_in;
+    const int nseg = tr.nseg, i0 = tr.i0;
+    if (a.xvec) {
+        const int nq = n >> 2;
+        for (int rc = wave; rc < rc_act; rc += 4) {
+            const float* xp = x + ((int64_t)i0 * a.c + r0 + rc) * plane;
+            float* l = X + rc * a.raw_pitch;
+            for (int c0 = 0; c0 < nq; c0 += 64) {
+                const int c = c0 + lane;
+                const int e = 4 * c;
+                const int r = (int)fast_div((uint32_t)e, a.div_w);
+                int yy;
+                const int sg = raw_segment(r, rr, nseg, a, &yy);
+                if (c < nq)
+                    __builtin_amdgcn_global_load_lds(xp + (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in),
+                                                     (lds_void*)(l + 4 * c0), 16, 0, 0);
+            }
+        }
+    } else {
+        for (int rc = wave; rc < rc_act; rc += 4) {
+            const float* xp = x + ((int64_t)i0 * a.c + r0 + rc) * plane;
+            float* l = X + rc * a.raw_pitch;
+            for (int e0 = 0; e0 < n; e0 += 64) {
+                const int e = e0 + lane;
+                const int r = (int)fast_div((uint32_t)e, a.div_w);
+                int yy;
+                const int sg = raw_segment(r, rr, nseg, a, &yy);
+                if (e < n)
+                    __builtin_amdgcn_global_load_lds(xp + (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in),
+                                                     (lds_void*)(l + e0), 4, 0, 0);
+            }
+        }
+    }
+}
+
+// Fused fp32: write every raw element x[yy][xx] of channel rc to the strip
+// positions that hold it, one per window row m with filter row
+// u = yy + ph - m*sh in [0, Fh): position (m, k = xx + pw, u) of the run
+// (the on-chip form of the transformation's scatter).  Positions in the
+// padding are never written; they were zeroed once.  An odd last chunk under
+// the channel split gets one zero channel.
+__device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
+                                  const RawRows& rr, int rc_act, int rc_stage) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nseg = tr.nseg, len0 = tr.len0, len_mid = tr.len_mid, len_last = tr.len_last,
+              m0 = tr.m0, m1 = tr.m1, qa0 = tr.qa0, d_second = tr.d_second, d_stride = tr.d_stride;
+    const int vw = a.xvec ? 4 : 1;
+    const int n = rr.rtot * a.w_in / vw;
+    for (int rc = wave; rc < rc_act; rc += 4) {
+        const float* xl = X + rc * a.raw_pitch;
+        float* sl = S + rc * a.sc;
+        for (int q = lane; q < n; q += 64) {
+            const int e = q * vw;
+            const int r = (int)fast_div((uint32_t)e, a.div_w);
+            const int xx = e - r * a.w_in;
+            int yy;
+            const int sg = raw_segment(r, rr, nseg, a, &yy);
+            const SegRun sr = seg_run(sg, nseg, len0, len_mid, len_last, m0, qa0, 0, d_second, d_stride);
+            const int m_end = sg == nseg - 1 ? m1 : a.ho - 1;
+            const int t = yy + a.ph - a.fh + 1;   // m*sh >= t
+            int m_lo = t <= 0 ? 0 : (int)fast_div((uint32_t)(t + a.sh - 1), a.div_sh);
+            if (m_lo < sr.m) m_lo = sr.m;
+            int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
+            if (m_hi > m_end) m_hi = m_end;
+            float v[4];
+            if (vw == 4) {
+                const float4 f = *reinterpret_cast<const float4*>(xl + e);
+                v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+            } else {
+                v[0] = xl[e];
+            }
+            for (int m = m_lo; m <= m_hi; ++m) {
+                const int u = yy + a.ph - m * a.sh;
+                const int rel = (m - sr.m) * a.row_len + (xx + a.pw) * a.fh + u - sr.q;
+                float* d = sl + sr.off + rel;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (j < vw && (unsigned)(rel + j * a.fh) < (unsigned)sr.len) d[j * a.fh] = v[j];
+            }
+        }
+    }
+    if (rc_stage > rc_act) zero_channels(S, a, tr, rc_act, rc_stage);
+}
+
+// Fused fp32, small tiles: the destinations of every raw element that a lane
+// expands are the same for every chunk and channel, so they are computed once
+// per kernel.  Lane l expands raw elements e = l + 64k (k < kExpandK) of each
+// of its channels; dst[k][i] is the strip offset (within a channel) of window
+// row m_lo + i, or the spare slot `trash` (past every strip extent, never
+// read by a window) when that row does not exist or holds no such position.
+constexpr int kExpandK = 8;
+constexpr int kExpandMaxRaw = 64 * kExpandK;   // raw floats per channel
+
+template <int FH>
+struct ExpandMap {
+    int dst[kExpandK][FH];
+};
+
+template <int FH>
+__device__ inline void expand_map_build(ExpandMap<FH>& mp, const ConvArgs& a, const TileRuns& tr,
+                                        const RawRows& rr, int trash) {
+    const int lane = threadIdx.x & 63;
+    const int n = rr.rtot * a.w_in;
+    const int nseg = tr.nseg;
+#pragma unroll
+    for (int k = 0; k < kExpandK; ++k) {
+        const int e = lane + 64 * k;
+#pragma unroll
+        for (int i = 0; i < FH; ++i) mp.dst[k][i] = trash;
+        if (e < n) {
+            const int r = (int)fast_div((uint32_t)e, a.div_w);
+            const int xx = e - r * a.w_in;
+            int yy;
+            const int sg = raw_segment(r, rr, nseg, a, &yy);
+            const SegRun sr = seg_run(sg, nseg, tr.len0, tr.len_mid, tr.len_last, tr.m0, tr.qa0, 0,
+                                      tr.d_second, tr.d_stride);
+            const int m_end = sg == nseg - 1 ? tr.m1 : a.ho - 1;
+            const int t = yy + a.ph - a.fh + 1;
+            int m_lo = t <= 0 ? 0 : (int)fast_div((uint32_t)(t + a.sh - 1), a.div_sh);
+            if (m_lo < sr.m) m_lo = sr.m;
+            int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
+            if (m_hi > m_end) m_hi = m_end;
+#pragma unroll
+            for (int i = 0; i < FH; ++i) {
+                const int m = m_lo + i;
+                const int u = yy + a.ph - m * a.sh;
+                const int rel = (m - sr.m) * a.row_len + (xx + a.pw) * a.fh + u - sr.q;
+                if (m <= m_hi && (unsigned)rel < (unsigned)sr.len) mp.dst[k][i] = sr.off + rel;
+            }
+        }
+    }
+}
+
+template <int FH>
+__device__ inline void expand_map_apply(float* S, const float* X, const ExpandMap<FH>& mp,
+                                        const ConvArgs& a, const TileRuns& tr, int rc_act, int rc_stage) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int rc = wave; rc < rc_act; rc += 4) {
+        const float* xl = X + rc * a.raw_pitch + lane;
+        float* sl = S + rc * a.sc;
+        float v[kExpandK];
+#pragma unroll
+        for (int k = 0; k < kExpandK; ++k) v[k] = 64 * k + lane < a.raw_pitch ? xl[64 * k] : 0.0f;
+#pragma unroll
+        for (int k = 0; k < kExpandK; ++k)
+#pragma unroll
+            for (int i = 0; i < FH; ++i) sl[mp.dst[k][i]] = v[k];
+    }
+    if (rc_stage > rc_act) zero_channels(S, a, tr, rc_act, rc_stage);
 }
 
 template <int NJ, int NP>
@@ -334,38 +515,66 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     // chunk c+1 land in the other.  One barrier per chunk: it waits for the
     // copies of chunk c (vmcnt 0 in every wave) and for every wave to be done
     // with chunk c-1, whose stage the copies of chunk c+1 then overwrite.
+    //
+    // Fused fp32 (RAW): the chunk's input rows are copied to LDS (X) instead
+    // and expanded into the strips after a second barrier; the copies of
+    // chunk c+1 land while chunk c is multiplied.  The strips' padding
+    // positions are zeroed once and never written again.
+    constexpr bool RAW = FUSED && sizeof(TIn) == 4;
     const int nchunks = (a.c + a.rc - 1) / a.rc;
+    float* X = S + a.raw_off;
+    RawRows rr{};
+    constexpr int FHM = FH > 0 ? FH : 1;
+    ExpandMap<FHM> emap;
+    const bool use_map = RAW && FH > 0 && a.raw_pitch <= kExpandMaxRaw;
     {
         const int rc_act = min(a.rc, a.c);
-        stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, ROWS ? rc_act : ((rc_act + 1) & ~1));
+        const int rc_stage = ROWS ? rc_act : a.rc;
+        if constexpr (RAW) {
+            rr = raw_rows(tr, a);
+            for (int sg = 0; sg < 2; ++sg)
+                for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
+            stage_raw(X, a, tr, rr, 0, rc_act);
+            stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
+            if (use_map) expand_map_build<FHM>(emap, a, tr, rr, a.strip_cap);
+            __syncthreads();   // zeros written, raw rows of chunk 0 landed
+            if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
+            else expand_raw(S, X, a, tr, rr, rc_act, rc_stage);
+        } else {
+            stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, rc_stage);
+        }
     }
     for (int ch = 0; ch < nchunks; ++ch) {
         const int r0 = ch * a.rc;
         const int rc_act = min(a.rc, a.c - r0);
-        const int rc_stage = ROWS ? rc_act : ((rc_act + 1) & ~1);
         const float* Sc = S + (ch & 1) * a.stage;
         const float* Fc = F + (ch & 1) * a.stage;
+        const int r1 = r0 + a.rc;
+        const int rc1 = min(a.rc, a.c - r1);
+        const int rc_stage1 = ROWS ? rc1 : a.rc;
+        const int off = ((ch + 1) & 1) * a.stage;
         __syncthreads();
         if (ch + 1 < nchunks) {
-            const int r1 = r0 + a.rc;
-            const int rc1 = min(a.rc, a.c - r1);
-            const int off = ((ch + 1) & 1) * a.stage;
-            stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, ROWS ? rc1 : ((rc1 + 1) & ~1));
+            if constexpr (RAW) {
+                stage_raw(X, a, tr, rr, r1, rc1);
+                stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
+            } else {
+                stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
-        if (ROWS) {
-            compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act);
-        } else if (rc_stage == a.rc) {
-            compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full);
-        } else {
-            // short last chunk: its second half starts at rc_stage/2
-            const int half = rc_stage >> 1;
-            int fl2[NJ], sl2[NP];
-#pragma unroll
-            for (int jb = 0; jb < NJ; ++jb) fl2[jb] = fl[jb] + kl * (half - half_full) * fh * fw;
-#pragma unroll
-            for (int pb = 0; pb < NP; ++pb) sl2[pb] = sl[pb] + kl * (half - half_full) * a.sc;
-            compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl2, sl2, kl, half);
+        if (ROWS) compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act);
+        else compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full);
+        if constexpr (RAW) {
+            // A wave expands the channels whose raw rows it copied itself
+            // (channels wave, wave + 4, ...), so waiting for its own copies
+            // is enough; the next barrier publishes the strips.
+            if (ch + 1 < nchunks) {
+                __builtin_amdgcn_sched_barrier(0);
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                if (use_map) expand_map_apply<FHM>(S + off, X, emap, a, tr, rc1, rc_stage1);
+                else expand_raw(S + off, X, a, tr, rr, rc1, rc_stage1);
+            }
         }
     }
 
@@ -387,6 +596,7 @@ template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int T
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipStream_t stream) {
     auto kern = fused ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, true>
                       : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, false>;
+    if (fused && sizeof(TIn) == 4) lds += (int64_t)a.rc * a.raw_pitch * 4;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
@@ -438,6 +648,11 @@ bool filter_vec(const Geometry& g, int rc) {
 // whole number of 16-byte chunks (fp32: Ho*Wp*Fh divisible by 4).
 bool strips_vec(const Geometry& g) { return g.elem == 4 && ((g.ho * g.row_len) & 3) == 0; }
 
+// LDS floats per channel for the raw input rows of a fused fp32 tile.
+int64_t raw_pitch_f32(const Geometry& g, int bn) {
+    return (raw_rows_bound(g, bn) * g.w + 3) & ~int64_t(3);
+}
+
 // Zero reduction slots each way of splitting the two k-slots adds: one zero
 // channel in total (odd C, channel halves) or one zero filter row per channel
 // (odd Fh, row halves).
@@ -474,13 +689,15 @@ ConvPlan plan_conv_f32(const Geometry& g) {
                 int64_t sc, fp, st;
                 const bool fv = filter_vec(g, rc);
                 const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, &sc, &fp, &st);
-                if (lds > budget) continue;
+                const int64_t raw = g.elem == 4 ? raw_pitch_f32(g, t.bn) : 0;
+                if (lds + rc * raw * 4 > budget) continue;
                 ConvPlan q;
                 q.kind = ConvPlan::kF32Lds;
                 q.bm = t.bm; q.bn = t.bn; q.rc = rc; q.tc = (int)g.taps; q.split = split;
                 q.strip_cap = cap; q.sc = sc; q.fp = fp; q.stage = st; q.lds_bytes = lds;
                 q.svec = vec ? 1 : 0;
                 q.fvec = fv ? 1 : 0;
+                q.raw_pitch = raw;
                 p = q;
                 if (fv) pv = q;
             }
@@ -508,6 +725,8 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     a.fvec = p.fvec;
     a.div_fp = make_fastdiv((uint32_t)(p.fvec ? p.fp / 4 : p.fp));
     a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 3) >> 2));
+    a.raw_pitch = (int)p.raw_pitch;
+    a.raw_off = 2 * (int)p.stage;
     return a;
 }
 
