@@ -191,14 +191,6 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                 }
             }
         }
-        if (bf16) {
-            // per-thread staging items of this tile (16-byte chunks, or positions)
-            const int64_t items = a.svec ? 2 * (int64_t)tr.ck_total : 2 * (int64_t)tr.extent;
-            const int64_t cap_items = (int64_t)kConvThreads * (a.svec ? kBf16StripVecItems : kBf16StripScalarItems);
-            if (items > cap_items)
-                r.fail("%s tile %lld: %lld strip items, registers hold %lld", what, (long long)t,
-                       (long long)items, (long long)cap_items);
-        }
         for (int q = 0; q < p.bn; ++q) {
             int px = tr.p0 + q;
             const bool valid = px <= tr.plast;
@@ -221,6 +213,103 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                     yoff + (g.k - 1) * g.ho * g.wo >= y_elems)
                     r.fail("%s tile %lld: pixel %d output offset %lld", what, (long long)t, px,
                            (long long)yoff);
+            }
+        }
+    }
+    if (r.violations == 0 && covered != g.npix)
+        r.fail("%s: tiles cover %lld of %lld pixels", what, (long long)covered, (long long)g.npix);
+}
+
+// bf16 channel-inner kernel: replay every staging item of every tile with
+// the kernel's own decode (segment, in-plane element, LDS position) and check
+// that loads stay inside the source planes, stores inside the strip plane,
+// and that every tap of every pixel's window reads the LDS position holding
+// exactly the window-tensor element that the tap needs.
+void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, Report& r) {
+    const ConvArgs a = conv_args_bf16(g, p, nullptr, nullptr, nullptr, fused);
+    const char* what = fused ? "fused bf16 conv" : "bf16 conv";
+    const int64_t plane = g.ho * g.row_len;
+    const int64_t y_elems = g.n * g.k * g.ho * g.wo;
+    const int64_t ptiles = (g.npix + p.bn - 1) / p.bn;
+    const int64_t pb = p.strip_cap;
+    int64_t covered = 0;
+    std::vector<int64_t> src;   // window-tensor element (segment * plane + e) held by each LDS position
+    for (int64_t t = 0; t < ptiles && r.violations < 16; ++t) {
+        TileRuns tr;
+        tr.init((int)t, p.bn, a);
+        const ClLayout cl = cl_layout(tr, a);
+        if (cl.extent > pb || cl.sb0 < 0 || cl.sb1 < 0 || cl.sp < 0)
+            r.fail("%s tile %lld: LDS extent %d, plane holds %lld", what, (long long)t, cl.extent, (long long)pb);
+        src.assign(pb, -1);
+        auto put = [&](int s, int64_t e, int pos) {
+            if (tr.i0 + s >= g.n || e < 0 || e >= plane || pos < 0 || pos >= pb) {
+                r.fail("%s tile %lld: element %lld of segment %d to LDS %d", what, (long long)t, (long long)e, s, pos);
+                return;
+            }
+            src[pos] = (int64_t)s * plane + e;
+        };
+        const int64_t items = a.svec ? 2 * (int64_t)tr.ck_total : 2 * (int64_t)tr.strip_len;
+        const int64_t cap_items = (int64_t)kConvThreads *
+                                  (a.svec ? (p.strip_items > kConvThreads ? 2 : 1) : kBf16StripScalarItems);
+        if (items > cap_items)
+            r.fail("%s tile %lld: %lld strip items, registers hold %lld", what, (long long)t,
+                   (long long)items, (long long)cap_items);
+        if (a.svec) {
+            const int start0 = tr.m0 * a.row_len + tr.qa0 - tr.shift0;
+            for (int c = 0; c < tr.ck_total && r.violations < 16; ++c) {
+                int s = 0, cs = c;
+                if (c >= tr.ck0) {
+                    s = 1 + (int)fast_div((uint32_t)(c - tr.ck0), a.div_ckmid);
+                    if (s > tr.nseg - 1) s = tr.nseg - 1;
+                    cs = c - tr.ck0 - (s - 1) * tr.ck_mid;
+                }
+                const int e = (s == 0 ? start0 : 0) + 4 * cs;
+                const int pos = cl_pos(cl, tr, a, s, e);
+                if ((e & 3) || e + 4 > plane) {
+                    r.fail("%s tile %lld: 8-byte group at element %d of a plane of %lld", what, (long long)t, e, (long long)plane);
+                    break;
+                }
+                for (int w = 0; w < 4; ++w) {
+                    if (cl_pos(cl, tr, a, s, e + w) != pos + w) {
+                        r.fail("%s tile %lld: group at element %d crosses a row", what, (long long)t, e);
+                        break;
+                    }
+                    put(s, e + w, pos + w);
+                }
+            }
+        } else {
+            for (int q = 0; q < tr.strip_len && r.violations < 16; ++q) {
+                int s = 0, base = 0;
+                if (q >= tr.len0) {
+                    s = 1 + (int)fast_div((uint32_t)(q - tr.len0), a.div_lenmid);
+                    if (s > tr.nseg - 1) s = tr.nseg - 1;
+                    base = tr.len0 + (s - 1) * tr.len_mid;
+                }
+                const int e = (s == 0 ? tr.m0 * a.row_len + tr.qa0 : 0) + q - base;
+                put(s, e, cl_pos(cl, tr, a, s, e));
+            }
+        }
+        for (int q = 0; q < p.bn && r.violations < 16; ++q) {
+            int px = tr.p0 + q;
+            const bool valid = px <= tr.plast;
+            if (!valid) px = tr.p0;
+            int64_t yoff;
+            const int base = cl_pixel_base(cl, tr, a, px, &yoff);
+            const int gi = px / (int)g.wo, ii = gi / (int)g.ho;
+            const int mm = gi - ii * (int)g.ho, nn = px - gi * (int)g.wo;
+            const int s = ii - tr.i0;
+            for (int tp = 0; tp < g.taps; ++tp) {
+                const int64_t want = (int64_t)s * plane + (int64_t)mm * g.row_len + (int64_t)nn * g.sw * g.fh + tp;
+                if (base + tp < 0 || base + tp >= pb || src[base + tp] != want) {
+                    r.fail("%s tile %lld: pixel %d tap %d reads LDS %d", what, (long long)t, px, tp, base + tp);
+                    break;
+                }
+            }
+            if (valid) {
+                ++covered;
+                if (yoff != (int64_t)ii * g.k * g.ho * g.wo + (int64_t)mm * g.wo + nn ||
+                    yoff + (g.k - 1) * g.ho * g.wo >= y_elems)
+                    r.fail("%s tile %lld: pixel %d output offset %lld", what, (long long)t, px, (long long)yoff);
             }
         }
     }
@@ -254,9 +343,11 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * p.rc * p.raw_pitch));
     }
     if (bf16) {
-        // two stages of S[cap][16] then F[taps][bm][16] (bf16 elements)
-        if (p.rc != kBf16Chunk || p.tc != g.taps || p.stage < (p.strip_cap + g.taps * p.bm) * kBf16Chunk ||
-            p.lds_bytes < 2 * 2 * p.stage || (p.bm & (p.bm - 1)) != 0)
+        // two stages of two strip planes [strip_cap] and two filter planes
+        // [cl_fpb >= taps*bm] of 8-element positions
+        if (p.rc != kBf16Chunk || p.tc != g.taps || p.cl_fpb < g.taps * p.bm ||
+            p.stage < 16 * (p.strip_cap + p.cl_fpb) || p.lds_bytes < 2 * 2 * p.stage ||
+            (p.bm & (p.bm - 1)) != 0 || p.cl_pitch < g.row_len)
             r.fail("conv: bf16 LDS layout too small (stage %lld, %lld bytes)", (long long)p.stage,
                    (long long)p.lds_bytes);
         if (p.fvec && ((g.c * g.taps) & 7))
@@ -265,8 +356,13 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: %lld bf16 filter items exceed the staging registers",
                    (long long)(2 * g.taps * p.bm));
     }
+    if (bf16) {
+        check_conv_bf16_variant(g, p, false, r);
+        check_conv_bf16_variant(g, p, true, r);
+        return;
+    }
     check_conv_variant(g, p, false, r);
-    if (bf16 || p.svec) check_conv_variant(g, p, true, r);
+    if (p.svec) check_conv_variant(g, p, true, r);
 }
 
 }  // namespace

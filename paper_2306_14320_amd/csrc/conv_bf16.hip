@@ -11,12 +11,18 @@
 // run of positions [base(p), base(p) + Fw*Fh), shared with the overlapping
 // windows of its neighbours (Sec. III-B).  The filter is held as F[t][j][16].
 //
+// Each operand is split into two planes of 8 channels (16 bytes per position)
+// so that a fragment read is one 16-byte vector per lane from one plane: the
+// filter planes are read contiguously, and the strip planes use a row pitch
+// and image-segment bases (ClLayout) that put the windows of 16 consecutive
+// pixels in 16 different bank groups when sw*Fh is odd.
+//
 // Neither operand has that layout in memory (the window tensor and the filter
 // are channel-outer), so each chunk passes through registers:
 //   - right after the barrier that opens chunk c, every thread loads its
-//     items of chunk c+1: 16-byte loads of 8 strip positions for each of 8
-//     channels, and of one output channel's filter row for 8 channels and all
-//     taps; they land while the MFMAs of chunk c run;
+//     items of chunk c+1: 8-byte loads of 4 strip positions for each of 8
+//     channels, and 16-byte loads of one output channel's filter row for 8
+//     channels and all taps; they land while the MFMAs of chunk c run;
 //   - after those MFMAs the items are transposed in registers (16-bit lane
 //     permutes) and written to the other of two LDS stages with 16-byte
 //     stores, so one barrier per chunk suffices.
@@ -45,109 +51,132 @@ enum StripMode { kStripVec = 0, kStripScalar = 1, kStripFused = 2 };
 __device__ inline uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
 __device__ inline uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 __device__ inline u32x4 load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ inline u32x2 load8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
 __device__ inline void store16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
 // Per-thread staging registers of one chunk's strips.
-template <int SMODE>
+template <int SMODE, int SVI = kStripVecItems>
 struct StripRegs {
-    static constexpr int kItems = SMODE == kStripVec ? kStripVecItems : kStripScalarItems;
-    static constexpr int kWords = SMODE == kStripVec ? 32 : 4;   // item: 8 channels x 8 or 1 positions
+    static constexpr int kItems = SMODE == kStripVec ? SVI : kStripScalarItems;
+    static constexpr int kWords = SMODE == kStripVec ? 16 : 4;   // item: 8 channels x 4 or 1 positions
     uint32_t d[kItems][kWords];
 };
 
 // The tile's runs, as plain values (kept in registers across the loop).
 struct Runs {
-    int i0, nseg, m0, qa0, d_first, d_second, d_stride, ck0, ck_mid, ck_total, start0, extent;
+    int i0, nseg, m0, qa0, len0, len_mid, ck0, ck_mid, ck_total, start0, strip_len;
 };
 
 __device__ inline Runs runs_of(const TileRuns& tr, const ConvArgs& a) {
     Runs r;
     r.i0 = tr.i0; r.nseg = tr.nseg; r.m0 = tr.m0; r.qa0 = tr.qa0;
-    r.d_first = tr.d_first; r.d_second = tr.d_second; r.d_stride = tr.d_stride;
+    r.len0 = tr.len0; r.len_mid = tr.len_mid;
     r.ck0 = tr.ck0; r.ck_mid = tr.ck_mid; r.ck_total = tr.ck_total;
     r.start0 = tr.m0 * a.row_len + tr.qa0 - tr.shift0;
-    r.extent = tr.extent;
+    r.strip_len = tr.strip_len;
     return r;
 }
 
-// Load the strips of channels [r0, r0 + 16) into registers.
-//   kStripVec:    item q = (16-byte chunk q/2 of the tile's runs, channel
-//                 group q%2): 8 loads of 8 positions, one per channel
-//                 (window-tensor planes are whole 16-byte vectors, so a chunk
-//                 never leaves its plane);
-//   kStripScalar: item q = (strip position q/2, channel group q%2), 8 loads
-//                 of one window-tensor element;
-//   kStripFused:  the same positions gathered from x, zero in the padding.
-template <int SMODE>
-__device__ inline void load_strips(StripRegs<SMODE>& R, const ConvArgs& a, const Runs& rn, int r0) {
+// LDS position (ClLayout) of in-plane element e of segment s.
+__device__ inline int lds_pos(const ClLayout& cl, const Runs& rn, const ConvArgs& a, int s, int e) {
+    const int row = (int)fast_div((uint32_t)e, a.div_row);
+    return cl.seg_base(s) + (row - (s == 0 ? rn.m0 : 0)) * a.cl_pitch + (e - row * a.row_len) -
+           (s == 0 ? rn.qa0 : 0);
+}
+
+// Segment and in-plane element of an item, as the loads and the stores of
+// the item both need them.
+struct ItemAt {
+    int s, e;
+};
+
+// kStripVec: item q = (4-element group q/2 of the tile's runs, channel half
+// q%2); the runs start on 4-element boundaries (shift0) and window-tensor
+// planes and rows are whole groups, so a group never leaves its row.
+__device__ inline ItemAt vec_item(int c, const Runs& rn, const ConvArgs& a) {
+    ItemAt it;
+    it.s = 0;
+    int cs = c;
+    if (c >= rn.ck0) {
+        it.s = 1 + (int)fast_div((uint32_t)(c - rn.ck0), a.div_ckmid);
+        if (it.s > rn.nseg - 1) it.s = rn.nseg - 1;
+        cs = c - rn.ck0 - (it.s - 1) * rn.ck_mid;
+    }
+    it.e = (it.s == 0 ? rn.start0 : 0) + 4 * cs;
+    return it;
+}
+
+// kStripScalar / kStripFused: item q = (run position q/2, channel half q%2),
+// runs back to back in run order.
+__device__ inline ItemAt scalar_item(int pos, const Runs& rn, const ConvArgs& a) {
+    ItemAt it;
+    it.s = 0;
+    int base = 0;
+    if (pos >= rn.len0) {
+        it.s = 1 + (int)fast_div((uint32_t)(pos - rn.len0), a.div_lenmid);
+        if (it.s > rn.nseg - 1) it.s = rn.nseg - 1;
+        base = rn.len0 + (it.s - 1) * rn.len_mid;
+    }
+    it.e = (it.s == 0 ? rn.m0 * a.row_len + rn.qa0 : 0) + pos - base;
+    return it;
+}
+
+// Load the strips of channels [r0, r0 + 16) into registers (the window
+// tensor, or for the fused kernel the same positions gathered from x, zero
+// in the padding).
+template <int SMODE, int SVI>
+__device__ inline void load_strips(StripRegs<SMODE, SVI>& R, const ConvArgs& a, const Runs& rn, int r0) {
     const uint16_t* src = static_cast<const uint16_t*>(a.src);
     if constexpr (SMODE == kStripVec) {
+        // Every load is issued, with indices clamped to valid memory: a
+        // thread without an item repeats item q%2 (and later stores the same
+        // values to the same place), channels beyond C read channel C-1 and
+        // are zeroed when stored.  Loads under no branch let the compiler
+        // wait for exactly the set it is about to store.
         const int64_t plane = (int64_t)a.ho * a.row_len;
         const int n = 2 * rn.ck_total;
 #pragma unroll
-        for (int k = 0; k < StripRegs<SMODE>::kItems; ++k) {
-            const int q = threadIdx.x + k * kConvThreads;
-            if (q < n) {
-                const int c = q >> 1, g = q & 1;
-                int s = 0, cs = c;
-                if (c >= rn.ck0) {
-                    s = 1 + (int)fast_div((uint32_t)(c - rn.ck0), a.div_ckmid);
-                    if (s > rn.nseg - 1) s = rn.nseg - 1;
-                    cs = c - rn.ck0 - (s - 1) * rn.ck_mid;
-                }
-                const int rb = r0 + 8 * g;
-                const uint16_t* base = src + ((int64_t)(rn.i0 + s) * a.c + rb) * plane +
-                                       (s == 0 ? rn.start0 : 0) + 8 * cs;
-                if (rb + 8 <= a.c) {
+        for (int k = 0; k < StripRegs<SMODE, SVI>::kItems; ++k) {
+            int q = threadIdx.x + k * kConvThreads;
+            if (q >= n) q &= 1;
+            const ItemAt it = vec_item(q >> 1, rn, a);
+            const int rb = r0 + 8 * (q & 1);
+            const uint16_t* base = src + (int64_t)(rn.i0 + it.s) * a.c * plane + it.e;
 #pragma unroll
-                    for (int ch = 0; ch < 8; ++ch) {
-                        const u32x4 v = load16(base + ch * plane);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) R.d[k][ch * 4 + e] = v[e];
-                    }
-                } else {
-#pragma unroll
-                    for (int ch = 0; ch < 8; ++ch) {
-                        u32x4 v = {0u, 0u, 0u, 0u};
-                        if (rb + ch < a.c) v = load16(base + ch * plane);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) R.d[k][ch * 4 + e] = v[e];
-                    }
-                }
+            for (int ch = 0; ch < 8; ++ch) {
+                const int cc = rb + ch < a.c ? rb + ch : a.c - 1;
+                const u32x2 v = load8(base + cc * plane);
+                R.d[k][2 * ch] = v[0];
+                R.d[k][2 * ch + 1] = v[1];
             }
         }
     } else {
-        const int n = 2 * rn.extent;
+        const int n = 2 * rn.strip_len;
 #pragma unroll
-        for (int k = 0; k < StripRegs<SMODE>::kItems; ++k) {
+        for (int k = 0; k < StripRegs<SMODE, SVI>::kItems; ++k) {
             const int q = threadIdx.x + k * kConvThreads;
             if (q < n) {
-                const int pos = q >> 1, g = q & 1;
-                int s = 0;
-                if (pos >= rn.d_second) {
-                    s = 1 + (int)fast_div((uint32_t)(pos - rn.d_second), a.div_lenmid);
-                    if (s > rn.nseg - 1) s = rn.nseg - 1;
-                }
-                const int e = pos - (s == 0 ? rn.d_first : rn.d_second + (s - 1) * rn.d_stride);
-                const int in_plane = (s == 0 ? rn.m0 * a.row_len + rn.qa0 : 0) + e;
-                const int rb = r0 + 8 * g;
+                const ItemAt it = scalar_item(q >> 1, rn, a);
+                const int rb = r0 + 8 * (q & 1);
                 uint32_t v[8];
                 if constexpr (SMODE == kStripScalar) {
                     const int64_t plane = (int64_t)a.ho * a.row_len;
-                    const uint16_t* p = src + ((int64_t)(rn.i0 + s) * a.c + rb) * plane + in_plane;
+                    const uint16_t* p = src + ((int64_t)(rn.i0 + it.s) * a.c + rb) * plane + it.e;
 #pragma unroll
                     for (int ch = 0; ch < 8; ++ch) v[ch] = rb + ch < a.c ? p[ch * plane] : 0u;
                 } else {
-                    // position (row m, column k, filter row u) of the window tensor
-                    const int m = (int)fast_div((uint32_t)in_plane, a.div_row);
-                    const int kq = in_plane - m * a.row_len;
+                    // element (row m, column k, filter row u) of the window tensor
+                    const int m = (int)fast_div((uint32_t)it.e, a.div_row);
+                    const int kq = it.e - m * a.row_len;
                     const int kc = (int)fast_div((uint32_t)kq, a.div_fh);
                     const int u = kq - kc * a.fh;
                     const int yy = m * a.sh + u - a.ph, xx = kc - a.pw;
                     const bool inb = (unsigned)yy < (unsigned)a.h && (unsigned)xx < (unsigned)a.w_in;
                     const int64_t plane = (int64_t)a.h * a.w_in;
-                    const uint16_t* p = src + ((int64_t)(rn.i0 + s) * a.c + rb) * plane +
+                    const uint16_t* p = src + ((int64_t)(rn.i0 + it.s) * a.c + rb) * plane +
                                         (inb ? (int64_t)yy * a.w_in + xx : 0);
 #pragma unroll
                     for (int ch = 0; ch < 8; ++ch) v[ch] = (inb && rb + ch < a.c) ? p[ch * plane] : 0u;
@@ -159,38 +188,49 @@ __device__ inline void load_strips(StripRegs<SMODE>& R, const ConvArgs& a, const
     }
 }
 
-// Write the loaded strips channel-innermost: S[pos][8g + ch].
-template <int SMODE>
-__device__ inline void store_strips(const StripRegs<SMODE>& R, uint16_t* S, const Runs& rn) {
+// Write the loaded strips channel-innermost into the two planes:
+// S + g*cl_pb*8 + pos*8 holds channels 8g .. 8g+7 of position pos.
+template <int SMODE, int SVI>
+__device__ inline void store_strips(const StripRegs<SMODE, SVI>& R, uint16_t* S, const Runs& rn,
+                                    const ClLayout& cl, const ConvArgs& a, int r0) {
     if constexpr (SMODE == kStripVec) {
         const int n = 2 * rn.ck_total;
 #pragma unroll
-        for (int k = 0; k < StripRegs<SMODE>::kItems; ++k) {
-            const int q = threadIdx.x + k * kConvThreads;
-            if (q < n) {
-                const int c = q >> 1, g = q & 1;
-                uint16_t* dst = S + (8 * c) * kRC + 8 * g;
+        for (int k = 0; k < StripRegs<SMODE, SVI>::kItems; ++k) {
+            int q = threadIdx.x + k * kConvThreads;
+            if (q >= n) q &= 1;
+            const ItemAt it = vec_item(q >> 1, rn, a);
+            uint16_t* dst = S + ((q & 1) * a.cl_pb + lds_pos(cl, rn, a, it.s, it.e)) * 8;
+            uint32_t d[16];
 #pragma unroll
-                for (int pq = 0; pq < 8; ++pq) {
-                    u32x4 o;
+            for (int i = 0; i < 16; ++i) d[i] = R.d[k][i];
+            if (r0 + kRC > a.c) {   // last chunk: channels beyond C are zero
+                const int rb = r0 + 8 * (q & 1);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t w0 = R.d[k][(2 * e) * 4 + pq / 2];
-                        const uint32_t w1 = R.d[k][(2 * e + 1) * 4 + pq / 2];
-                        o[e] = (pq & 1) ? hi_pair(w0, w1) : lo_pair(w0, w1);
-                    }
-                    store16(dst + pq * kRC, o);
+                for (int ch = 0; ch < 8; ++ch)
+                    if (rb + ch >= a.c) d[2 * ch] = d[2 * ch + 1] = 0u;
+            }
+#pragma unroll
+            for (int pq = 0; pq < 4; ++pq) {
+                u32x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t w0 = d[(2 * e) * 2 + pq / 2];
+                    const uint32_t w1 = d[(2 * e + 1) * 2 + pq / 2];
+                    o[e] = (pq & 1) ? hi_pair(w0, w1) : lo_pair(w0, w1);
                 }
+                store16(dst + pq * 8, o);
             }
         }
     } else {
-        const int n = 2 * rn.extent;
+        const int n = 2 * rn.strip_len;
 #pragma unroll
-        for (int k = 0; k < StripRegs<SMODE>::kItems; ++k) {
+        for (int k = 0; k < StripRegs<SMODE, SVI>::kItems; ++k) {
             const int q = threadIdx.x + k * kConvThreads;
             if (q < n) {
+                const ItemAt it = scalar_item(q >> 1, rn, a);
                 const u32x4 o = {R.d[k][0], R.d[k][1], R.d[k][2], R.d[k][3]};
-                store16(S + (q >> 1) * kRC + 8 * (q & 1), o);
+                store16(S + ((q & 1) * a.cl_pb + lds_pos(cl, rn, a, it.s, it.e)) * 8, o);
             }
         }
     }
@@ -213,29 +253,25 @@ __device__ inline void load_filter(FilterRegs<FVEC, FH * FW, BM>& R, const ConvA
     const uint16_t* w = static_cast<const uint16_t*>(a.w);
     if constexpr (FVEC) {
         constexpr int T = FH * FW;
+        // Unconditional loads with clamped indices, as for the strips: a
+        // thread beyond the 2*BM items repeats one, output channels beyond K
+        // read channel K-1, and 16-byte groups past the channels of the
+        // filter row are clamped to its last group; all of these are zeroed
+        // or duplicated when stored.
 #pragma unroll
         for (int k = 0; k < FilterRegs<FVEC, T, BM>::kItems; ++k) {
-            const int q = threadIdx.x + k * kConvThreads;
+            const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
             const int j = q >> 1, g = q & 1;
             const int rb = r0 + 8 * g;
-            const int nvalid_el = (a.c - rb) * T;   // elements of this group inside the filter row
-            const bool ok = q < 2 * BM && j0 + j < a.k;
-            const uint16_t* base = w + ((int64_t)(j0 + j) * a.c + rb) * T;
-            if (ok && rb + 8 <= a.c) {
+            const int jc = j0 + j < a.k ? j0 + j : a.k - 1;
+            const int rbc = rb < a.c ? rb : (a.c - 1) & ~7;   // keeps the groups 16-byte aligned
+            const int last = ((a.c - rbc) * T - 1) >> 3;   // last 16-byte group inside the row
+            const uint16_t* base = w + ((int64_t)jc * a.c + rbc) * T;
 #pragma unroll
-                for (int v4 = 0; v4 < T; ++v4) {
-                    const u32x4 v = load16(base + 8 * v4);
+            for (int v4 = 0; v4 < T; ++v4) {
+                const u32x4 v = load16(base + 8 * (v4 < last ? v4 : last));
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) R.d[k][v4 * 4 + e] = v[e];
-                }
-            } else {
-#pragma unroll
-                for (int v4 = 0; v4 < T; ++v4) {
-                    u32x4 v = {0u, 0u, 0u, 0u};
-                    if (ok && 8 * v4 < nvalid_el) v = load16(base + 8 * v4);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) R.d[k][v4 * 4 + e] = v[e];
-                }
+                for (int e = 0; e < 4; ++e) R.d[k][v4 * 4 + e] = v[e];
             }
         }
     } else {
@@ -269,19 +305,21 @@ __device__ inline uint32_t elem16(const uint32_t (&d)[W], int i) {
     return (i & 1) ? (d[i >> 1] >> 16) : (d[i >> 1] & 0xffffu);
 }
 
-// Write the loaded filter as F[t][j][8g + ch], t = v*Fh + u (the order of a
-// window's positions); channels beyond C are zeroed here.
+// Write the loaded filter into two planes, F + (g*cl_fpb + t*BM + j)*8
+// holding channels 8g .. 8g+7 of tap t = v*Fh + u (the order of a window's
+// positions) of output channel j; channels beyond C are zeroed here.
 template <bool FVEC, int FH, int FW, int BM>
 __device__ inline void store_filter(const FilterRegs<FVEC, FH * FW, BM>& R, uint16_t* F,
-                                    const ConvArgs& a, int r0) {
+                                    const ConvArgs& a, int j0, int r0) {
     if constexpr (FVEC) {
         constexpr int T = FH * FW;
 #pragma unroll
         for (int k = 0; k < FilterRegs<FVEC, T, BM>::kItems; ++k) {
-            const int q = threadIdx.x + k * kConvThreads;
-            if (q < 2 * BM) {
+            const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
+            {
                 const int j = q >> 1, g = q & 1;
-                const int nvalid = a.c - (r0 + 8 * g);   // channels of this group inside C
+                // channels of this group inside C (none for output channels beyond K)
+                const int nvalid = j0 + j < a.k ? a.c - (r0 + 8 * g) : 0;
 #pragma unroll
                 for (int v = 0; v < FW; ++v)
 #pragma unroll
@@ -294,7 +332,7 @@ __device__ inline void store_filter(const FilterRegs<FVEC, FH * FW, BM>& R, uint
                             const uint32_t hi = 2 * e + 1 < nvalid ? elem16(R.d[k], (2 * e + 1) * T + nat) : 0u;
                             o[e] = lo | (hi << 16);
                         }
-                        store16(F + (t * BM + j) * kRC + 8 * g, o);
+                        store16(F + (g * a.cl_fpb + t * BM + j) * 8, o);
                     }
             }
         }
@@ -307,7 +345,7 @@ __device__ inline void store_filter(const FilterRegs<FVEC, FH * FW, BM>& R, uint
                 const int g = q & 1, rest = q >> 1;
                 const int j = rest & (BM - 1), t = rest / BM;
                 const u32x4 o = {R.d[k][0], R.d[k][1], R.d[k][2], R.d[k][3]};
-                store16(F + (t * BM + j) * kRC + 8 * g, o);
+                store16(F + (g * a.cl_fpb + t * BM + j) * 8, o);
             }
         }
     }
@@ -325,9 +363,9 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const uint16_t* F, c
     bf16x8 a0[NJ], b0[NP], a1[NJ], b1[NP];
     auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
 #pragma unroll
-        for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * kRC + fo[jb]);
+        for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * 8 + fo[jb]);
 #pragma unroll
-        for (int pb = 0; pb < NP; ++pb) bv[pb] = frag(S + t * kRC + so[pb]);
+        for (int pb = 0; pb < NP; ++pb) bv[pb] = frag(S + t * 8 + so[pb]);
     };
     auto mm = [&](const bf16x8 (&av)[NJ], const bf16x8 (&bv)[NP]) {
 #pragma unroll
@@ -353,7 +391,7 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const uint16_t* F, c
     if (t < T) mm(a0, b0);
 }
 
-template <int FH, int FW, int BM, int BN, int TJ, int TP, int SMODE, bool FVEC>
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int SMODE, bool FVEC, int SVI>
 __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     static_assert((BM & (BM - 1)) == 0, "BM is a power of two");
@@ -362,8 +400,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
     constexpr int FT = FH * FW;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t* lds = reinterpret_cast<uint16_t*>(smem);   // stage s: S at s*stage, F after S
-    const int f_off = a.strip_cap * kRC;
+    uint16_t* lds = reinterpret_cast<uint16_t*>(smem);   // stage s: strip planes, then filter planes
+    const int f_off = 2 * a.cl_pb * 8;
 
     const int jtile = blockIdx.x % a.num_jtiles;
     const int ptile = blockIdx.x / a.num_jtiles;
@@ -372,6 +410,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
     TileRuns tr;
     tr.init(ptile, BN, a);
     const Runs rn = runs_of(tr, a);
+    const ClLayout cl = cl_layout(tr, a);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -386,11 +425,11 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
         int p = tr.p0 + wp_ * TP + pb * 32 + l32;
         pvalid[pb] = p <= tr.plast;
         if (!pvalid[pb]) p = tr.p0;
-        so[pb] = pixel_base(tr, a, p, &yoff[pb]) * kRC + 8 * kl;
+        so[pb] = (kl * a.cl_pb + cl_pixel_base(cl, tr, a, p, &yoff[pb])) * 8;
     }
     int fo[NJ];
 #pragma unroll
-    for (int jb = 0; jb < NJ; ++jb) fo[jb] = (wj * TJ + jb * 32 + l32) * kRC + 8 * kl;
+    for (int jb = 0; jb < NJ; ++jb) fo[jb] = (kl * a.cl_fpb + wj * TJ + jb * 32 + l32) * 8;
 
     f32x16 acc[NJ][NP];
 #pragma unroll
@@ -400,32 +439,44 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
 
-    StripRegs<SMODE> sr;
-    FilterRegs<FVEC, FT, BM> fr;
+    // Two register sets: chunk k is staged through set k % 2.  Its loads are
+    // issued right after the barrier that opens chunk k - 2, so they have two
+    // chunks of MFMA work to land; after the MFMAs of chunk k - 1 the set is
+    // transposed into the LDS stage of chunk k.  One barrier per chunk
+    // publishes that stage and frees the other one; it waits for LDS
+    // operations only, not for the loads still in flight.
+    StripRegs<SMODE, SVI> sr0, sr1;
+    FilterRegs<FVEC, FT, BM> fr0, fr1;
     const int nchunks = (a.c + kRC - 1) / kRC;
-    load_strips<SMODE>(sr, a, rn, 0);
-    load_filter<FVEC, FH, FW, BM>(fr, a, j0, 0);
-    store_strips<SMODE>(sr, lds, rn);
-    store_filter<FVEC, FH, FW, BM>(fr, lds + f_off, a, 0);
-    // One barrier per chunk: it publishes the stage written after the MFMAs
-    // of the previous chunk and tells every wave that the other stage, read
-    // by those MFMAs, may be overwritten.  The next chunk's loads are issued
-    // after the barrier so that the barrier does not wait for them.
-    for (int ch = 0; ch < nchunks; ++ch) {
+    load_strips<SMODE, SVI>(sr0, a, rn, 0);
+    load_filter<FVEC, FH, FW, BM>(fr0, a, j0, 0);
+    store_strips<SMODE, SVI>(sr0, lds, rn, cl, a, 0);
+    store_filter<FVEC, FH, FW, BM>(fr0, lds + f_off, a, j0, 0);
+    if (nchunks > 1) {
+        load_strips<SMODE, SVI>(sr1, a, rn, kRC);
+        load_filter<FVEC, FH, FW, BM>(fr1, a, j0, kRC);
+    }
+    auto step = [&](int ch, StripRegs<SMODE, SVI>& s_ld, FilterRegs<FVEC, FT, BM>& f_ld,
+                    StripRegs<SMODE, SVI>& s_st, FilterRegs<FVEC, FT, BM>& f_st) {
         const uint16_t* cur = lds + (ch & 1) * a.stage;
         uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
-        const bool more = ch + 1 < nchunks;
-        __syncthreads();
-        if (more) {
-            load_strips<SMODE>(sr, a, rn, (ch + 1) * kRC);
-            load_filter<FVEC, FH, FW, BM>(fr, a, j0, (ch + 1) * kRC);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (ch + 2 < nchunks) {
+            load_strips<SMODE, SVI>(s_ld, a, rn, (ch + 2) * kRC);
+            load_filter<FVEC, FH, FW, BM>(f_ld, a, j0, (ch + 2) * kRC);
         }
         compute_chunk<FT, BM, NJ, NP>(acc, cur + f_off, cur, fo, so, a.taps);
-        if (more) {
-            store_strips<SMODE>(sr, nxt, rn);
-            store_filter<FVEC, FH, FW, BM>(fr, nxt + f_off, a, (ch + 1) * kRC);
+        if (ch + 1 < nchunks) {
+            store_strips<SMODE, SVI>(s_st, nxt, rn, cl, a, (ch + 1) * kRC);
+            store_filter<FVEC, FH, FW, BM>(f_st, nxt + f_off, a, j0, (ch + 1) * kRC);
         }
+    };
+    int ch = 0;
+    for (; ch + 2 <= nchunks; ch += 2) {
+        step(ch, sr0, fr0, sr1, fr1);
+        step(ch + 1, sr1, fr1, sr0, fr0);
     }
+    if (ch < nchunks) step(ch, sr0, fr0, sr1, fr1);
 
     // D[row][col]: col = lane%32 (pixel), row = 8*(v/4) + 4*(lane/32) + v%4 (channel)
 #pragma unroll
@@ -441,11 +492,230 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
         }
 }
 
+// The common case, as one branch-free loop: strips in 4-element groups and
+// filter rows in 16-byte vectors (both operands whole vectors), C a multiple
+// of the 16-channel chunk and K of the tile's channels.  The item addresses
+// are the same for every chunk but for the channel offset, so they are
+// computed once; the stores of chunk c+1 (transposes + 16-byte LDS writes,
+// one filter tap and one strip position per step) are interleaved with the
+// MFMAs of chunk c, which a single wave per SIMD cannot otherwise overlap.
+// Chunks past the last are loaded again from the last one and written to the
+// stage no MFMA reads any more, so no step needs a branch.
+template <int FH, int FW, int BM, int NJ, int NP, int SVI>
+struct FastStage {
+    static constexpr int T = FH * FW;
+    static constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
+    uint32_t sd[SVI][16];          // strips: 8 channels x 4 positions per item
+    uint32_t fd[FI][4 * T];        // filter: 8 channels x T taps per item
+};
+
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int SVI>
+__global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a) {
+    static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+    constexpr int NJ = TJ / 32, NP = TP / 32;
+    constexpr int WAVES_P = BN / TP;
+    constexpr int T = FH * FW;
+    constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
+    using St = FastStage<FH, FW, BM, NJ, NP, SVI>;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+    const int f_off = 2 * a.cl_pb * 8;
+
+    const int jtile = blockIdx.x % a.num_jtiles;
+    const int ptile = blockIdx.x / a.num_jtiles;
+    const int j0 = jtile * BM;
+
+    TileRuns tr;
+    tr.init(ptile, BN, a);
+    const Runs rn = runs_of(tr, a);
+    const ClLayout cl = cl_layout(tr, a);
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wj = wave / WAVES_P, wp_ = wave % WAVES_P;
+    const int l32 = lane & 31, kl = lane >> 5;
+
+    int so[NP];
+    int64_t yoff[NP];
+    bool pvalid[NP];
+#pragma unroll
+    for (int pb = 0; pb < NP; ++pb) {
+        int p = tr.p0 + wp_ * TP + pb * 32 + l32;
+        pvalid[pb] = p <= tr.plast;
+        if (!pvalid[pb]) p = tr.p0;
+        so[pb] = (kl * a.cl_pb + cl_pixel_base(cl, tr, a, p, &yoff[pb])) * 8;
+    }
+    int fo[NJ];
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) fo[jb] = (kl * a.cl_fpb + wj * TJ + jb * 32 + l32) * 8;
+
+    // per-item sources (channel 0 of the chunk) and LDS destinations
+    const uint16_t* src = static_cast<const uint16_t*>(a.src);
+    const uint16_t* wsrc = static_cast<const uint16_t*>(a.w);
+    const int plane = a.ho * a.row_len;
+    const uint16_t* sp[SVI];
+    int sdst[SVI];
+    const int nitems = 2 * rn.ck_total;
+#pragma unroll
+    for (int k = 0; k < SVI; ++k) {
+        int q = threadIdx.x + k * kConvThreads;
+        if (q >= nitems) q &= 1;          // repeat an item: same values, same place
+        const ItemAt it = vec_item(q >> 1, rn, a);
+        sp[k] = src + ((int64_t)(rn.i0 + it.s) * a.c + 8 * (q & 1)) * plane + it.e;
+        sdst[k] = ((q & 1) * a.cl_pb + lds_pos(cl, rn, a, it.s, it.e)) * 8;
+    }
+    const uint16_t* fp[FI];
+    int fdst[FI];
+#pragma unroll
+    for (int k = 0; k < FI; ++k) {
+        const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
+        fp[k] = wsrc + ((int64_t)(j0 + (q >> 1)) * a.c + 8 * (q & 1)) * T;
+        fdst[k] = ((q & 1) * a.cl_fpb + (q >> 1)) * 8;
+    }
+
+    St st0, st1;
+    const int nchunks = a.c / kRC;
+    auto load = [&](St& r, int ch) {
+        const int r0 = (ch < nchunks ? ch : nchunks - 1) * kRC;
+#pragma unroll
+        for (int k = 0; k < SVI; ++k) {
+            const uint16_t* p = sp[k] + (int64_t)r0 * plane;
+#pragma unroll
+            for (int c8 = 0; c8 < 8; ++c8) {
+                const u32x2 v = load8(p + c8 * plane);
+                r.sd[k][2 * c8] = v[0];
+                r.sd[k][2 * c8 + 1] = v[1];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < FI; ++k) {
+            const uint16_t* p = fp[k] + r0 * T;
+#pragma unroll
+            for (int v4 = 0; v4 < T; ++v4) {
+                const u32x4 v = load16(p + 8 * v4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r.fd[k][4 * v4 + e] = v[e];
+            }
+        }
+    };
+    // part t of the stores of one stage: filter tap t, and strip position t (< 4)
+    auto part = [&](const St& r, uint16_t* stg, int t) {
+        if (t < T) {
+            const int u = t % FH, v = t / FH, nat = u * FW + v;
+#pragma unroll
+            for (int k = 0; k < FI; ++k) {
+                u32x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    o[e] = elem16(r.fd[k], (2 * e) * T + nat) | (elem16(r.fd[k], (2 * e + 1) * T + nat) << 16);
+                store16(stg + f_off + fdst[k] + t * BM * 8, o);
+            }
+        }
+        if (t < 4) {
+#pragma unroll
+            for (int k = 0; k < SVI; ++k) {
+                u32x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t w0 = r.sd[k][(2 * e) * 2 + t / 2];
+                    const uint32_t w1 = r.sd[k][(2 * e + 1) * 2 + t / 2];
+                    o[e] = (t & 1) ? hi_pair(w0, w1) : lo_pair(w0, w1);
+                }
+                store16(stg + sdst[k] + t * 8, o);
+            }
+        }
+    };
+
+    f32x16 acc[NJ][NP];
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
+
+    // chunk 0 into stage 0; chunk 1 in flight
+    load(st0, 0);
+#pragma unroll
+    for (int t = 0; t < (T > 4 ? T : 4); ++t) part(st0, lds, t);
+    load(st1, 1);
+
+    auto step = [&](int ch, St& r_ld, St& r_st) {
+        const uint16_t* cur = lds + (ch & 1) * a.stage;
+        uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        load(r_ld, ch + 2);
+        __builtin_amdgcn_sched_barrier(0);   // keep the loads at the head of the step
+        const uint16_t* F = cur + f_off;
+        bf16x8 a0[NJ], b0[NP], a1[NJ], b1[NP];
+        auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
+#pragma unroll
+            for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * 8 + fo[jb]);
+#pragma unroll
+            for (int pb = 0; pb < NP; ++pb) bv[pb] = frag(cur + t * 8 + so[pb]);
+        };
+        auto mm = [&](const bf16x8 (&av)[NJ], const bf16x8 (&bv)[NP]) {
+#pragma unroll
+            for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+                for (int pb = 0; pb < NP; ++pb)
+                    acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
+        };
+        ld(a0, b0, 0);
+        int t = 0;
+#pragma unroll
+        for (; t + 2 <= T; t += 2) {
+            ld(a1, b1, t + 1);
+            mm(a0, b0);
+            part(r_st, nxt, t);
+            if (t + 2 < T) ld(a0, b0, t + 2);
+            mm(a1, b1);
+            part(r_st, nxt, t + 1);
+        }
+        if (t < T) {
+            mm(a0, b0);
+            part(r_st, nxt, t);
+        }
+#pragma unroll
+        for (int t2 = T; t2 < 4; ++t2) part(r_st, nxt, t2);   // strip positions when T < 4
+    };
+    int ch = 0;
+    for (; ch + 2 <= nchunks; ch += 2) {
+        step(ch, st0, st1);
+        step(ch + 1, st1, st0);
+    }
+    if (ch < nchunks) step(ch, st0, st1);
+
+    // D[row][col]: col = lane%32 (pixel), row = 8*(v/4) + 4*(lane/32) + v%4 (channel)
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb) {
+            if (!pvalid[pb]) continue;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int j = j0 + wj * TJ + jb * 32 + 8 * (v >> 2) + 4 * kl + (v & 3);
+                a.y[yoff[pb] + (int64_t)j * a.howo] = acc[jb][pb][v];
+            }
+        }
+}
+
 template <int FH, int FW, int BM, int BN, int TJ, int TP, bool FVEC>
-void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int smode, hipStream_t stream) {
-    auto kern = smode == kStripVec      ? conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripVec, FVEC>
-                : smode == kStripScalar ? conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripScalar, FVEC>
-                                        : conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripFused, FVEC>;
+void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int smode, int svi, hipStream_t stream) {
+    auto kern = smode == kStripVec      ? (svi == 1 ? conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripVec, FVEC, 1>
+                                                    : conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripVec, FVEC, 2>)
+                : smode == kStripScalar ? conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripScalar, FVEC, 1>
+                                        : conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripFused, FVEC, 1>;
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
+}
+
+template <int FH, int FW, int BM, int BN, int TJ, int TP>
+void launch_fast_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int svi, hipStream_t stream) {
+    auto kern = svi == 1 ? conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 1>
+                         : conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 2>;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
@@ -453,9 +723,18 @@ void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int smode, hipSt
 
 template <int FH, int FW, bool FVEC>
 void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode, hipStream_t stream) {
-    if (p.bm == 128) launch_cfg<FH, FW, 128, 128, 64, 64, FVEC>(a, blocks, p.lds_bytes, smode, stream);
-    else if (p.bn == 128) launch_cfg<FH, FW, 64, 128, 32, 64, FVEC>(a, blocks, p.lds_bytes, smode, stream);
-    else launch_cfg<FH, FW, 64, 64, 32, 32, FVEC>(a, blocks, p.lds_bytes, smode, stream);
+    const int svi = p.strip_items > kConvThreads ? 2 : 1;
+    if constexpr (FVEC) {
+        if (smode == kStripVec && a.c % kRC == 0 && a.k % p.bm == 0) {
+            if (p.bm == 128) launch_fast_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, svi, stream);
+            else if (p.bn == 128) launch_fast_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, svi, stream);
+            else launch_fast_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, svi, stream);
+            return;
+        }
+    }
+    if (p.bm == 128) launch_cfg<FH, FW, 128, 128, 64, 64, FVEC>(a, blocks, p.lds_bytes, smode, svi, stream);
+    else if (p.bn == 128) launch_cfg<FH, FW, 64, 128, 32, 64, FVEC>(a, blocks, p.lds_bytes, smode, svi, stream);
+    else launch_cfg<FH, FW, 64, 64, 32, 32, FVEC>(a, blocks, p.lds_bytes, smode, svi, stream);
 }
 
 // Filter sizes with a compile-time kernel (16-byte filter loads).
@@ -465,8 +744,14 @@ bool known_filter(const Geometry& g) {
 
 }  // namespace
 
-// Window-tensor planes that are whole 16-byte vectors allow 16-byte strip loads.
-bool bf16_strips_vec(const Geometry& g) { return ((g.ho * g.row_len) & 7) == 0; }
+// Strips are loaded in groups of 4 elements (8 bytes) when window-tensor
+// planes and rows are whole groups.
+bool bf16_strips_vec(const Geometry& g) { return ((g.ho * g.row_len) & 3) == 0 && (g.row_len & 3) == 0; }
+
+// LDS row pitch of the channel-inner strips: congruent to sw*Fh*Wo mod 16.
+int64_t bf16_cl_pitch(const Geometry& g) {
+    return g.row_len + mod16((int)((g.sw * g.fh * g.wo - g.row_len) % 16));
+}
 
 // Tile candidates in order of preference; the first that fits (LDS, and the
 // per-thread staging registers of every strip and filter item) and gives
@@ -479,25 +764,31 @@ ConvPlan plan_conv_bf16(const Geometry& g) {
     const int ncfg = g.k > 64 ? 3 : 2;
     const bool fvec = known_filter(g) && ((g.c * g.taps) & 7) == 0;
     const bool svec = bf16_strips_vec(g);
+    const int64_t pitch = bf16_cl_pitch(g);
     ConvPlan best;
     int64_t best_blocks = 0;
     for (int ci = 0; ci < ncfg; ++ci) {
         const TileCfg t = cfgs[ci];
-        const int64_t cap_plain = strip_capacity(g, t.bn, 0);
-        const int64_t cap_vec = strip_capacity(g, t.bn, 8);
-        const int64_t cap = svec ? std::max(cap_plain, cap_vec) : cap_plain;
-        if (2 * cap_plain > (int64_t)kConvThreads * kStripScalarItems) continue;
-        if (svec && 2 * ((cap_vec + 7) / 8) > (int64_t)kConvThreads * kStripVecItems) continue;
+        const int64_t run_plain = strip_capacity(g, t.bn, 0);
+        const int64_t run_vec = strip_capacity(g, t.bn, 4);
+        if (2 * run_plain > (int64_t)kConvThreads * kStripScalarItems) continue;
+        const int64_t vec_items = 2 * ((run_vec + 3) / 4);   // 4-element groups x 2 halves
+        if (svec && vec_items > (int64_t)kConvThreads * kStripVecItems) continue;
         if (!fvec && 2 * g.taps * t.bm > (int64_t)kConvThreads * kFilterScalarItems) continue;
-        const int64_t stage = (cap + g.taps * t.bm) * kRC;   // elements
+        const int64_t ext = cl_extent_bound(g, t.bn, pitch);
+        const int64_t pb = ext + mod16((int)((2 - ext) % 16));       // = 2 mod 16
+        const int64_t fpb = g.taps * t.bm + 8;                        // = 8 mod 16
+        const int64_t stage = 16 * (pb + fpb);                       // elements
         const int64_t lds = 2 * stage * 2;
-        if (lds > kConvLdsMaxBytes) continue;
+        if (lds > kConvLdsMaxBytes || stage > (int64_t(1) << 30)) continue;
         ConvPlan p;
         p.kind = ConvPlan::kBf16Lds;
         p.bm = t.bm; p.bn = t.bn; p.rc = kRC; p.tc = (int)g.taps;
-        p.strip_cap = cap; p.stage = stage; p.lds_bytes = lds;
+        p.strip_cap = pb; p.stage = stage; p.lds_bytes = lds;
+        p.cl_pitch = pitch; p.cl_fpb = fpb;
         p.svec = svec ? 1 : 0;
         p.fvec = fvec ? 1 : 0;
+        p.strip_items = svec ? vec_items : 0;
         const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
         if (blocks >= 256) return p;
         if (blocks > best_blocks) { best = p; best_blocks = blocks; }
@@ -514,8 +805,12 @@ ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, c
     a.stage = (int)p.stage;
     a.tc = p.tc;
     a.svec = (!fused && p.svec) ? 1 : 0;
+    a.vchunk = 4;
     a.fvec = p.fvec;
-    a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 7) >> 3));
+    a.cl_pitch = (int)p.cl_pitch;
+    a.cl_pb = (int)p.strip_cap;
+    a.cl_fpb = (int)p.cl_fpb;
+    a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 3) >> 2));
     return a;
 }
 

@@ -48,6 +48,10 @@ struct ConvArgs {
     int rmid;              // input rows that the windows of a whole image use
     int ylo_mid;           // first of them
     FastDiv div_w, div_sh, div_rmid;   // by W, sh, max(rmid, 1)
+    // bf16: channel-inner LDS layout (positions of 16 bytes = 8 channels)
+    int cl_pitch;          // LDS positions per window-tensor row (>= row_len)
+    int cl_pb;             // positions per strip plane (one plane per 8-channel half)
+    int cl_fpb;            // positions per filter plane
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -174,6 +178,68 @@ __host__ __device__ inline RawRows raw_rows(const TileRuns& tr, const ConvArgs& 
     return r;
 }
 
+__host__ __device__ inline int mod16(int v) { return ((v % 16) + 16) % 16; }
+__host__ __device__ inline int round_up4(int v) { return (v + 3) & ~3; }
+
+// bf16 channel-inner LDS layout of one tile's strips: positions of 16 bytes
+// (8 channels), one plane per 8-channel half.  Row m of image segment s
+// starts at seg_base(s) + (m - seg_m(s))*cl_pitch - seg_q(s).  The row pitch
+// is congruent to sw*Fh*Wo and the segment bases to sw*Fh times the number
+// of tile pixels before them (mod 16 positions), so the windows of the
+// tile's flattened pixels P start at positions congruent to sw*Fh*P + sb0:
+// for odd sw*Fh, 16 consecutive pixels fall in 16 different 16-byte bank
+// groups.  sb0 is the 4-position alignment shift of the first run.
+struct ClLayout {
+    int sb0, sb1, sp, extent;
+    __host__ __device__ int seg_base(int s) const { return s == 0 ? sb0 : sb1 + (s - 1) * sp; }
+};
+
+__host__ __device__ inline ClLayout cl_layout(const TileRuns& tr, const ConvArgs& a) {
+    ClLayout c;
+    const int lp = a.cl_pitch, spx = a.sw * a.fh, hw = a.ho * a.wo;
+    const int last_col = (tr.n1 * a.sw + a.fw) * a.fh;   // end of the tile's last row
+    c.sb0 = tr.shift0;
+    const int m_end0 = tr.nseg == 1 ? tr.m1 : a.ho - 1;
+    const int end0 = c.sb0 + (m_end0 - tr.m0) * lp + round_up4(tr.nseg == 1 ? last_col : a.used_len) - tr.qa0;
+    if (tr.nseg == 1) {
+        c.sb1 = 0;
+        c.sp = 0;
+        c.extent = end0;
+        return c;
+    }
+    c.sb1 = end0 + mod16(spx * (hw - tr.m0 * a.wo - tr.n0) + c.sb0 - end0);
+    const int full = (a.ho - 1) * lp + round_up4(a.used_len);
+    c.sp = full + mod16(spx * hw - full);
+    c.extent = c.sb1 + (tr.nseg - 2) * c.sp + tr.m1 * lp + round_up4(last_col);
+    return c;
+}
+
+// LDS position of in-plane element e of segment s's window-tensor plane.
+__host__ __device__ inline int cl_pos(const ClLayout& c, const TileRuns& tr, const ConvArgs& a, int s, int e) {
+    const int row = (int)fast_div((uint32_t)e, a.div_row);
+    return c.seg_base(s) + (row - tr.seg_m(s)) * a.cl_pitch + (e - row * a.row_len) - tr.seg_q(s);
+}
+
+// LDS position of the window of pixel p, and the output offset of its
+// channel-0 element (pixels past the tile are clamped to its first pixel).
+__host__ __device__ inline int cl_pixel_base(const ClLayout& c, const TileRuns& tr, const ConvArgs& a, int p,
+                                             int64_t* yoff) {
+    const int g = (int)fast_div((uint32_t)p, a.div_wo);
+    const int n = p - g * a.wo;
+    const int i = (int)fast_div((uint32_t)g, a.div_ho);
+    const int m = g - i * a.ho;
+    const int s = i - tr.i0;
+    *yoff = (int64_t)i * a.k * a.howo + m * a.wo + n;
+    return c.seg_base(s) + (m - tr.seg_m(s)) * a.cl_pitch + n * a.sw * a.fh - tr.seg_q(s);
+}
+
+// Host bound of ClLayout::extent over the tiles of `bn` pixels.
+inline int64_t cl_extent_bound(const Geometry& g, int bn, int64_t pitch) {
+    const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
+    const int64_t nseg = std::min<int64_t>(dmax + 1, (bn - 1) / (g.ho * g.wo) + 2);
+    return 4 + (dmax + 1) * pitch + 20 * nseg;
+}
+
 // Launch plan of a convolution kernel (chosen on the host).
 struct ConvPlan {
     enum Kind { kNone, kF32Lds, kBf16Lds };
@@ -186,6 +252,9 @@ struct ConvPlan {
     int64_t sc = 0, fp = 0;  // fp32: LDS strides of strips and filter rows
     int64_t stage = 0;       // LDS elements per pipeline stage
     int64_t raw_pitch = 0;   // fused fp32: LDS floats per channel of the raw input rows
+    int64_t cl_pitch = 0;    // bf16: LDS positions per window-tensor row
+    int64_t cl_fpb = 0;      // bf16: positions per filter plane (strip planes: strip_cap)
+    int64_t strip_items = 0; // bf16, 16-byte strip loads: bound of the staging items per tile
     int svec = 0;            // unfused: 16-byte strip copies
     int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
@@ -293,6 +362,9 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.div_w = make_fastdiv((uint32_t)g.w);
     a.div_sh = make_fastdiv((uint32_t)g.sh);
     a.div_rmid = make_fastdiv((uint32_t)std::max(a.rmid, 1));
+    a.cl_pitch = a.row_len;
+    a.cl_pb = 0;
+    a.cl_fpb = 0;
     return a;
 }
 
