@@ -665,8 +665,11 @@ int choose_split(const Geometry& g) {
 }  // namespace
 
 ConvPlan plan_conv_f32(const Geometry& g) {
-    // Tiles in order of preference; the first that gives every CU two
-    // workgroups is taken, else the one with the most workgroups.  Both
+    // Tiles in order of preference; the first that gives every CU a
+    // workgroup is taken, else the one with the most workgroups.  (Larger
+    // tiles give each wave more independent accumulators and stage the
+    // filter less often; measured on the resnet 3x3 layer, 64x256 with 392
+    // workgroups beats 64x128 with 784.)  Both
     // pipeline stages together are sized for 80 KB of LDS (two workgroups per
     // CU); only shapes that fit nothing there use up to the full 160 KB.
     const TileCfg small_k[] = {{64, 256}, {64, 128}, {64, 64}};
@@ -704,7 +707,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
             if (pv.kind != ConvPlan::kNone) p = pv;
             if (p.kind == ConvPlan::kNone) continue;
             const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
-            if (blocks >= 2 * 256) return p;
+            if (blocks >= 256) return p;
             if (blocks > best_blocks) { best = p; best_blocks = blocks; }
         }
         if (best.kind != ConvPlan::kNone) return best;
