@@ -341,6 +341,10 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
         if (g.elem == 4 && p.lds_bytes + 4 * p.rc * p.raw_pitch > kConvLdsMaxBytes)
             r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * p.rc * p.raw_pitch));
+        if (g.elem == 4 && g.fh <= 3 && p.sc < p.strip_cap + g.fh + 64)
+            r.fail("conv: strip stride %lld leaves no spare expansion slots", (long long)p.sc);
+        if (g.elem == 4 && (p.raw_pitch & 63))
+            r.fail("conv: raw row pitch %lld is not a multiple of 64", (long long)p.raw_pitch);
     }
     if (bf16) {
         // two stages of two strip planes [strip_cap] and two filter planes

@@ -299,10 +299,13 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
 // expands are the same for every chunk and channel, so they are computed once
 // per kernel.  Lane l expands raw elements e = l + 64k (k < kExpandK) of each
 // of its channels; dst[k][i] is the strip offset (within a channel) of window
-// row m_lo + i, or the spare slot `trash` (past every strip extent, never
-// read by a window) when that row does not exist or holds no such position.
-constexpr int kExpandK = 8;
+// row m_lo + i, or, when that row does not exist or holds no such position,
+// the lane's own spare slot among the kExpandSpare positions that end every
+// channel's strip (past any window; one slot for many lanes of a store would
+// serialise it).  Entries are plain offsets, so a store needs no select.
+constexpr int kExpandK = 12;
 constexpr int kExpandMaxRaw = 64 * kExpandK;   // raw floats per channel
+constexpr int kExpandSpare = 64;               // spare strip positions per channel
 
 template <int FH>
 struct ExpandMap {
@@ -311,7 +314,7 @@ struct ExpandMap {
 
 template <int FH>
 __device__ inline void expand_map_build(ExpandMap<FH>& mp, const ConvArgs& a, const TileRuns& tr,
-                                        const RawRows& rr, int trash) {
+                                        const RawRows& rr) {
     const int lane = threadIdx.x & 63;
     const int n = rr.rtot * a.w_in;
     const int nseg = tr.nseg;
@@ -319,7 +322,7 @@ __device__ inline void expand_map_build(ExpandMap<FH>& mp, const ConvArgs& a, co
     for (int k = 0; k < kExpandK; ++k) {
         const int e = lane + 64 * k;
 #pragma unroll
-        for (int i = 0; i < FH; ++i) mp.dst[k][i] = trash;
+        for (int i = 0; i < FH; ++i) mp.dst[k][i] = a.sc - kExpandSpare + lane;
         if (e < n) {
             const int r = (int)fast_div((uint32_t)e, a.div_w);
             const int xx = e - r * a.w_in;
@@ -348,16 +351,18 @@ template <int FH>
 __device__ inline void expand_map_apply(float* S, const float* X, const ExpandMap<FH>& mp,
                                         const ConvArgs& a, const TileRuns& tr, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int ngroups = a.raw_pitch >> 6;   // raw pitch is a multiple of 64
     for (int rc = wave; rc < rc_act; rc += 4) {
         const float* xl = X + rc * a.raw_pitch + lane;
         float* sl = S + rc * a.sc;
-        float v[kExpandK];
 #pragma unroll
-        for (int k = 0; k < kExpandK; ++k) v[k] = 64 * k + lane < a.raw_pitch ? xl[64 * k] : 0.0f;
+        for (int k = 0; k < kExpandK; ++k) {
+            if (k < ngroups) {
+                const float v = xl[64 * k];
 #pragma unroll
-        for (int k = 0; k < kExpandK; ++k)
-#pragma unroll
-            for (int i = 0; i < FH; ++i) sl[mp.dst[k][i]] = v[k];
+                for (int i = 0; i < FH; ++i) sl[mp.dst[k][i]] = v;
+            }
+        }
     }
     if (rc_stage > rc_act) zero_channels(S, a, tr, rc_act, rc_stage);
 }
@@ -524,9 +529,12 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     const int nchunks = (a.c + a.rc - 1) / a.rc;
     float* X = S + a.raw_off;
     RawRows rr{};
-    constexpr int FHM = FH > 0 ? FH : 1;
+    // the map holds FH destinations per element: kept for filters of up to
+    // three rows (larger ones expand with the per-element decode)
+    constexpr bool MAP = RAW && FH > 0 && FH <= 3;
+    constexpr int FHM = MAP ? FH : 1;
     ExpandMap<FHM> emap;
-    const bool use_map = RAW && FH > 0 && a.raw_pitch <= kExpandMaxRaw;
+    const bool use_map = MAP && a.raw_pitch <= kExpandMaxRaw;
     {
         const int rc_act = min(a.rc, a.c);
         const int rc_stage = ROWS ? rc_act : a.rc;
@@ -536,7 +544,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
                 for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
             stage_raw(X, a, tr, rr, 0, rc_act);
             stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
-            if (use_map) expand_map_build<FHM>(emap, a, tr, rr, a.strip_cap);
+            if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
             __syncthreads();   // zeros written, raw rows of chunk 0 landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
             else expand_raw(S, X, a, tr, rr, rc_act, rc_stage);
@@ -622,9 +630,23 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, bool fuse
 // channels (stride sc) and bm filter rows (stride fp, odd so that 32
 // consecutive rows fall in different banks), with slack for the reads past
 // the last tap that a dead k-slot makes.
-int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, bool fvec, int64_t* sc,
-                   int64_t* fp, int64_t* stage) {
+int64_t f32_layout(const Geometry& g, int bm, int rc, int64_t cap, bool fvec, int split,
+                   int64_t* sc, int64_t* fp, int64_t* stage) {
     *sc = (cap + g.fh + 3) & ~int64_t(3);
+    // fused fp32 with filters of up to 3 rows: spare expansion slots per strip
+    if (g.elem == 4 && g.fh <= 3) *sc += kExpandSpare;
+    // channel split: the second k-slot reads (rc/2)*sc floats after the first;
+    // (rc/2)*sc = 32 mod 64 puts the two half-waves' window reads on
+    // disjoint banks (all 64 lanes conflict-free for an odd pixel stride)
+    if (!split) {
+        const int64_t half = rc / 2;
+        for (int i = 0; i < 16; ++i) {
+            if ((half * (*sc + 4 * i)) % 64 == 32) {
+                *sc += 4 * i;
+                break;
+            }
+        }
+    }
     *fp = (int64_t)rc * g.taps + g.fw + 1;
     if (fvec) {
         // 16-byte rows: a multiple of 4 floats, and not of 8, so that 32
@@ -649,8 +671,9 @@ bool filter_vec(const Geometry& g, int rc) {
 bool strips_vec(const Geometry& g) { return g.elem == 4 && ((g.ho * g.row_len) & 3) == 0; }
 
 // LDS floats per channel for the raw input rows of a fused fp32 tile.
+// (a multiple of 64: the expansion map reads whole groups of 64)
 int64_t raw_pitch_f32(const Geometry& g, int bn) {
-    return (raw_rows_bound(g, bn) * g.w + 3) & ~int64_t(3);
+    return (raw_rows_bound(g, bn) * g.w + 63) & ~int64_t(63);
 }
 
 // Zero reduction slots each way of splitting the two k-slots adds: one zero
@@ -691,7 +714,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
             for (int rc = step; rc <= rc_max; rc += step) {
                 int64_t sc, fp, st;
                 const bool fv = filter_vec(g, rc);
-                const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, &sc, &fp, &st);
+                const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, split, &sc, &fp, &st);
                 const int64_t raw = g.elem == 4 ? raw_pitch_f32(g, t.bn) : 0;
                 if (lds + rc * raw * 4 > budget) continue;
                 ConvPlan q;
