@@ -254,7 +254,40 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
         if (items > cap_items)
             r.fail("%s tile %lld: %lld strip items, registers hold %lld", what, (long long)t,
                    (long long)items, (long long)cap_items);
-        if (a.svec) {
+        const bool raw_items = fused && p.fused_fast;
+        if (raw_items) {
+            // fused kernel from raw row items: every item's source inside x,
+            // its destinations the strip positions of the window-tensor
+            // elements it holds (spare slots aside)
+            const RawRows rw = raw_rows(tr, a);
+            const int nitems = rw.rtot * (int)g.w;
+            if (nitems > kConvThreads * kBf16FusedItems || (g.w & 1))
+                r.fail("%s tile %lld: %d raw items, registers hold %d", what, (long long)t, nitems,
+                       kConvThreads * kBf16FusedItems);
+            for (int q = 0; q < nitems && r.violations < 16; ++q) {
+                const int e0 = 2 * (q >> 1);
+                const int rr2 = e0 / (int)g.w, xx = e0 - rr2 * (int)g.w;
+                int sg = rr2 < rw.r0 ? 0 : 1 + (rr2 - rw.r0) / std::max(a.rmid, 1);
+                if (sg > tr.nseg - 1) sg = tr.nseg - 1;
+                const int yy = sg == 0 ? rw.ylo0 + rr2 : a.ylo_mid + (rr2 - rw.r0 - (sg - 1) * a.rmid);
+                if (yy < 0 || yy >= g.h || xx + 1 >= g.w + 1 || tr.i0 + sg >= g.n) {
+                    r.fail("%s tile %lld: item %d reads x row %d col %d of image %d", what, (long long)t, q, yy,
+                           xx, tr.i0 + sg);
+                    break;
+                }
+                const int m_st = tr.seg_m(sg), q_st = tr.seg_q(sg), len = tr.seg_len(sg);
+                const int m_end = sg == tr.nseg - 1 ? tr.m1 : (int)g.ho - 1;
+                for (int m = m_st; m <= m_end; ++m) {
+                    const int u = yy + (int)g.ph - m * (int)g.sh;
+                    if (u < 0 || u >= g.fh) continue;
+                    for (int h = 0; h < 2; ++h) {
+                        const int e_in = m * (int)g.row_len + (xx + h + (int)g.pw) * (int)g.fh + u;
+                        const int rel = e_in - (m_st * (int)g.row_len + q_st);
+                        if (rel >= 0 && rel < len) put(sg, e_in, cl_pos(cl, tr, a, sg, e_in));
+                    }
+                }
+            }
+        } else if (a.svec) {
             const int start0 = tr.m0 * a.row_len + tr.qa0 - tr.shift0;
             for (int c = 0; c < tr.ck_total && r.violations < 16; ++c) {
                 int s = 0, cs = c;
@@ -299,8 +332,15 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
             const int mm = gi - ii * (int)g.ho, nn = px - gi * (int)g.wo;
             const int s = ii - tr.i0;
             for (int tp = 0; tp < g.taps; ++tp) {
-                const int64_t want = (int64_t)s * plane + (int64_t)mm * g.row_len + (int64_t)nn * g.sw * g.fh + tp;
-                if (base + tp < 0 || base + tp >= pb || src[base + tp] != want) {
+                const int64_t e = (int64_t)mm * g.row_len + (int64_t)nn * g.sw * g.fh + tp;
+                int64_t want = (int64_t)s * plane + e;
+                if (raw_items) {
+                    // padding elements are never written (zero since the start)
+                    const int64_t qq = e % g.row_len;
+                    const int64_t yy = mm * g.sh + qq % g.fh - g.ph, xx = qq / g.fh - g.pw;
+                    if (yy < 0 || yy >= g.h || xx < 0 || xx >= g.w) want = -1;
+                }
+                if (base + tp < 0 || base + tp >= pb - kBf16Spare || src[base + tp] != want) {
                     r.fail("%s tile %lld: pixel %d tap %d reads LDS %d", what, (long long)t, px, tp, base + tp);
                     break;
                 }

@@ -52,6 +52,7 @@ __device__ inline uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu
 __device__ inline uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
 
 __device__ inline u32x4 load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ inline u32x2 load8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
@@ -701,6 +702,285 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
         }
 }
 
+// Fused kernel for the same common case, and x rows of an even number of
+// elements: the strips are built on chip from the input rows the tile uses.
+// An item is a pair of neighbouring input elements of one row for the 8
+// channels of one half: each wave copies its items into LDS with 4-byte DMA
+// (a DMA lane may read any address, so the 8 channels of an item land side
+// by side, 32 bytes per item), and after the MFMAs of the chunk it expands
+// them: transposed to two 8-channel positions and written to every strip
+// position that holds them, one per window row m with filter row
+// u = y + ph - m*sh.  These destinations do not change between chunks, so
+// they are computed once; the ones outside the tile's runs go to the lane's
+// own spare slot at the end of the strip plane.  A wave only reads items it
+// copied, so it waits for its own copies; the chunk barrier publishes the
+// strips.  Padding positions are zeroed once.
+template <int FH>
+struct FusedMap {
+    int dst[2][FH];   // element offsets in a stage of the two positions, per window-row slot
+};
+
+template <int FH, int FW, int BM, int BN, int TJ, int TP>
+__global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs a) {
+    static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+    constexpr int NJ = TJ / 32, NP = TP / 32;
+    constexpr int WAVES_P = BN / TP;
+    constexpr int T = FH * FW;
+    constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
+    constexpr int IPT = kBf16FusedItems;   // items per thread
+    using St = FastStage<FH, FW, BM, NJ, NP, 1>;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+    const int f_off = 2 * a.cl_pb * 8;
+    uint32_t* X = reinterpret_cast<uint32_t*>(lds + 2 * a.stage);   // 8 dwords per item
+
+    const int jtile = blockIdx.x % a.num_jtiles;
+    const int ptile = blockIdx.x / a.num_jtiles;
+    const int j0 = jtile * BM;
+
+    TileRuns tr;
+    tr.init(ptile, BN, a);
+    const ClLayout cl = cl_layout(tr, a);
+    const RawRows rr = raw_rows(tr, a);
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wj = wave / WAVES_P, wp_ = wave % WAVES_P;
+    const int l32 = lane & 31, kl = lane >> 5;
+
+    int so[NP];
+    int64_t yoff[NP];
+    bool pvalid[NP];
+#pragma unroll
+    for (int pb = 0; pb < NP; ++pb) {
+        int p = tr.p0 + wp_ * TP + pb * 32 + l32;
+        pvalid[pb] = p <= tr.plast;
+        if (!pvalid[pb]) p = tr.p0;
+        so[pb] = (kl * a.cl_pb + cl_pixel_base(cl, tr, a, p, &yoff[pb])) * 8;
+    }
+    int fo[NJ];
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) fo[jb] = (kl * a.cl_fpb + wj * TJ + jb * 32 + l32) * 8;
+
+    const uint16_t* xsrc = static_cast<const uint16_t*>(a.src);
+    const uint16_t* wsrc = static_cast<const uint16_t*>(a.w);
+    const int64_t xplane = (int64_t)a.h * a.w_in;
+    const int nitems = rr.rtot * a.w_in;   // (rtot*W/2 pairs) x 2 halves
+
+    // item q: half g = q & 1, element pair e0 = 2*(q >> 1) of the raw rows
+    // -> raw row r, column xx (even), segment s, input row yy
+    auto item_at = [&](int q, int* s, int* yy, int* xx) {
+        const int e0 = 2 * (q >> 1);
+        const int r = (int)fast_div((uint32_t)e0, a.div_w);
+        *xx = e0 - r * a.w_in;
+        *s = r < rr.r0 ? 0 : 1 + (int)fast_div((uint32_t)(r - rr.r0), a.div_rmid);
+        if (*s > tr.nseg - 1) *s = tr.nseg - 1;
+        *yy = *s == 0 ? rr.ylo0 + r : a.ylo_mid + (r - rr.r0 - (*s - 1) * a.rmid);
+    };
+    // DMA sources: instruction i (of 8 per item block of this thread's wave)
+    // covers items base + 8i .. +7, lane L: item base + 8i + L/8, channel L%8
+    int64_t dsrc[IPT][8];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            int q = wave * 64 + j * kConvThreads + 8 * i + (lane >> 3);
+            if (q >= nitems) q = q & 1;   // a valid address; the item is never expanded
+            int sg, yy, xx;
+            item_at(q, &sg, &yy, &xx);
+            dsrc[j][i] = ((int64_t)(tr.i0 + sg) * a.c + 8 * (q & 1) + (lane & 7)) * xplane +
+                         (int64_t)yy * a.w_in + xx;
+        }
+    // expansion map of this thread's items
+    FusedMap<FH> mp[IPT];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+        const int q = threadIdx.x + j * kConvThreads;
+        const int g = q & 1;
+        const int spare = (g * a.cl_pb + a.cl_pb - kBf16Spare + lane) * 8;
+#pragma unroll
+        for (int i = 0; i < FH; ++i) mp[j].dst[0][i] = mp[j].dst[1][i] = spare;
+        if (q < nitems) {
+            int sg, yy, xx;
+            item_at(q, &sg, &yy, &xx);
+            const int m_st = sg == 0 ? tr.m0 : 0, q_st = sg == 0 ? tr.qa0 : 0;
+            const int len = sg == 0 ? tr.len0 : (sg == tr.nseg - 1 ? tr.len_last : tr.len_mid);
+            const int m_end = sg == tr.nseg - 1 ? tr.m1 : a.ho - 1;
+            const int t0 = yy + a.ph - a.fh + 1;
+            int m_lo = t0 <= 0 ? 0 : (int)fast_div((uint32_t)(t0 + a.sh - 1), a.div_sh);
+            if (m_lo < m_st) m_lo = m_st;
+            int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
+            if (m_hi > m_end) m_hi = m_end;
+#pragma unroll
+            for (int i = 0; i < FH; ++i) {
+                const int m = m_lo + i;
+                if (m > m_hi) continue;
+                const int u = yy + a.ph - m * a.sh;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int e_in = m * a.row_len + (xx + h + a.pw) * a.fh + u;
+                    const int rel = e_in - (m_st * a.row_len + q_st);
+                    if (xx + h < a.w_in && (unsigned)rel < (unsigned)len)
+                        mp[j].dst[h][i] = (g * a.cl_pb + cl_pos(cl, tr, a, sg, e_in)) * 8;
+                }
+            }
+        }
+    }
+    const uint16_t* fp[FI];
+    int fdst[FI];
+#pragma unroll
+    for (int k = 0; k < FI; ++k) {
+        const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
+        fp[k] = wsrc + ((int64_t)(j0 + (q >> 1)) * a.c + 8 * (q & 1)) * T;
+        fdst[k] = ((q & 1) * a.cl_fpb + (q >> 1)) * 8;
+    }
+
+    St st0, st1;
+    const int nchunks = a.c / kRC;
+    auto load_f = [&](St& r, int ch) {
+        const int r0 = (ch < nchunks ? ch : nchunks - 1) * kRC;
+#pragma unroll
+        for (int k = 0; k < FI; ++k) {
+            const uint16_t* p = fp[k] + r0 * T;
+#pragma unroll
+            for (int v4 = 0; v4 < T; ++v4) {
+                const u32x4 v = load16(p + 8 * v4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r.fd[k][4 * v4 + e] = v[e];
+            }
+        }
+    };
+    auto part_f = [&](const St& r, uint16_t* stg, int t) {
+        const int u = t % FH, v = t / FH, nat = u * FW + v;
+#pragma unroll
+        for (int k = 0; k < FI; ++k) {
+            u32x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                o[e] = elem16(r.fd[k], (2 * e) * T + nat) | (elem16(r.fd[k], (2 * e + 1) * T + nat) << 16);
+            store16(stg + f_off + fdst[k] + t * BM * 8, o);
+        }
+    };
+    auto dma = [&](int ch) {
+        const int64_t off = (int64_t)(ch < nchunks ? ch : nchunks - 1) * kRC * xplane;
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            if (wave * 64 + j * kConvThreads < nitems) {   // this wave's block has items
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    __builtin_amdgcn_global_load_lds(
+                        reinterpret_cast<const uint32_t*>(xsrc + dsrc[j][i] + off),
+                        (lds_u32*)(X + (wave * 64 + j * kConvThreads + 8 * i) * 8), 4, 0, 0);
+            }
+        }
+    };
+    auto expand = [&](uint16_t* stg) {
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            const int q = threadIdx.x + j * kConvThreads;
+            if (q < nitems) {
+                const u32x4 v0 = *reinterpret_cast<const u32x4*>(X + q * 8);
+                const u32x4 v1 = *reinterpret_cast<const u32x4*>(X + q * 8 + 4);
+                const uint32_t d[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+                u32x4 o0, o1;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    o0[e] = lo_pair(d[2 * e], d[2 * e + 1]);
+                    o1[e] = hi_pair(d[2 * e], d[2 * e + 1]);
+                }
+#pragma unroll
+                for (int i = 0; i < FH; ++i) {
+                    store16(stg + mp[j].dst[0][i], o0);
+                    store16(stg + mp[j].dst[1][i], o1);
+                }
+            }
+        }
+    };
+
+    f32x16 acc[NJ][NP];
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
+
+    // strip planes of both stages start at zero (the padding stays zero)
+    {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        for (int st = 0; st < 2; ++st)
+            for (int e = threadIdx.x; e < 2 * a.cl_pb; e += kConvThreads) store16(lds + st * a.stage + e * 8, z);
+    }
+    load_f(st0, 0);
+    dma(0);
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");   // zeros before strips
+#pragma unroll
+    for (int t = 0; t < T; ++t) part_f(st0, lds, t);
+    expand(lds);
+    load_f(st1, 1);
+
+    auto step = [&](int ch, St& r_ld, St& r_st) {
+        const uint16_t* cur = lds + (ch & 1) * a.stage;
+        uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        dma(ch + 1);
+        load_f(r_ld, ch + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        const uint16_t* F = cur + f_off;
+        bf16x8 a0[NJ], b0[NP], a1[NJ], b1[NP];
+        auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
+#pragma unroll
+            for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * 8 + fo[jb]);
+#pragma unroll
+            for (int pb = 0; pb < NP; ++pb) bv[pb] = frag(cur + t * 8 + so[pb]);
+        };
+        auto mm = [&](const bf16x8 (&av)[NJ], const bf16x8 (&bv)[NP]) {
+#pragma unroll
+            for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+                for (int pb = 0; pb < NP; ++pb)
+                    acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
+        };
+        ld(a0, b0, 0);
+        int t = 0;
+#pragma unroll
+        for (; t + 2 <= T; t += 2) {
+            ld(a1, b1, t + 1);
+            mm(a0, b0);
+            part_f(r_st, nxt, t);
+            if (t + 2 < T) ld(a0, b0, t + 2);
+            mm(a1, b1);
+            part_f(r_st, nxt, t + 1);
+        }
+        if (t < T) {
+            mm(a0, b0);
+            part_f(r_st, nxt, t);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of chunk ch+1
+        expand(nxt);
+    };
+    int ch = 0;
+    for (; ch + 2 <= nchunks; ch += 2) {
+        step(ch, st0, st1);
+        step(ch + 1, st1, st0);
+    }
+    if (ch < nchunks) step(ch, st0, st1);
+
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+        for (int pb = 0; pb < NP; ++pb) {
+            if (!pvalid[pb]) continue;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int j = j0 + wj * TJ + jb * 32 + 8 * (v >> 2) + 4 * kl + (v & 3);
+                a.y[yoff[pb] + (int64_t)j * a.howo] = acc[jb][pb][v];
+            }
+        }
+}
+
 template <int FH, int FW, int BM, int BN, int TJ, int TP, bool FVEC>
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int smode, int svi, hipStream_t stream) {
     auto kern = smode == kStripVec      ? (svi == 1 ? conv_bf16_kernel<FH, FW, BM, BN, TJ, TP, kStripVec, FVEC, 1>
@@ -721,9 +1001,26 @@ void launch_fast_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int svi, hi
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
 }
 
+template <int FH, int FW, int BM, int BN, int TJ, int TP>
+void launch_fused_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, hipStream_t stream) {
+    auto kern = conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP>;
+    lds += kConvThreads * kBf16FusedItems * 32;   // raw row items
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
+}
+
 template <int FH, int FW, bool FVEC>
 void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode, hipStream_t stream) {
     const int svi = p.strip_items > kConvThreads ? 2 : 1;
+    if constexpr (FVEC && FH <= 3) {
+        if (smode == kStripFused && p.fused_fast) {
+            if (p.bm == 128) launch_fused_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, stream);
+            else if (p.bn == 128) launch_fused_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, stream);
+            else launch_fused_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, stream);
+            return;
+        }
+    }
     if constexpr (FVEC) {
         if (smode == kStripVec && a.c % kRC == 0 && a.k % p.bm == 0) {
             if (p.bm == 128) launch_fast_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, svi, stream);
@@ -775,12 +1072,18 @@ ConvPlan plan_conv_bf16(const Geometry& g) {
         const int64_t vec_items = 2 * ((run_vec + 3) / 4);   // 4-element groups x 2 halves
         if (svec && vec_items > (int64_t)kConvThreads * kStripVecItems) continue;
         if (!fvec && 2 * g.taps * t.bm > (int64_t)kConvThreads * kFilterScalarItems) continue;
-        const int64_t ext = cl_extent_bound(g, t.bn, pitch);
+        const int64_t ext = cl_extent_bound(g, t.bn, pitch) + kBf16Spare;
         const int64_t pb = ext + mod16((int)((2 - ext) % 16));       // = 2 mod 16
         const int64_t fpb = g.taps * t.bm + 8;                        // = 8 mod 16
         const int64_t stage = 16 * (pb + fpb);                       // elements
         const int64_t lds = 2 * stage * 2;
         if (lds > kConvLdsMaxBytes || stage > (int64_t(1) << 30)) continue;
+        // fused kernel from raw row items: whole 16-channel chunks, whole
+        // tiles of output channels, even rows, filters of up to 3 rows,
+        // and the items of every tile in the per-thread registers and LDS
+        const bool fused_fast = fvec && g.c % kRC == 0 && g.k % t.bm == 0 && g.w % 2 == 0 && g.fh <= 3 &&
+                                raw_rows_bound(g, t.bn) * g.w <= (int64_t)kConvThreads * kBf16FusedItems &&
+                                lds + kConvThreads * kBf16FusedItems * 32 <= kConvLdsMaxBytes;
         ConvPlan p;
         p.kind = ConvPlan::kBf16Lds;
         p.bm = t.bm; p.bn = t.bn; p.rc = kRC; p.tc = (int)g.taps;
@@ -789,6 +1092,7 @@ ConvPlan plan_conv_bf16(const Geometry& g) {
         p.svec = svec ? 1 : 0;
         p.fvec = fvec ? 1 : 0;
         p.strip_items = svec ? vec_items : 0;
+        p.fused_fast = fused_fast ? 1 : 0;
         const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
         if (blocks >= 256) return p;
         if (blocks > best_blocks) { best = p; best_blocks = blocks; }

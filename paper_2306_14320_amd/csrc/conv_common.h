@@ -255,6 +255,7 @@ struct ConvPlan {
     int64_t cl_pitch = 0;    // bf16: LDS positions per window-tensor row
     int64_t cl_fpb = 0;      // bf16: positions per filter plane (strip planes: strip_cap)
     int64_t strip_items = 0; // bf16, 16-byte strip loads: bound of the staging items per tile
+    int fused_fast = 0;      // bf16: the fused kernel builds strips from raw row items
     int svec = 0;            // unfused: 16-byte strip copies
     int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
@@ -272,6 +273,8 @@ constexpr int kBf16Chunk = 16;
 constexpr int kBf16StripVecItems = 2;
 constexpr int kBf16StripScalarItems = 8;
 constexpr int kBf16FilterScalarItems = 16;
+constexpr int kBf16Spare = 64;        // spare positions at the end of every strip plane
+constexpr int kBf16FusedItems = 1;    // fused kernel: raw items per thread (2 elements x 8 channels)
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
 
