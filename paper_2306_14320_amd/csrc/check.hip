@@ -379,8 +379,11 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: channel split with an odd chunk of %d", p.rc);
         if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
-        if (g.elem == 4 && p.lds_bytes + 4 * p.rc * p.raw_pitch > kConvLdsMaxBytes)
-            r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * p.rc * p.raw_pitch));
+        // raw rows: two buffers with 768 floats of slack each when the map is used
+        const int64_t mx = 64 * kF32ExpandGroups;
+        const int64_t rawf = (g.fh <= 3 && p.raw_pitch <= mx) ? 2 * (p.rc * p.raw_pitch + mx) : p.rc * p.raw_pitch;
+        if (g.elem == 4 && p.lds_bytes + 4 * rawf > kConvLdsMaxBytes)
+            r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * rawf));
         if (g.elem == 4 && g.fh <= 3 && p.sc < p.strip_cap + g.fh + 64)
             r.fail("conv: strip stride %lld leaves no spare expansion slots", (long long)p.sc);
         if (g.elem == 4 && (p.raw_pitch & 63))

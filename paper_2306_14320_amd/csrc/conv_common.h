@@ -273,6 +273,7 @@ constexpr int kBf16Chunk = 16;
 constexpr int kBf16StripVecItems = 2;
 constexpr int kBf16StripScalarItems = 8;
 constexpr int kBf16FilterScalarItems = 16;
+constexpr int kF32ExpandGroups = 10;  // fused fp32 expansion map: raw floats per channel / 64
 constexpr int kBf16Spare = 64;        // spare positions at the end of every strip plane
 constexpr int kBf16FusedItems = 1;    // fused kernel: raw items per thread (2 elements x 8 channels)
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,

@@ -303,7 +303,7 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
 // the lane's own spare slot among the kExpandSpare positions that end every
 // channel's strip (past any window; one slot for many lanes of a store would
 // serialise it).  Entries are plain offsets, so a store needs no select.
-constexpr int kExpandK = 12;
+constexpr int kExpandK = kF32ExpandGroups;
 constexpr int kExpandMaxRaw = 64 * kExpandK;   // raw floats per channel
 constexpr int kExpandSpare = 64;               // spare strip positions per channel
 
@@ -355,12 +355,15 @@ __device__ inline void expand_map_apply(float* S, const float* X, const ExpandMa
     for (int rc = wave; rc < rc_act; rc += 4) {
         const float* xl = X + rc * a.raw_pitch + lane;
         float* sl = S + rc * a.sc;
+        float v[kExpandK];   // all reads in flight before the first write (the
+                             // buffer ends with kExpandMaxRaw floats of slack)
+#pragma unroll
+        for (int k = 0; k < kExpandK; ++k) v[k] = xl[64 * k];
 #pragma unroll
         for (int k = 0; k < kExpandK; ++k) {
             if (k < ngroups) {
-                const float v = xl[64 * k];
 #pragma unroll
-                for (int i = 0; i < FH; ++i) sl[mp.dst[k][i]] = v;
+                for (int i = 0; i < FH; ++i) sl[mp.dst[k][i]] = v[k];
             }
         }
     }
@@ -465,8 +468,12 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, cons
     }
 }
 
-template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, bool FUSED>
+// MODE: 0 unfused; 1 fused (the strips of the chunk are gathered or
+// expanded after the MFMAs); 2 fused fp32 with the expansion map and
+// double-buffered raw rows (filters of up to 3 rows, small tiles).
+template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, int MODE>
 __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
+    constexpr bool FUSED = MODE != 0;
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
@@ -531,10 +538,15 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     RawRows rr{};
     // the map holds FH destinations per element: kept for filters of up to
     // three rows (larger ones expand with the per-element decode)
-    constexpr bool MAP = RAW && FH > 0 && FH <= 3;
-    constexpr int FHM = MAP ? FH : 1;
+    constexpr bool use_map = RAW && MODE == 2;
+    static_assert(!use_map || (FH > 0 && FH <= 3), "expansion map for filters of up to 3 rows");
+    constexpr int FHM = use_map ? FH : 1;
     ExpandMap<FHM> emap;
-    const bool use_map = MAP && a.raw_pitch <= kExpandMaxRaw;
+    // With the map the raw rows are double-buffered (chunk k in
+    // X + (k % 2) * rc * raw_pitch): the copies of chunk c+2 land while chunk
+    // c+1 is expanded, so the expansion needs no wait of its own and runs
+    // ahead of the MFMAs of chunk c, all within one barrier interval.
+    float* const Xb[2] = {X, X + a.rc * a.raw_pitch + kExpandMaxRaw};
     {
         const int rc_act = min(a.rc, a.c);
         const int rc_stage = ROWS ? rc_act : a.rc;
@@ -543,9 +555,10 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             for (int sg = 0; sg < 2; ++sg)
                 for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
             stage_raw(X, a, tr, rr, 0, rc_act);
+            if (use_map && nchunks > 1) stage_raw(Xb[1], a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
             stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
-            __syncthreads();   // zeros written, raw rows of chunk 0 landed
+            __syncthreads();   // zeros written, raw rows of chunk 0 (and 1) landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
             else expand_raw(S, X, a, tr, rr, rc_act, rc_stage);
         } else {
@@ -564,8 +577,14 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         __syncthreads();
         if (ch + 1 < nchunks) {
             if constexpr (RAW) {
-                stage_raw(X, a, tr, rr, r1, rc1);
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
+                if (use_map) {
+                    // a wave copies and expands the same channels (wave, wave + 4, ...)
+                    if (ch + 2 < nchunks) stage_raw(Xb[ch & 1], a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
+                    expand_map_apply<FHM>(S + off, Xb[(ch + 1) & 1], emap, a, tr, rc1, rc_stage1);
+                } else {
+                    stage_raw(X, a, tr, rr, r1, rc1);
+                }
             } else {
                 stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
             }
@@ -574,14 +593,13 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         if (ROWS) compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act);
         else compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full);
         if constexpr (RAW) {
-            // A wave expands the channels whose raw rows it copied itself
-            // (channels wave, wave + 4, ...), so waiting for its own copies
-            // is enough; the next barrier publishes the strips.
-            if (ch + 1 < nchunks) {
+            // Without the map: a wave expands the channels whose raw rows it
+            // copied itself (channels wave, wave + 4, ...), so waiting for its
+            // own copies is enough; the next barrier publishes the strips.
+            if (!use_map && ch + 1 < nchunks) {
                 __builtin_amdgcn_sched_barrier(0);
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-                if (use_map) expand_map_apply<FHM>(S + off, X, emap, a, tr, rc1, rc_stage1);
-                else expand_raw(S + off, X, a, tr, rr, rc1, rc_stage1);
+                expand_raw(S + off, X, a, tr, rr, rc1, rc_stage1);
             }
         }
     }
@@ -600,11 +618,21 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         }
 }
 
+// LDS floats of the raw rows of the fused fp32 kernel: with the expansion
+// map (filters of up to 3 rows, raw rows of up to kExpandMaxRaw floats) two
+// buffers, each with kExpandMaxRaw floats of slack for the map's reads.
+int64_t raw_floats(int fh, int rc, int64_t raw_pitch) {
+    if (fh <= 3 && raw_pitch <= kExpandMaxRaw) return 2 * (rc * raw_pitch + kExpandMaxRaw);
+    return rc * raw_pitch;
+}
+
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP>
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipStream_t stream) {
-    auto kern = fused ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, true>
-                      : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, false>;
-    if (fused && sizeof(TIn) == 4) lds += (int64_t)a.rc * a.raw_pitch * 4;
+    auto kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 0>;
+    if (fused) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 1>;
+    if constexpr (sizeof(TIn) == 4 && FH > 0 && FH <= 3)
+        if (fused && a.raw_pitch <= kExpandMaxRaw) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
+    if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch) * 4;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
@@ -716,7 +744,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
                 const bool fv = filter_vec(g, rc);
                 const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, split, &sc, &fp, &st);
                 const int64_t raw = g.elem == 4 ? raw_pitch_f32(g, t.bn) : 0;
-                if (lds + rc * raw * 4 > budget) continue;
+                if (lds + (raw ? raw_floats((int)g.fh, rc, raw) : 0) * 4 > budget) continue;
                 ConvPlan q;
                 q.kind = ConvPlan::kF32Lds;
                 q.bm = t.bm; q.bn = t.bn; q.rc = rc; q.tc = (int)g.taps; q.split = split;
