@@ -49,7 +49,7 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
         _wait(p, verbose)
     tmp = LIB + ".tmp"
     link = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs + [
-        "-Wl,-rpath,/opt/rocm/lib"]
+        "-Wl,-rpath,/opt/rocm/lib", "-Wl,-z,defs"]
     if verbose:
         print(" ".join(link), flush=True)
     subprocess.run(link, check=True)

@@ -145,6 +145,9 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                     r.fail("%s tile %lld: 16-byte run %d misplaced (shift %d)", what, (long long)t, s, shift);
             }
         }
+        if (a.ilv && (tr.ck_total > 64 * kIlvSlots || 4 * (int64_t)tr.ck_total > p.sc))
+            r.fail("conv tile %lld: %d 16-byte strip copies, in-loop issue covers %d (slot %lld)", (long long)t,
+                   tr.ck_total, 64 * kIlvSlots, (long long)p.sc);
         if (fused && !bf16 && g.elem == 4) {
             // raw input rows: inside x and inside their LDS area; their
             // expansion writes each strip position once if it has a source
@@ -379,6 +382,10 @@ void check_conv(const Geometry& g, Report& r) {
             r.fail("conv: channel split with an odd chunk of %d", p.rc);
         if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
+        if (conv_args_f32(g, p, nullptr, nullptr, nullptr, false).ilv &&
+            (!p.fvec || p.bm * (p.fp / 4) > (int64_t)kConvThreads * kIlvSlots))
+            r.fail("conv: %lld 16-byte filter copies per chunk, in-loop issue covers %d", (long long)(p.bm * (p.fp / 4)),
+                   kConvThreads * kIlvSlots);
         // raw rows: two buffers with 768 floats of slack each when the map is used
         const int64_t mx = 64 * kF32ExpandGroups;
         const int64_t rawf = (g.fh <= 3 && p.raw_pitch <= mx) ? 2 * (p.rc * p.raw_pitch + mx) : p.rc * p.raw_pitch;

@@ -52,6 +52,7 @@ struct ConvArgs {
     int cl_pitch;          // LDS positions per window-tensor row (>= row_len)
     int cl_pb;             // positions per strip plane (one plane per 8-channel half)
     int cl_fpb;            // positions per filter plane
+    int ilv;               // fp32 unfused: copies issued from inside the MFMA loop
 };
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
@@ -276,6 +277,7 @@ constexpr int kBf16FilterScalarItems = 16;
 constexpr int kF32ExpandGroups = 10;  // fused fp32 expansion map: raw floats per channel / 64
 constexpr int kBf16Spare = 64;        // spare positions at the end of every strip plane
 constexpr int kBf16FusedItems = 1;    // fused kernel: raw items per thread (2 elements x 8 channels)
+constexpr int kIlvSlots = 8;          // fp32 copies issued inside the MFMA loop: per lane and channel / chunk
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
 
@@ -369,6 +371,7 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.cl_pitch = a.row_len;
     a.cl_pb = 0;
     a.cl_fpb = 0;
+    a.ilv = 0;
     return a;
 }
 

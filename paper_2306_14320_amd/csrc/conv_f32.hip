@@ -406,10 +406,17 @@ struct RowRegs {
 // matrix-core instructions of the current group are issued, so LDS latency is
 // hidden behind the MFMAs of the same wave.  ROWS: the k-slots are split by
 // filter rows (the second k-slot has no row left when Fh is odd: zeroed).
-template <int FH, int FW, bool ROWS, int NJ, int NP>
+struct NoHook {
+    __device__ void operator()(int) const {}
+};
+
+// `hook(g)` runs after the matrix-core instructions of group g have been
+// issued (the copies of the next chunk are issued there, so they overlap
+// the MFMAs).
+template <int FH, int FW, bool ROWS, int NJ, int NP, typename Hook = NoHook>
 __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, const float* S,
                                      const ConvArgs& a, const int (&fl)[NJ], const int (&sl)[NP],
-                                     int kl, int iters) {
+                                     int kl, int iters, Hook&& hook = Hook()) {
     if constexpr (FH > 0 && FW > 0) {
         constexpr int T = FH * FW, U0 = (FH + 1) / 2;
         constexpr int UEND = ROWS ? U0 : FH;
@@ -450,10 +457,15 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, cons
         for (; g + 2 <= ng; g += 2) {
             load(r1, g + 1);
             mma(r0, g);
+            hook(g);
             if (g + 2 < ng) load(r0, g + 2);
             mma(r1, g + 1);
+            hook(g + 1);
         }
-        if (g < ng) mma(r0, g);
+        if (g < ng) {
+            mma(r0, g);
+            hook(g);
+        }
     } else {
         const int fh = a.fh, fw = a.fw, T = fh * fw, u0 = (fh + 1) >> 1;
         const int uend = ROWS ? u0 : fh;
@@ -463,6 +475,7 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, cons
                 const bool dead = ROWS && kl && (u + u0 >= fh);
                 for (int v = 0; v < fw; ++v)
                     mfma_step<NJ, NP>(acc, F, S, fl, sl, fo + u * fw + v, so + v * fh + u, dead);
+                hook(it * uend + u);
             }
         }
     }
@@ -470,10 +483,86 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, cons
 
 // MODE: 0 unfused; 1 fused (the strips of the chunk are gathered or
 // expanded after the MFMAs); 2 fused fp32 with the expansion map and
-// double-buffered raw rows (filters of up to 3 rows, small tiles).
+// double-buffered raw rows (filters of up to 3 rows, small tiles);
+// 3 unfused with 16-byte strips and filter rows whose copies are issued from
+// inside the MFMA loop, from per-lane offsets computed once.
+
+// MODE 3 copies of one tile: the 16-byte strip copies of one channel and the
+// filter-row copies of one whole chunk, as in stage(), from per-lane byte
+// offsets that hold for every chunk and channel but for the channel offset
+// (kIlvNone: the lane has no copy in that slot).  Bases are wave-uniform and
+// offsets 32-bit, so each copy is one scalar-base load with a vector offset.
+constexpr uint32_t kIlvNone = 0xffffffffu;
+
+struct IlvCopies {
+    const char* s_base = nullptr;  // channel 0 of the tile's first image
+    const char* f_base = nullptr;  // channel 0 of the tile's first filter
+    uint32_t s_off[kIlvSlots];
+    uint32_t f_off[kIlvSlots];
+    int ck_total = 0, f_total = 0;
+
+    __device__ void init(const ConvArgs& a, const TileRuns& tr, int j0) {
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int64_t plane = (int64_t)a.ho * a.row_len;
+        ck_total = tr.ck_total;
+        s_base = static_cast<const char*>(a.src) + 4 * (int64_t)tr.i0 * a.c * plane;
+        const int start0 = tr.m0 * a.row_len + tr.qa0 - tr.shift0;
+#pragma unroll
+        for (int i = 0; i < kIlvSlots; ++i) {
+            const int c = 64 * i + lane;
+            int sgi = 0, cs = c;
+            if (c >= tr.ck0) {
+                sgi = 1 + (int)fast_div((uint32_t)(c - tr.ck0), a.div_ckmid);
+                if (sgi > tr.nseg - 1) sgi = tr.nseg - 1;
+                cs = c - tr.ck0 - (sgi - 1) * tr.ck_mid;
+            }
+            const uint32_t e = (uint32_t)(sgi * a.c * (int)plane + (sgi == 0 ? start0 : 0) + 4 * cs);
+            s_off[i] = c < ck_total ? 4 * e : kIlvNone;
+        }
+        f_base = static_cast<const char*>(a.w) + 4 * (int64_t)j0 * a.c * a.taps;
+        const int cpr = a.fp >> 2, creal = (a.rc * a.taps) >> 2;
+        f_total = min(a.k - j0, a.bm) * cpr;
+#pragma unroll
+        for (int i = 0; i < kIlvSlots; ++i) {
+            const int c = wave * 64 + kConvThreads * i + lane;
+            const int jj = (int)fast_div((uint32_t)c, a.div_fp);
+            const int col = c - jj * cpr;
+            f_off[i] = c < f_total && col < creal ? (uint32_t)(4 * (jj * a.c * a.taps + 4 * col)) : kIlvNone;
+        }
+    }
+    // filter rows of the whole chunk starting at channel r0 into F
+    __device__ void filter(float* F, const ConvArgs& a, int r0) const {
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const char* b = f_base + 4 * (int64_t)r0 * a.taps;
+#pragma unroll
+        for (int i = 0; i < kIlvSlots; ++i) {
+            uint32_t o = f_off[i];
+            asm volatile("" : "+v"(o));  // widened here, not held widened across the loop
+            if (kConvThreads * i < f_total && o != kIlvNone)
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const float*>(b + o),
+                                                 (lds_void*)(F + 4 * (wave * 64 + kConvThreads * i)), 16, 0, 0);
+        }
+    }
+    // strip of channel r0 + rc into its LDS slot in S
+    __device__ void strips(float* S, const ConvArgs& a, int rc, int r0) const {
+        const char* b = s_base + 4 * (int64_t)(r0 + rc) * a.ho * a.row_len;
+        float* l = S + rc * a.sc;
+#pragma unroll
+        for (int i = 0; i < kIlvSlots; ++i) {
+            uint32_t o = s_off[i];
+            asm volatile("" : "+v"(o));
+            if (64 * i < ck_total && o != kIlvNone)
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const float*>(b + o),
+                                                 (lds_void*)(l + 4 * 64 * i), 16, 0, 0);
+        }
+    }
+};
+
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, int MODE>
 __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
-    constexpr bool FUSED = MODE != 0;
+    constexpr bool FUSED = MODE == 1 || MODE == 2;
+    constexpr bool ILV = MODE == 3;
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
@@ -565,6 +654,9 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, rc_stage);
         }
     }
+    IlvCopies ilv;
+    if constexpr (ILV) ilv.init(a, tr, j0);
+
     for (int ch = 0; ch < nchunks; ++ch) {
         const int r0 = ch * a.rc;
         const int rc_act = min(a.rc, a.c - r0);
@@ -575,7 +667,9 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         const int rc_stage1 = ROWS ? rc1 : a.rc;
         const int off = ((ch + 1) & 1) * a.stage;
         __syncthreads();
-        if (ch + 1 < nchunks) {
+        // MODE 3: a whole next chunk is copied from inside the MFMA loop
+        const bool ilv_next = ILV && ch + 1 < nchunks && rc1 == a.rc;
+        if (ch + 1 < nchunks && !ilv_next) {
             if constexpr (RAW) {
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
                 if (use_map) {
@@ -590,8 +684,24 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             }
         }
         __builtin_amdgcn_sched_barrier(0);
-        if (ROWS) compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act);
-        else compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full);
+        // wave w copies channels w, w + 4, ...: one channel per row group
+        auto hook = [&](int g) {
+            if constexpr (ILV) {
+                if (ilv_next) {
+                    const int rc = 4 * g + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+                    if (g == 0) ilv.filter(F + off, a, r1);
+                    if (rc < rc1) ilv.strips(S + off, a, rc, r1);
+                }
+            }
+        };
+        if (ROWS) compute_chunk<FH, FW, true, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, rc_act, hook);
+        else compute_chunk<FH, FW, false, NJ, NP>(acc, Fc, Sc, a, fl, sl, kl, half_full, hook);
+        if constexpr (ILV) {
+            if (ilv_next) {
+                const int ng = ROWS ? rc_act * ((FH + 1) / 2) : half_full * FH;
+                for (int rc = 4 * ng + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); rc < rc1; rc += 4) ilv.strips(S + off, a, rc, r1);
+            }
+        }
         if constexpr (RAW) {
             // Without the map: a wave expands the channels whose raw rows it
             // copied itself (channels wave, wave + 4, ...), so waiting for its
@@ -629,6 +739,8 @@ int64_t raw_floats(int fh, int rc, int64_t raw_pitch) {
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP>
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipStream_t stream) {
     auto kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 0>;
+    constexpr int kIlvMode = sizeof(TIn) == 4 && FH > 0 ? 3 : 0;
+    if (!fused && a.svec && a.fvec && a.ilv) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, kIlvMode>;
     if (fused) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 1>;
     if constexpr (sizeof(TIn) == 4 && FH > 0 && FH <= 3)
         if (fused && a.raw_pitch <= kExpandMaxRaw) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
@@ -781,6 +893,16 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     a.div_ckmid = make_fastdiv((uint32_t)((((g.ho - 1) * g.row_len + g.used_len) + 3) >> 2));
     a.raw_pitch = (int)p.raw_pitch;
     a.raw_off = 2 * (int)p.stage;
+    // MODE 3 copies a channel's strip (at most sc / 4 chunks of 16 bytes,
+    // since it fits its LDS slot) and a chunk's filter rows with kIlvSlots
+    // copies per lane, at 32-bit offsets from the tile's first image
+    const int64_t plane = (int64_t)g.ho * g.row_len;
+    const int64_t segs = p.bn / ((int64_t)g.ho * g.wo) + 2;
+    // (byte offsets below 2^32); the filter-row split keeps the copies
+    // before the MFMAs (its MODE 3 build holds too many registers)
+    a.ilv = (!fused && p.svec && p.fvec && p.split == 0 && p.sc / 4 <= 64 * kIlvSlots &&
+             (int64_t)p.bm * (p.fp / 4) <= (int64_t)kConvThreads * kIlvSlots &&
+             segs * g.c * plane < (1ll << 30) && (int64_t)p.bm * g.c * g.fh * g.fw < (1ll << 30)) ? 1 : 0;
     return a;
 }
 
