@@ -21,9 +21,15 @@
  *  - Padding is symmetric zero padding (not in the paper; the convolution is
  *    the one of PyTorch's conv2d with these strides and paddings, no bias, no
  *    dilation, no groups).
- *  - Device pointers (x, w, ws, y) are owned by the caller; the library never
- *    allocates, frees or keeps device memory.  Each must be 16-byte aligned
- *    and the buffers must not overlap.
+ *  - Device pointers (x, w, ws, y) are owned by the caller.  Each must be
+ *    16-byte aligned and the buffers must not overlap.  The library keeps no
+ *    device memory between calls.  The one temporary it uses: bf16
+ *    convolutions that run on its fast kernels (C a multiple of 16, K a
+ *    multiple of 64, filter 3x3, 3x5 or 1x1, among other shape conditions)
+ *    first rewrite w into the order those kernels copy to on-chip memory,
+ *    in a buffer of K*C*Fh*Fw*2 bytes taken from the device's stream-ordered
+ *    memory pool (hipMallocAsync on `stream`) and released on `stream`
+ *    (hipFreeAsync) after the convolution; a failed allocation is EHIP.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Calls only
  *    enqueue work: they never synchronise, hold no state between calls and may
  *    be made from several host threads at once.

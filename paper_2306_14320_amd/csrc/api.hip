@@ -102,8 +102,9 @@ int check_ptr(const void* p, const char* name) {
     return IM2WIN_OK;
 }
 
+// rc: 0, or the IM2WIN_E* code of a failure the launcher detected (msg says which)
 int after_launch(int rc, const char* what, const char* msg) {
-    if (rc != 0) return fail(IM2WIN_EOVERFLOW, "%s", msg);
+    if (rc != 0) return fail(rc == IM2WIN_EHIP ? IM2WIN_EHIP : IM2WIN_EOVERFLOW, "%s", msg);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(IM2WIN_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
     return ok();

@@ -360,8 +360,55 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
         r.fail("%s: tiles cover %lld of %lld pixels", what, (long long)covered, (long long)g.npix);
 }
 
-void check_conv(const Geometry& g, Report& r) {
-    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g) : plan_conv_f32(g);
+// Packed bf16 filter: every piece reads 8 channels inside w, the blocks tile
+// the packed buffer, and within a block the DMA destination of piece P (the
+// kernels' dma_filter: plane P / (T*BM), position P mod T*BM) is the LDS
+// position packed_piece() assigns, where the matrix-core reads expect
+// channels c0 .. c0+7 of tap t of output channel j: each filter position of
+// both planes filled exactly once.
+void check_packed_filter(const Geometry& g, const ConvPlan& p, Report& r) {
+    const int T = (int)g.taps, bm = p.bm, plane = T * bm, pieces = 2 * plane;
+    const int nchunks = (int)(g.c / kBf16Chunk);
+    if (g.c % kBf16Chunk || g.k % bm || plane % 64) {
+        r.fail("conv: packed bf16 filter with C %% 16 = %lld, K %% BM = %lld, T*BM = %d", (long long)(g.c % 16),
+               (long long)(g.k % bm), plane);
+        return;
+    }
+    const int64_t npieces = g.k * g.c * T / 8;
+    if (npieces != (g.k / bm) * (int64_t)nchunks * pieces) {
+        r.fail("conv: %lld packed pieces, blocks hold %lld", (long long)npieces,
+               (long long)((g.k / bm) * nchunks * pieces));
+        return;
+    }
+    std::vector<int> seen(2 * (size_t)p.cl_fpb, 0);
+    for (int64_t gid = 0; gid < npieces && r.violations < 16; ++gid) {
+        const PackedPiece pc = packed_piece(gid, T, (int)g.fh, (int)g.fw, bm, nchunks, (int)p.cl_fpb);
+        const int64_t blk = gid / pieces;
+        const int P = (int)(gid - blk * pieces);
+        const int jt = (int)(blk / nchunks), ch = (int)(blk % nchunks);
+        const int gg = P / plane, q = P % plane, t = q / bm, jj = q % bm;
+        const int v = t / (int)g.fh, u = t % (int)g.fh;
+        const int dma_pos = gg * (int)p.cl_fpb + P - gg * plane;
+        if (pc.j != jt * bm + jj || pc.j >= g.k || pc.c0 != 16 * ch + 8 * gg || pc.c0 + 8 > g.c ||
+            packed_index(pc.j, ch, gg, t, T, bm, nchunks) != gid || g.k % kPackRows ||
+            pc.nat != u * g.fw + v || pc.nat >= T || pc.lds_pos != dma_pos || dma_pos < 0 ||
+            dma_pos >= 2 * p.cl_fpb || (gg == 0 && dma_pos >= p.cl_fpb))
+            r.fail("conv: packed filter piece %lld -> j %d c0 %d tap %d LDS %d (DMA %d)", (long long)gid, pc.j,
+                   pc.c0, pc.nat, pc.lds_pos, dma_pos);
+        else if (blk == 0)
+            ++seen[dma_pos];
+    }
+    for (int gg = 0; gg < 2 && r.violations < 16; ++gg)
+        for (int q = 0; q < plane; ++q)
+            if (seen[gg * p.cl_fpb + q] != 1) {
+                r.fail("conv: packed filter LDS position %d of plane %d written %d times", q, gg,
+                       seen[gg * p.cl_fpb + q]);
+                break;
+            }
+}
+
+void check_conv(const Geometry& g, bool fused_plan, Report& r) {
+    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused_plan) : plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) {
         r.fail("conv: no tile configuration fits in LDS (the launch would be refused)");
         return;
@@ -409,12 +456,15 @@ void check_conv(const Geometry& g, Report& r) {
         if (!p.fvec && 2 * g.taps * p.bm > (int64_t)kConvThreads * kBf16FilterScalarItems)
             r.fail("conv: %lld bf16 filter items exceed the staging registers",
                    (long long)(2 * g.taps * p.bm));
+        if (p.fast || p.fused_fast) check_packed_filter(g, p, r);
     }
     if (bf16) {
-        check_conv_bf16_variant(g, p, false, r);
-        check_conv_bf16_variant(g, p, true, r);
+        // unfused and fused plans may differ (the unfused fast kernel has a
+        // larger tile); each is checked for the variant that uses it
+        check_conv_bf16_variant(g, p, fused_plan, r);
         return;
     }
+    if (fused_plan) return;   // fp32: one plan for both variants
     check_conv_variant(g, p, false, r);
     if (p.svec) check_conv_variant(g, p, true, r);
 }
@@ -427,7 +477,8 @@ int64_t check_plans(const Geometry& g, char* msg, size_t msglen) {
     r.msglen = msglen;
     if (msglen) msg[0] = '\0';
     check_transform(g, r);
-    check_conv(g, r);
+    check_conv(g, false, r);
+    check_conv(g, true, r);
     return r.violations;
 }
 

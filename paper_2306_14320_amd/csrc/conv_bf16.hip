@@ -354,6 +354,58 @@ __device__ inline void store_filter(const FilterRegs<FVEC, FH * FW, BM>& R, uint
 
 __device__ inline bf16x8 frag(const uint16_t* p) { return __builtin_bit_cast(bf16x8, load16(p)); }
 
+// Repack K x C x Fh x Fw into the blocks of packed_piece().  Workgroup
+// (row group jg, chunk ch) copies the 16*T filter elements of chunk ch of
+// output channels kPackRows*jg .. +kPackRows-1 (one contiguous run per output
+// channel) to LDS, then writes its 2*T*kPackRows pieces: for each (half g,
+// tap t) the kPackRows pieces of consecutive output channels are
+// consecutive in the packed tensor.
+__global__ __launch_bounds__(256) void pack_filter_bf16_kernel(const uint16_t* __restrict__ w,
+                                                               uint16_t* __restrict__ wp, int c, int fh,
+                                                               int fw, int bm, int nchunks) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* L = reinterpret_cast<uint16_t*>(smem);   // [kPackRows][16*T]
+    const int T = fh * fw, run = kBf16ChunkChannels * T;
+    const int ch = blockIdx.x % nchunks, jg = blockIdx.x / nchunks;
+    const int j0 = jg * kPackRows;
+    // 2-byte elements: runs start at even element offsets only when T is even
+    for (int e = threadIdx.x; e < kPackRows * run; e += 256) {
+        const int r = e / run, q = e - r * run;
+        L[e] = w[((int64_t)(j0 + r) * c + kBf16ChunkChannels * ch) * T + q];
+    }
+    __syncthreads();
+    for (int pc = threadIdx.x; pc < 2 * T * kPackRows; pc += 256) {
+        const int jj = pc % kPackRows, gt = pc / kPackRows;   // gt = g*T + t
+        const int g = gt / T, t = gt - g * T;
+        const int v = t / fh, u = t - v * fh, nat = u * fw + v;
+        const uint16_t* s = L + jj * run + 8 * g * T + nat;
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = uint32_t(s[(2 * e) * T]) | (uint32_t(s[(2 * e + 1) * T]) << 16);
+        store16(wp + packed_index(j0 + jj, ch, g, t, T, bm, nchunks) * 8, o);
+    }
+}
+
+// Copy one chunk's packed filter block (2*T*BM pieces) into the filter planes
+// of an LDS stage by 16-byte DMA: one instruction moves 64 consecutive pieces,
+// which land in 64 consecutive positions of one plane (T*BM is a multiple of
+// 64).  The caller's next vmcnt(0) wait and barrier publish them.
+template <int T, int BM>
+__device__ inline void dma_filter(const uint16_t* blk, uint16_t* planes, int cl_fpb) {
+    constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
+    static_assert(kPlane % 64 == 0, "a DMA instruction stays inside one plane");
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int p0 = 0; p0 < kPieces; p0 += kConvThreads) {
+        const int P0 = p0 + 64 * wave;
+        if (P0 < kPieces) {
+            const int g = P0 >= kPlane ? 1 : 0;
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint32_t*>(blk + (int64_t)(P0 + lane) * 8),
+                                             (lds_u32*)(planes + (g * cl_fpb + P0 - g * kPlane) * 8), 16, 0, 0);
+        }
+    }
+}
+
 // MFMA over one staged chunk: for each tap, NJ filter fragments and NP window
 // fragments, read from LDS one tap ahead of the matrix-core instructions that
 // use them.  FT > 0 fixes the number of taps at compile time.
@@ -502,22 +554,23 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
 // MFMAs of chunk c, which a single wave per SIMD cannot otherwise overlap.
 // Chunks past the last are loaded again from the last one and written to the
 // stage no MFMA reads any more, so no step needs a branch.
-template <int FH, int FW, int BM, int NJ, int NP, int SVI>
+// Per-thread staging registers of one chunk's strips (fast kernels).
+template <int SVI>
 struct FastStage {
-    static constexpr int T = FH * FW;
-    static constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
-    uint32_t sd[SVI][16];          // strips: 8 channels x 4 positions per item
-    uint32_t fd[FI][4 * T];        // filter: 8 channels x T taps per item
+    uint32_t sd[SVI][16];          // 8 channels x 4 positions per item
 };
 
+// Unfused kernel for the common case: whole 16-channel chunks, whole tiles of
+// output channels, window-tensor planes and rows of whole 4-element groups.
+// The filter comes packed (packed_piece) and is copied by 16-byte DMA, one
+// chunk ahead; the strips pass through registers two chunks ahead.
 template <int FH, int FW, int BM, int BN, int TJ, int TP, int SVI>
 __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a) {
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
     constexpr int T = FH * FW;
-    constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
-    using St = FastStage<FH, FW, BM, NJ, NP, SVI>;
+    using St = FastStage<SVI>;
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -553,7 +606,6 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
 
     // per-item sources (channel 0 of the chunk) and LDS destinations
     const uint16_t* src = static_cast<const uint16_t*>(a.src);
-    const uint16_t* wsrc = static_cast<const uint16_t*>(a.w);
     const int plane = a.ho * a.row_len;
     const uint16_t* sp[SVI];
     int sdst[SVI];
@@ -566,17 +618,11 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
         sp[k] = src + ((int64_t)(rn.i0 + it.s) * a.c + 8 * (q & 1)) * plane + it.e;
         sdst[k] = ((q & 1) * a.cl_pb + lds_pos(cl, rn, a, it.s, it.e)) * 8;
     }
-    const uint16_t* fp[FI];
-    int fdst[FI];
-#pragma unroll
-    for (int k = 0; k < FI; ++k) {
-        const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
-        fp[k] = wsrc + ((int64_t)(j0 + (q >> 1)) * a.c + 8 * (q & 1)) * T;
-        fdst[k] = ((q & 1) * a.cl_fpb + (q >> 1)) * 8;
-    }
+    const int nchunks = a.c / kRC;
+    // packed filter blocks of this tile of output channels
+    const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
 
     St st0, st1;
-    const int nchunks = a.c / kRC;
     auto load = [&](St& r, int ch) {
         const int r0 = (ch < nchunks ? ch : nchunks - 1) * kRC;
 #pragma unroll
@@ -589,42 +635,19 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
                 r.sd[k][2 * c8 + 1] = v[1];
             }
         }
-#pragma unroll
-        for (int k = 0; k < FI; ++k) {
-            const uint16_t* p = fp[k] + r0 * T;
-#pragma unroll
-            for (int v4 = 0; v4 < T; ++v4) {
-                const u32x4 v = load16(p + 8 * v4);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) r.fd[k][4 * v4 + e] = v[e];
-            }
-        }
     };
-    // part t of the stores of one stage: filter tap t, and strip position t (< 4)
+    // strip position t (< 4) of every item: 16-bit transpose, one 16-byte store
     auto part = [&](const St& r, uint16_t* stg, int t) {
-        if (t < T) {
-            const int u = t % FH, v = t / FH, nat = u * FW + v;
 #pragma unroll
-            for (int k = 0; k < FI; ++k) {
-                u32x4 o;
+        for (int k = 0; k < SVI; ++k) {
+            u32x4 o;
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    o[e] = elem16(r.fd[k], (2 * e) * T + nat) | (elem16(r.fd[k], (2 * e + 1) * T + nat) << 16);
-                store16(stg + f_off + fdst[k] + t * BM * 8, o);
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t w0 = r.sd[k][(2 * e) * 2 + t / 2];
+                const uint32_t w1 = r.sd[k][(2 * e + 1) * 2 + t / 2];
+                o[e] = (t & 1) ? hi_pair(w0, w1) : lo_pair(w0, w1);
             }
-        }
-        if (t < 4) {
-#pragma unroll
-            for (int k = 0; k < SVI; ++k) {
-                u32x4 o;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t w0 = r.sd[k][(2 * e) * 2 + t / 2];
-                    const uint32_t w1 = r.sd[k][(2 * e + 1) * 2 + t / 2];
-                    o[e] = (t & 1) ? hi_pair(w0, w1) : lo_pair(w0, w1);
-                }
-                store16(stg + sdst[k] + t * 8, o);
-            }
+            store16(stg + sdst[k] + t * 8, o);
         }
     };
 
@@ -636,20 +659,23 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
 
-    // chunk 0 into stage 0; chunk 1 in flight
+    // chunk 0 into stage 0 (filter by DMA); chunk 1's strips in flight
+    dma_filter<T, BM>(fblk, lds + f_off, a.cl_fpb);
     load(st0, 0);
 #pragma unroll
-    for (int t = 0; t < (T > 4 ? T : 4); ++t) part(st0, lds, t);
+    for (int t = 0; t < 4; ++t) part(st0, lds, t);
     load(st1, 1);
 
     auto step = [&](int ch, St& r_ld, St& r_st) {
         const uint16_t* cur = lds + (ch & 1) * a.stage;
         uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        // chunk ch complete in LDS (this wave's DMA and stores, then everyone's),
+        // and every wave done with chunk ch-1, whose stage is refilled below
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (ch + 1 < nchunks) dma_filter<T, BM>(fblk + (int64_t)(ch + 1) * (16 * T * BM), nxt + f_off, a.cl_fpb);
         load(r_ld, ch + 2);
-        __builtin_amdgcn_sched_barrier(0);   // keep the loads at the head of the step
+        __builtin_amdgcn_sched_barrier(0);   // keep the copies at the head of the step
         const uint16_t* F = cur + f_off;
-        bf16x8 a0[NJ], b0[NP], a1[NJ], b1[NP];
         auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
 #pragma unroll
             for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * 8 + fo[jb]);
@@ -663,20 +689,15 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
                 for (int pb = 0; pb < NP; ++pb)
                     acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
         };
-        ld(a0, b0, 0);
-        int t = 0;
+        // operands read two taps ahead of the matrix-core instructions
+        bf16x8 av[3][NJ], bv[3][NP];
+        ld(av[0], bv[0], 0);
+        if (1 < T) ld(av[1], bv[1], 1);
 #pragma unroll
-        for (; t + 2 <= T; t += 2) {
-            ld(a1, b1, t + 1);
-            mm(a0, b0);
-            part(r_st, nxt, t);
-            if (t + 2 < T) ld(a0, b0, t + 2);
-            mm(a1, b1);
-            part(r_st, nxt, t + 1);
-        }
-        if (t < T) {
-            mm(a0, b0);
-            part(r_st, nxt, t);
+        for (int t = 0; t < T; ++t) {
+            if (t + 2 < T) ld(av[(t + 2) % 3], bv[(t + 2) % 3], t + 2);
+            mm(av[t % 3], bv[t % 3]);
+            if (t < 4) part(r_st, nxt, t);
         }
 #pragma unroll
         for (int t2 = T; t2 < 4; ++t2) part(r_st, nxt, t2);   // strip positions when T < 4
@@ -726,9 +747,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
     constexpr int T = FH * FW;
-    constexpr int FI = (2 * BM + kConvThreads - 1) / kConvThreads;
     constexpr int IPT = kBf16FusedItems;   // items per thread
-    using St = FastStage<FH, FW, BM, NJ, NP, 1>;
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -764,7 +783,6 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     for (int jb = 0; jb < NJ; ++jb) fo[jb] = (kl * a.cl_fpb + wj * TJ + jb * 32 + l32) * 8;
 
     const uint16_t* xsrc = static_cast<const uint16_t*>(a.src);
-    const uint16_t* wsrc = static_cast<const uint16_t*>(a.w);
     const int64_t xplane = (int64_t)a.h * a.w_in;
     const int nitems = rr.rtot * a.w_in;   // (rtot*W/2 pairs) x 2 halves
 
@@ -827,41 +845,9 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
             }
         }
     }
-    const uint16_t* fp[FI];
-    int fdst[FI];
-#pragma unroll
-    for (int k = 0; k < FI; ++k) {
-        const int q = (threadIdx.x + k * kConvThreads) & (2 * BM - 1);
-        fp[k] = wsrc + ((int64_t)(j0 + (q >> 1)) * a.c + 8 * (q & 1)) * T;
-        fdst[k] = ((q & 1) * a.cl_fpb + (q >> 1)) * 8;
-    }
-
-    St st0, st1;
     const int nchunks = a.c / kRC;
-    auto load_f = [&](St& r, int ch) {
-        const int r0 = (ch < nchunks ? ch : nchunks - 1) * kRC;
-#pragma unroll
-        for (int k = 0; k < FI; ++k) {
-            const uint16_t* p = fp[k] + r0 * T;
-#pragma unroll
-            for (int v4 = 0; v4 < T; ++v4) {
-                const u32x4 v = load16(p + 8 * v4);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) r.fd[k][4 * v4 + e] = v[e];
-            }
-        }
-    };
-    auto part_f = [&](const St& r, uint16_t* stg, int t) {
-        const int u = t % FH, v = t / FH, nat = u * FW + v;
-#pragma unroll
-        for (int k = 0; k < FI; ++k) {
-            u32x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                o[e] = elem16(r.fd[k], (2 * e) * T + nat) | (elem16(r.fd[k], (2 * e + 1) * T + nat) << 16);
-            store16(stg + f_off + fdst[k] + t * BM * 8, o);
-        }
-    };
+    // packed filter blocks of this tile of output channels
+    const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
     auto dma = [&](int ch) {
         const int64_t off = (int64_t)(ch < nchunks ? ch : nchunks - 1) * kRC * xplane;
 #pragma unroll
@@ -912,23 +898,21 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
         for (int st = 0; st < 2; ++st)
             for (int e = threadIdx.x; e < 2 * a.cl_pb; e += kConvThreads) store16(lds + st * a.stage + e * 8, z);
     }
-    load_f(st0, 0);
+    dma_filter<T, BM>(fblk, lds + f_off, a.cl_fpb);
     dma(0);
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");   // zeros before strips
-#pragma unroll
-    for (int t = 0; t < T; ++t) part_f(st0, lds, t);
     expand(lds);
-    load_f(st1, 1);
 
-    auto step = [&](int ch, St& r_ld, St& r_st) {
+    auto step = [&](int ch) {
         const uint16_t* cur = lds + (ch & 1) * a.stage;
         uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
+        // the wave's own copies of chunk ch landed before its expansion (end
+        // of the previous step); the barrier publishes everyone's
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
         dma(ch + 1);
-        load_f(r_ld, ch + 2);
+        if (ch + 1 < nchunks) dma_filter<T, BM>(fblk + (int64_t)(ch + 1) * (16 * T * BM), nxt + f_off, a.cl_fpb);
         __builtin_amdgcn_sched_barrier(0);
         const uint16_t* F = cur + f_off;
-        bf16x8 a0[NJ], b0[NP], a1[NJ], b1[NP];
         auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
 #pragma unroll
             for (int jb = 0; jb < NJ; ++jb) av[jb] = frag(F + t * BM * 8 + fo[jb]);
@@ -942,31 +926,19 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
                 for (int pb = 0; pb < NP; ++pb)
                     acc[jb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[jb], bv[pb], acc[jb][pb], 0, 0, 0);
         };
-        ld(a0, b0, 0);
-        int t = 0;
+        bf16x8 av[3][NJ], bv[3][NP];
+        ld(av[0], bv[0], 0);
+        if (1 < T) ld(av[1], bv[1], 1);
 #pragma unroll
-        for (; t + 2 <= T; t += 2) {
-            ld(a1, b1, t + 1);
-            mm(a0, b0);
-            part_f(r_st, nxt, t);
-            if (t + 2 < T) ld(a0, b0, t + 2);
-            mm(a1, b1);
-            part_f(r_st, nxt, t + 1);
-        }
-        if (t < T) {
-            mm(a0, b0);
-            part_f(r_st, nxt, t);
+        for (int t = 0; t < T; ++t) {
+            if (t + 2 < T) ld(av[(t + 2) % 3], bv[(t + 2) % 3], t + 2);
+            mm(av[t % 3], bv[t % 3]);
         }
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of chunk ch+1
         expand(nxt);
     };
-    int ch = 0;
-    for (; ch + 2 <= nchunks; ch += 2) {
-        step(ch, st0, st1);
-        step(ch + 1, st1, st0);
-    }
-    if (ch < nchunks) step(ch, st0, st1);
+    for (int ch = 0; ch < nchunks; ++ch) step(ch);
 
 #pragma unroll
     for (int jb = 0; jb < NJ; ++jb)
@@ -1022,8 +994,9 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode
         }
     }
     if constexpr (FVEC) {
-        if (smode == kStripVec && a.c % kRC == 0 && a.k % p.bm == 0) {
-            if (p.bm == 128) launch_fast_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, svi, stream);
+        if (smode == kStripVec && p.fast) {
+            if (p.bn == 256) launch_fast_cfg<FH, FW, 128, 256, 64, 128>(a, blocks, p.lds_bytes, svi, stream);
+            else if (p.bm == 128) launch_fast_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, svi, stream);
             else if (p.bn == 128) launch_fast_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, svi, stream);
             else launch_fast_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, svi, stream);
             return;
@@ -1054,7 +1027,7 @@ int64_t bf16_cl_pitch(const Geometry& g) {
 // per-thread staging registers of every strip and filter item) and gives
 // every CU a workgroup is taken, else the one with the most workgroups.  When
 // none fits, the bf16 problem runs on the fp32-strip kernel (inputs widened).
-ConvPlan plan_conv_bf16(const Geometry& g) {
+ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
     const TileCfg large_k[] = {{128, 128}, {64, 128}, {64, 64}};
     const TileCfg small_k[] = {{64, 128}, {64, 64}};
     const TileCfg* cfgs = g.k > 64 ? large_k : small_k;
@@ -1093,12 +1066,40 @@ ConvPlan plan_conv_bf16(const Geometry& g) {
         p.fvec = fvec ? 1 : 0;
         p.strip_items = svec ? vec_items : 0;
         p.fused_fast = fused_fast ? 1 : 0;
+        p.fast = fvec && svec && g.c % kRC == 0 && g.k % t.bm == 0 ? 1 : 0;
         const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
-        if (blocks >= 256) return p;
+        if (blocks >= 256) {
+            best = p;
+            best_blocks = blocks;
+            break;
+        }
         if (blocks > best_blocks) { best = p; best_blocks = blocks; }
     }
-    if (best.kind != ConvPlan::kNone) return best;
-    return plan_conv_f32(g);
+    if (best.kind == ConvPlan::kNone) return plan_conv_f32(g);
+    // The unfused fast kernel also has a 128 x 256 tile (4 waves of 64 x 128:
+    // fewer LDS reads per matrix-core instruction and half the filter copies
+    // per pixel).  It only fits one workgroup per CU, as 128 x 128 does, so it
+    // is taken when it needs no more rounds of workgroups over the CUs.
+    if (!fused && best.fast && best.bm == 128 && best.bn == 128) {
+        ConvPlan q = best;
+        q.bn = 256;
+        const int64_t run_vec = strip_capacity(g, 256, 4);
+        const int64_t vec_items = 2 * ((run_vec + 3) / 4);
+        const int64_t ext = cl_extent_bound(g, 256, pitch) + kBf16Spare;
+        const int64_t pb = ext + mod16((int)((2 - ext) % 16));
+        const int64_t stage = 16 * (pb + q.cl_fpb);
+        const int64_t blocks = ((g.npix + 255) / 256) * (g.k / 128);
+        if (vec_items <= (int64_t)kConvThreads * kStripVecItems && 2 * stage * 2 <= kConvLdsMaxBytes &&
+            (blocks + 255) / 256 <= (best_blocks + 255) / 256) {
+            q.strip_cap = pb;
+            q.stage = stage;
+            q.lds_bytes = 2 * stage * 2;
+            q.strip_items = vec_items;
+            q.fused_fast = 0;
+            return q;
+        }
+    }
+    return best;
 }
 
 ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
@@ -1122,9 +1123,12 @@ int bf16_strip_mode(const ConvPlan& p, bool fused) {
     return fused ? kStripFused : (p.svec ? kStripVec : kStripScalar);
 }
 
+// The fast kernels read the filter packed (packed_piece).
+bool bf16_packed(const ConvPlan& p, bool fused) { return fused ? p.fused_fast != 0 : p.fast != 0; }
+
 int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, float* y,
                      hipStream_t stream, char* err, size_t errlen) {
-    const ConvPlan p = plan_conv_bf16(g);
+    const ConvPlan p = plan_conv_bf16(g, fused);
     if (p.kind == ConvPlan::kNone) {
         snprintf(err, errlen,
                  "conv: the window strips of one tile (row length %lld) do not fit in LDS; "
@@ -1133,17 +1137,41 @@ int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void*
     }
     if (p.kind == ConvPlan::kF32Lds)
         return launch_conv_f32_plan(g, p, fused, src, w, y, stream, err, errlen);
-    const ConvArgs a = conv_args_bf16(g, p, src, w, y, fused);
+    ConvArgs a = conv_args_bf16(g, p, src, w, y, fused);
     const int64_t blocks = ((g.npix + p.bn - 1) / p.bn) * a.num_jtiles;
     if (blocks > 0x7fffffff) {
         snprintf(err, errlen, "conv: grid of %lld workgroups is too large", (long long)blocks);
         return -5;
     }
     const int smode = bf16_strip_mode(p, fused);
+    void* wpack = nullptr;
+    if (bf16_packed(p, fused)) {
+        // the filter, repacked for 16-byte DMA, in a buffer of the stream's
+        // memory pool that lives until this call's kernels are done
+        const int64_t npieces = g.k * g.c * g.taps / 8;
+        const hipError_t e = hipMallocAsync(&wpack, (size_t)npieces * 16, stream);
+        if (e != hipSuccess) {
+            snprintf(err, errlen, "conv: packed-filter buffer of %lld bytes: %s", (long long)npieces * 16,
+                     hipGetErrorString(e));
+            return -4;
+        }
+        const int64_t nchunks = g.c / kRC;
+        hipLaunchKernelGGL(pack_filter_bf16_kernel, dim3((unsigned)(g.k / kPackRows * nchunks)), dim3(256),
+                           (size_t)kPackRows * kRC * g.taps * 2, stream, static_cast<const uint16_t*>(w),
+                           static_cast<uint16_t*>(wpack), (int)g.c, (int)g.fh, (int)g.fw, p.bm, (int)nchunks);
+        a.w = wpack;
+    }
     if (p.fvec && g.fh == 3 && g.fw == 3) launch_tile<3, 3, true>(p, a, blocks, smode, stream);
     else if (p.fvec && g.fh == 3 && g.fw == 5) launch_tile<3, 5, true>(p, a, blocks, smode, stream);
     else if (p.fvec && g.fh == 1 && g.fw == 1) launch_tile<1, 1, true>(p, a, blocks, smode, stream);
     else launch_tile<0, 0, false>(p, a, blocks, smode, stream);
+    if (wpack) {
+        const hipError_t e = hipFreeAsync(wpack, stream);
+        if (e != hipSuccess) {
+            snprintf(err, errlen, "conv: releasing the packed-filter buffer: %s", hipGetErrorString(e));
+            return -4;
+        }
+    }
     return 0;
 }
 

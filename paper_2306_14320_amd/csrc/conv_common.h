@@ -10,6 +10,8 @@ namespace im2win {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+constexpr int kBf16ChunkChannels = 16;   // bf16: input channels per chunk (MFMA reduction width)
+
 constexpr int kConvThreads = 256;            // 4 waves of 64 lanes
 constexpr int kConvLdsBudgetBytes = 64 * 1024;    // preferred LDS per workgroup
 constexpr int kConvLdsMaxBytes = 160 * 1024;      // gfx950 LDS per workgroup
@@ -234,6 +236,47 @@ __host__ __device__ inline int cl_pixel_base(const ClLayout& c, const TileRuns& 
     return c.seg_base(s) + (m - tr.seg_m(s)) * a.cl_pitch + n * a.sw * a.fh - tr.seg_q(s);
 }
 
+// Packed bf16 filter of the fast kernels (whole 16-channel chunks, whole
+// tiles of BM output channels).  One block per (output-channel tile jt,
+// chunk ch), blocks in order jt*nchunks + ch, each 2*T*BM pieces of 16 bytes
+// laid out as the filter planes of an LDS stage: piece P = g*T*BM + t*BM + jj
+// holds channels 16ch + 8g .. 16ch + 8g + 7 of tap t (window order
+// t = v*Fh + u) of output channel jt*BM + jj.  A chunk's block is therefore
+// one contiguous range that 16-byte DMA copies into LDS unchanged.
+struct PackedPiece {
+    int j, c0, nat, lds_pos;   // output channel, first input channel, tap (u*Fw + v), LDS position
+};
+
+__host__ __device__ inline PackedPiece packed_piece(int64_t gid, int t_taps, int fh, int fw, int bm,
+                                                    int nchunks, int cl_fpb) {
+    const int pieces = 2 * t_taps * bm, plane = t_taps * bm;
+    const int64_t blk = gid / pieces;
+    const int pc = (int)(gid - blk * pieces);
+    const int jt = (int)(blk / nchunks), ch = (int)(blk - (int64_t)jt * nchunks);
+    const int g = pc / plane, q = pc - g * plane;
+    const int t = q / bm, jj = q - t * bm;
+    const int v = t / fh, u = t - v * fh;
+    PackedPiece r;
+    r.j = jt * bm + jj;
+    r.c0 = kBf16ChunkChannels * ch + 8 * g;
+    r.nat = u * fw + v;
+    r.lds_pos = g * cl_fpb + q;
+    return r;
+}
+
+// Inverse of packed_piece: the piece holding channels 16ch + 8g .. + 7 of tap
+// t of output channel j.
+__host__ __device__ inline int64_t packed_index(int j, int ch, int g, int t, int t_taps, int bm,
+                                                int nchunks) {
+    const int jt = j / bm, jj = j - jt * bm;
+    return (((int64_t)jt * nchunks + ch) * 2 + g) * (int64_t)(t_taps * bm) + (int64_t)t * bm + jj;
+}
+
+// Filter packing: a workgroup repacks kPackRows output channels x one chunk
+// of 16 input channels through LDS (reads of whole filter rows, writes of
+// kPackRows consecutive pieces).
+constexpr int kPackRows = 8;
+
 // Host bound of ClLayout::extent over the tiles of `bn` pixels.
 inline int64_t cl_extent_bound(const Geometry& g, int bn, int64_t pitch) {
     const int64_t dmax = (g.wo - 1 + bn - 1) / g.wo;
@@ -257,20 +300,21 @@ struct ConvPlan {
     int64_t cl_fpb = 0;      // bf16: positions per filter plane (strip planes: strip_cap)
     int64_t strip_items = 0; // bf16, 16-byte strip loads: bound of the staging items per tile
     int fused_fast = 0;      // bf16: the fused kernel builds strips from raw row items
+    int fast = 0;            // bf16 unfused: the fast kernel (16-byte strip loads, packed filter)
     int svec = 0;            // unfused: 16-byte strip copies
     int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
 };
 
 ConvPlan plan_conv_f32(const Geometry& g);
-ConvPlan plan_conv_bf16(const Geometry& g);
+ConvPlan plan_conv_bf16(const Geometry& g, bool fused);
 ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
                        float* y, bool fused);
 ConvArgs conv_args_bf16(const Geometry& g, const ConvPlan& p, const void* src, const void* w,
                         float* y, bool fused);
 
 // bf16 kernel: channels per chunk and per-thread staging registers (items)
-constexpr int kBf16Chunk = 16;
+constexpr int kBf16Chunk = kBf16ChunkChannels;
 constexpr int kBf16StripVecItems = 2;
 constexpr int kBf16StripScalarItems = 8;
 constexpr int kBf16FilterScalarItems = 16;
