@@ -74,6 +74,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter scaling)")
+    ap.add_argument("--table1", action="store_true",
+                    help="time the paper's twelve benchmark layers (Table 1: batch 128, fp32, no "
+                         "padding) instead: one line per layer, then a summary line")
     return ap.parse_args()
 
 
@@ -214,6 +217,34 @@ def cpu_baseline(wl, conv_flops):
             "sample": f"full workload (N={wl.n}), {reps} run(s), {total:.1f} s"}
 
 
+def table1_sweep(steps, warmup):
+    """The paper's benchmark layers (Sec. IV-A, Table 1) at its batch of 128:
+    each line as for a workload (no CPU baseline), then the workspace ratio
+    im2col / im2win averaged over the layers (Sec. IV-C prints 2.93) and the
+    sweep's aggregate rates."""
+    import torch
+    import workloads
+    lines = []
+    for wl in workloads.TABLE1:
+        line = run_workload(wl, steps, warmup, False)
+        line["sweep"] = "table1"
+        print(json.dumps(line), flush=True)
+        lines.append(line)
+        torch.cuda.empty_cache()
+    ratios = [l["workspace"]["im2col_bytes"] / l["workspace"]["im2win_bytes"] for l in lines]
+    flops = sum(l["conv_flops"] for l in lines)
+    t = {k: sum(l["kernels"][k]["ms"] for l in lines) * 1e-3 for k in ("transform", "conv2d", "conv2d_fused")}
+    print(json.dumps({
+        "sweep": "table1", "layers": len(lines), "batch": workloads.TABLE1_BATCH, "dtype": "f32",
+        "im2col_over_im2win_mean": round(sum(ratios) / len(ratios), 4),
+        "conv2d_GFLOP_per_s": round(flops / t["conv2d"] / 1e9, 1),
+        "conv2d_fused_GFLOP_per_s": round(flops / t["conv2d_fused"] / 1e9, 1),
+        "transform_plus_conv2d_GFLOP_per_s": round(flops / (t["transform"] + t["conv2d"]) / 1e9, 1),
+        "mfma_frac_conv2d": round(flops / t["conv2d"] / 1e12 / PEAK["f32"], 4),
+        "mfma_frac_conv2d_fused": round(flops / t["conv2d_fused"] / 1e12 / PEAK["f32"], 4),
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -224,6 +255,9 @@ def main():
         copy_calibration()
         return
     import workloads
+    if args.table1:
+        table1_sweep(args.steps, args.warmup)
+        return
     wl = workloads.BY_NAME[args.workload] if args.workload else workloads.HEADLINE
     if args.all_workloads:
         for other in workloads.WORKLOADS:

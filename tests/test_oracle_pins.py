@@ -303,3 +303,16 @@ def test_workload_shapes_fit_and_shrink_workspace():
         s = Shape(wl.n, wl.c, wl.h, wl.w, wl.k, wl.fh, wl.fw, wl.sh, wl.sw, wl.ph, wl.pw)
         assert s.wp <= s.fw * s.wo
         assert oracle.im2win_elems(s) < oracle.im2col_elems(s)
+
+
+def test_table1_workloads_are_the_printed_layers():
+    """The Table 1 workloads that the sweep times and the GPU tests check are
+    the printed layers (input, filter, stride, no padding) at the paper's batch."""
+    import workloads
+    t = json.load(open(os.path.join(GOLDEN, "table1.json")))
+    assert len(workloads.TABLE1) == len(t["layers"])
+    for wl, layer in zip(workloads.TABLE1, t["layers"]):
+        assert [wl.c, wl.h, wl.w] == layer["input"], layer["name"]
+        assert [wl.k, wl.fh, wl.fw] == layer["filter"], layer["name"]
+        assert wl.sh == wl.sw == layer["stride"] and wl.ph == wl.pw == 0, layer["name"]
+        assert wl.n == t["batch"] and wl.dtype == "f32"

@@ -61,6 +61,34 @@ WORKLOADS = [
 
 BY_NAME = {wl.name: wl for wl in WORKLOADS}
 
+# The paper's twelve benchmark layers (Sec. IV-A, Table 1): input Ci x Hi x Wi,
+# filter Co x Hf x Wf with stride s, no padding, batch 128 (Sec. IV-B), fp32.
+# The paper states no data distribution; these draw U[-1,1] inputs and
+# He-scaled normal weights.  Layer i (1-based) seeds x with 1000+10i+1 and w
+# with 1000+10i+2.
+_TABLE1_SHAPES = [
+    # (Ci, Hi, Wi, Co, Hf, Wf, s)
+    (3, 227, 227, 96, 11, 11, 4),
+    (3, 231, 231, 96, 11, 11, 4),
+    (3, 227, 227, 64, 7, 7, 2),
+    (64, 224, 224, 64, 7, 7, 2),
+    (96, 24, 24, 256, 5, 5, 1),
+    (256, 12, 12, 512, 3, 3, 1),
+    (3, 224, 224, 64, 3, 3, 1),
+    (64, 112, 112, 128, 3, 3, 1),
+    (64, 56, 56, 64, 3, 3, 1),
+    (128, 28, 28, 128, 3, 3, 1),
+    (256, 14, 14, 256, 3, 3, 1),
+    (512, 7, 7, 512, 3, 3, 1),
+]
+TABLE1_BATCH = 128
+TABLE1 = [
+    Workload(f"table1_conv{i}", TABLE1_BATCH, ci, hi, wi, co, hf, wf, s, s, 0, 0, "f32",
+             ("uniform", -1.0, 1.0), ("he",), 1000 + 10 * i + 1, 1000 + 10 * i + 2)
+    for i, (ci, hi, wi, co, hf, wf, s) in enumerate(_TABLE1_SHAPES, start=1)
+]
+BY_NAME.update({wl.name: wl for wl in TABLE1})
+
 # The workload the benchmark's headline line is quoted on.
 HEADLINE = BY_NAME["resnet_3x3_f32"]
 
