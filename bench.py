@@ -74,6 +74,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter scaling)")
+    ap.add_argument("--profile-call", choices=["transform", "conv2d", "conv2d_fused"], default=None,
+                    help="launch only this entry point (warmup + steps times) on the workload and "
+                         "print its mean launch time: the program that counter runs profile")
+    ap.add_argument("--traffic-summary", metavar="DIR", default=None,
+                    help="turn the counter runs under DIR (see profiles/hbm_traffic_all_workloads.md) "
+                         "into profiles/traffic.json and print the table")
     ap.add_argument("--table1", action="store_true",
                     help="time the paper's twelve benchmark layers (Table 1: batch 128, fp32, no "
                          "padding) instead: one line per layer, then a summary line")
@@ -217,6 +223,109 @@ def cpu_baseline(wl, conv_flops):
             "sample": f"full workload (N={wl.n}), {reps} run(s), {total:.1f} s"}
 
 
+def profile_call(wl, call, steps, warmup):
+    """warmup + steps launches of one entry point, nothing else on the GPU
+    after the inputs are made (the transform runs once first for conv2d)."""
+    import torch
+    import paper_2306_14320_amd as P
+    import workloads
+    dev = "cuda:0"
+    d = P.desc_for((wl.n, wl.c, wl.h, wl.w), (wl.k, wl.c, wl.fh, wl.fw), (wl.sh, wl.sw),
+                   (wl.ph, wl.pw), workloads.torch_dtype(wl.dtype))
+    ho, wo = P.im2win_output_shape(d)
+    ws_bytes = P.im2win_workspace_bytes(d)
+    x = workloads.make_input(wl).to(dev)
+    w = workloads.make_filter(wl).to(dev)
+    ws = torch.empty(P.workspace_shape(d), dtype=x.dtype, device=dev)
+    y = torch.empty((wl.n, wl.k, ho, wo), dtype=torch.float32, device=dev)
+    sp = torch.cuda.current_stream().cuda_stream
+    fn = {"transform": lambda: P.im2win_transform(d, x.data_ptr(), ws.data_ptr(), ws_bytes, sp),
+          "conv2d": lambda: P.im2win_conv2d(d, ws.data_ptr(), ws_bytes, w.data_ptr(), y.data_ptr(), sp),
+          "conv2d_fused": lambda: P.im2win_conv2d_fused(d, x.data_ptr(), w.data_ptr(), y.data_ptr(), sp)}[call]
+    if call == "conv2d":
+        P.im2win_transform(d, x.data_ptr(), ws.data_ptr(), ws_bytes, sp)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(warmup + steps):
+        fn()
+    torch.cuda.synchronize()
+    print(json.dumps({"workload": wl.name, "call": call, "launches": warmup + steps,
+                      "ms_per_launch": round((time.perf_counter() - t0) / (warmup + steps) * 1e3, 4)}),
+          flush=True)
+
+
+# Counter runs read by --traffic-summary, one rocprofv3 --pmc process each:
+#   DIR/calib_<COUNTER>/        bench.py --copy-calibration
+#   DIR/<workload>__<call>__<COUNTER>/   bench.py --workload <w> --profile-call <call>
+# with COUNTER in FETCH_SIZE, WRITE_SIZE.
+TRAFFIC_CALLS = {"transform": "transform", "conv2d": "conv", "conv2d_fused": "fused"}
+
+
+def _counter_rows(path):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {path}")
+    with open(files[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _per_dispatch(rows, select):
+    """Counter value summed per dispatch over the kernels `select` accepts:
+    {dispatch id: (kernel name, KiB)}."""
+    out = {}
+    for r in rows:
+        if select(r["Kernel_Name"]):
+            name, v = out.get(r["Dispatch_Id"], (r["Kernel_Name"], 0.0))
+            out[r["Dispatch_Id"]] = (name, v + float(r["Counter_Value"]))
+    return out
+
+
+def traffic_summary(root):
+    import workloads
+    copy = lambda n: "copyBuffer" in n
+    ours = lambda n: "im2win::" in n
+    factor = {}
+    for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+        disp = _per_dispatch(_counter_rows(os.path.join(root, "calib_" + ctr)), copy)
+        kib = max(v for _, v in disp.values())   # the 256 MiB copy (torch may add small copies)
+        factor[ctr] = (256 << 20) / (kib * 1024)
+    out = {"_calibration": {"copy_bytes": 256 << 20, "fetch_factor": round(factor["FETCH_SIZE"], 4),
+                            "write_factor": round(factor["WRITE_SIZE"], 4),
+                            "note": "HBM bytes = counter KiB * 1024 * factor"}}
+    print("| workload | call | kernels | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM read MB | HBM write MB |")
+    print("|---|---|---|---|---|---|---|")
+    for wl in workloads.WORKLOADS:
+        for call, kind in TRAFFIC_CALLS.items():
+            kib, names, calls = {}, set(), None
+            for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+                d = os.path.join(root, f"{wl.name}__{call}__{ctr}")
+                if not os.path.isdir(d):
+                    break
+                disp = _per_dispatch(_counter_rows(d), ours)
+                if call == "conv2d":   # the one transform launched before the timed calls
+                    disp = {k: v for k, v in disp.items() if "transform" not in v[0]}
+                main = [k for k, (n, _) in disp.items() if "pack_filter" not in n]
+                calls = len(main)
+                kib[ctr] = sum(v for _, v in disp.values()) / max(calls, 1)
+                names |= {n.replace("void ", "").replace("im2win::(anonymous namespace)::", "").split("(")[0]
+                          for n, _ in disp.values()}
+            if len(kib) != 2:
+                continue
+            fetch = int(kib["FETCH_SIZE"] * 1024 * factor["FETCH_SIZE"])
+            write = int(kib["WRITE_SIZE"] * 1024 * factor["WRITE_SIZE"])
+            src = "transform" if kind == "transform" else "conv"
+            out.setdefault(wl.name, {})[kind] = {
+                "kernels": sorted(names), "fetch_bytes": fetch, "write_bytes": write,
+                "bytes_per_launch": fetch + write, "launches": calls, "source_hash": source_hash(src)}
+            print(f"| {wl.name} | {call} | {', '.join('`%s`' % n for n in sorted(names))} | "
+                  f"{kib['FETCH_SIZE']:.1f} | {kib['WRITE_SIZE']:.1f} | {fetch / 1e6:.2f} | {write / 1e6:.2f} |")
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+
+
 def table1_sweep(steps, warmup):
     """The paper's benchmark layers (Sec. IV-A, Table 1) at its batch of 128:
     each line as for a workload (no CPU baseline), then the workspace ratio
@@ -254,7 +363,14 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary)
+        return
     import workloads
+    if args.profile_call:
+        profile_call(workloads.BY_NAME[args.workload] if args.workload else workloads.HEADLINE,
+                     args.profile_call, args.steps, args.warmup)
+        return
     if args.table1:
         table1_sweep(args.steps, args.warmup)
         return

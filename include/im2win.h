@@ -22,17 +22,20 @@
  *    the one of PyTorch's conv2d with these strides and paddings, no bias, no
  *    dilation, no groups).
  *  - Device pointers (x, w, ws, y) are owned by the caller.  Each must be
- *    16-byte aligned and the buffers must not overlap.  The library keeps no
- *    device memory between calls.  The one temporary it uses: bf16
- *    convolutions that run on its fast kernels (C a multiple of 16, K a
- *    multiple of 64, filter 3x3, 3x5 or 1x1, among other shape conditions)
- *    first rewrite w into the order those kernels copy to on-chip memory,
- *    in a buffer of K*C*Fh*Fw*2 bytes taken from the device's stream-ordered
- *    memory pool (hipMallocAsync on `stream`) and released on `stream`
- *    (hipFreeAsync) after the convolution; a failed allocation is EHIP.
+ *    16-byte aligned and the buffers must not overlap.  The only device
+ *    memory the library holds itself: bf16 convolutions that run on its fast
+ *    kernels (C a multiple of 16, K a multiple of 64, filter 3x3, 3x5 or 1x1,
+ *    among other shape conditions) first rewrite w into the order those
+ *    kernels copy to on-chip memory, in a buffer of K*C*Fh*Fw*2 bytes that
+ *    the library keeps per stream (the default stream once per device),
+ *    taken from the device's stream-ordered memory pool (hipMallocAsync on
+ *    that stream) and replaced, stream-ordered, only when a larger filter
+ *    needs more; it is held until the process ends.  A failed allocation is
+ *    EHIP.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Calls only
- *    enqueue work: they never synchronise, hold no state between calls and may
- *    be made from several host threads at once.
+ *    enqueue work: they never synchronise and may be made from several host
+ *    threads at once; apart from the per-stream filter buffer above they hold
+ *    no state between calls.
  *  - Return value: IM2WIN_OK or a negative IM2WIN_E* code.  Arguments are
  *    validated on the host before any HIP call, so an invalid call enqueues
  *    nothing.  im2win_last_error() then describes the failure.

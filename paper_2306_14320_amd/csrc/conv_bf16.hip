@@ -33,6 +33,9 @@
 #include "conv_common.h"
 
 #include <cstdio>
+#include <map>
+#include <mutex>
+#include <utility>
 
 namespace im2win {
 namespace {
@@ -368,15 +371,16 @@ __global__ __launch_bounds__(256) void pack_filter_bf16_kernel(const uint16_t* _
     const int T = fh * fw, run = kBf16ChunkChannels * T;
     const int ch = blockIdx.x % nchunks, jg = blockIdx.x / nchunks;
     const int j0 = jg * kPackRows;
-    // 2-byte elements: runs start at even element offsets only when T is even
-    for (int e = threadIdx.x; e < kPackRows * run; e += 256) {
-        const int r = e / run, q = e - r * run;
-        L[e] = w[((int64_t)(j0 + r) * c + kBf16ChunkChannels * ch) * T + q];
+    // 2-byte elements (runs start at even element offsets only when T is even)
+#pragma unroll
+    for (int r = 0; r < kPackRows; ++r) {
+        const uint16_t* src = w + ((int64_t)(j0 + r) * c + kBf16ChunkChannels * ch) * T;
+        for (int q = threadIdx.x; q < run; q += 256) L[r * run + q] = src[q];
     }
     __syncthreads();
     for (int pc = threadIdx.x; pc < 2 * T * kPackRows; pc += 256) {
         const int jj = pc % kPackRows, gt = pc / kPackRows;   // gt = g*T + t
-        const int g = gt / T, t = gt - g * T;
+        const int g = gt >= T ? 1 : 0, t = gt - g * T;
         const int v = t / fh, u = t - v * fh, nat = u * fw + v;
         const uint16_t* s = L + jj * run + 8 * g * T + nat;
         u32x4 o;
@@ -1126,6 +1130,41 @@ int bf16_strip_mode(const ConvPlan& p, bool fused) {
 // The fast kernels read the filter packed (packed_piece).
 bool bf16_packed(const ConvPlan& p, bool fused) { return fused ? p.fused_fast != 0 : p.fast != 0; }
 
+// One packed-filter buffer per stream (the legacy default stream counted once
+// per device), from the stream-ordered memory pool.  A call reuses its
+// stream's buffer, so steady-state calls enqueue no pool operations; a larger
+// filter replaces it by a stream-ordered free and allocation, after the work
+// already enqueued on the stream.  Calls on one stream are ordered, so they
+// never overwrite a buffer another call is still reading.
+struct PackBuffers {
+    std::mutex mu;
+    std::map<std::pair<int, hipStream_t>, std::pair<void*, size_t>> bufs;
+};
+
+static hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out) {
+    static PackBuffers pb;
+    int dev = -1;
+    if (stream == nullptr) {
+        const hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+    }
+    std::lock_guard<std::mutex> lock(pb.mu);
+    auto& slot = pb.bufs[{dev, stream}];
+    if (slot.second < bytes) {
+        if (slot.first) {
+            const hipError_t e = hipFreeAsync(slot.first, stream);
+            slot = {nullptr, 0};
+            if (e != hipSuccess) return e;
+        }
+        void* p = nullptr;
+        const hipError_t e = hipMallocAsync(&p, bytes, stream);
+        if (e != hipSuccess) return e;
+        slot = {p, bytes};
+    }
+    *out = slot.first;
+    return hipSuccess;
+}
+
 int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, float* y,
                      hipStream_t stream, char* err, size_t errlen) {
     const ConvPlan p = plan_conv_bf16(g, fused);
@@ -1146,10 +1185,9 @@ int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void*
     const int smode = bf16_strip_mode(p, fused);
     void* wpack = nullptr;
     if (bf16_packed(p, fused)) {
-        // the filter, repacked for 16-byte DMA, in a buffer of the stream's
-        // memory pool that lives until this call's kernels are done
+        // the filter, repacked for 16-byte DMA, in the stream's buffer
         const int64_t npieces = g.k * g.c * g.taps / 8;
-        const hipError_t e = hipMallocAsync(&wpack, (size_t)npieces * 16, stream);
+        const hipError_t e = packed_filter_buffer(stream, (size_t)npieces * 16, &wpack);
         if (e != hipSuccess) {
             snprintf(err, errlen, "conv: packed-filter buffer of %lld bytes: %s", (long long)npieces * 16,
                      hipGetErrorString(e));
@@ -1165,13 +1203,6 @@ int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void*
     else if (p.fvec && g.fh == 3 && g.fw == 5) launch_tile<3, 5, true>(p, a, blocks, smode, stream);
     else if (p.fvec && g.fh == 1 && g.fw == 1) launch_tile<1, 1, true>(p, a, blocks, smode, stream);
     else launch_tile<0, 0, false>(p, a, blocks, smode, stream);
-    if (wpack) {
-        const hipError_t e = hipFreeAsync(wpack, stream);
-        if (e != hipSuccess) {
-            snprintf(err, errlen, "conv: releasing the packed-filter buffer: %s", hipGetErrorString(e));
-            return -4;
-        }
-    }
     return 0;
 }
 

@@ -242,3 +242,30 @@ def test_bf16_error_against_unrounded_data():
     rel = np.linalg.norm(got - ref) / np.linalg.norm(ref)
     print(f"[parity] bf16 vs unrounded fp32 data: rel-L2 {rel:.3e}", flush=True)
     assert rel < 1e-2
+
+
+def test_bf16_packed_filter_per_stream():
+    """The bf16 fast kernels read a repacked filter that the library keeps per
+    stream: two streams with different filters in flight at once, then a
+    larger filter on the first stream (its buffer is replaced in stream
+    order), each result against the oracle."""
+    small = (2, 32, 14, 14, 64, 3, 3, 1, 1, 1, 1)
+    large = (1, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)
+    s1, s2 = torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)
+    runs = []
+    for seed, shape, stream in ((1, small, s1), (2, small, s2), (3, large, s1), (4, small, s2)):
+        wl, x_cpu, w_cpu = workloads.random_case(700 + seed, *shape, dtype="bf16")
+        _label("packed-filter stream", wl)
+        d = _desc(wl)
+        assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+        with torch.cuda.stream(stream):
+            x, w = x_cpu.to(DEV), w_cpu.to(DEV)
+            y_fused = P.conv2d_fused(x, w, d, stream=stream)
+            y = P.conv2d(P.transform(x, d, stream=stream), w, d, stream=stream)
+        runs.append((wl, x_cpu, w_cpu, y, y_fused))
+    torch.cuda.synchronize()
+    for wl, x_cpu, w_cpu, y, y_fused in runs:
+        ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
+        for what, out in (("unfused", y), ("fused", y_fused)):
+            _assert_close(out.cpu().numpy().astype(np.float64), ref, ref_abs, wl.c * wl.fh * wl.fw, "bf16",
+                          f"{wl.name} {what}")
