@@ -39,6 +39,14 @@ __device__ inline float to_f32(uint16_t v) { return __uint_as_float(uint32_t(v) 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Barrier that also publishes the copies this wave issued to LDS by DMA
+// (global_load_lds): they complete through the vector-memory counter, which
+// the workgroup barrier's own fence does not wait for.
+__device__ inline void dma_barrier() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+}
+
 // One wave copies `len` consecutive floats from global memory to LDS (DMA).
 __device__ inline void dma_run(const float* g, float* l, int len, int lane) {
     for (int e0 = 0; e0 < len; e0 += 64) {
@@ -635,7 +643,11 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     // X + (k % 2) * rc * raw_pitch): the copies of chunk c+2 land while chunk
     // c+1 is expanded, so the expansion needs no wait of its own and runs
     // ahead of the MFMAs of chunk c, all within one barrier interval.
-    float* const Xb[2] = {X, X + a.rc * a.raw_pitch + kExpandMaxRaw};
+    // (selected by arithmetic on the LDS base: a pointer picked from an array
+    // loses its address space, and reads through it become flat loads that
+    // wait for every copy in flight)
+    const int xstride = a.rc * a.raw_pitch + kExpandMaxRaw;
+    auto Xb = [&](int k) { return X + (k & 1) * xstride; };
     {
         const int rc_act = min(a.rc, a.c);
         const int rc_stage = ROWS ? rc_act : a.rc;
@@ -644,10 +656,10 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             for (int sg = 0; sg < 2; ++sg)
                 for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
             stage_raw(X, a, tr, rr, 0, rc_act);
-            if (use_map && nchunks > 1) stage_raw(Xb[1], a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
+            if (use_map && nchunks > 1) stage_raw(Xb(1), a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
             stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
-            __syncthreads();   // zeros written, raw rows of chunk 0 (and 1) landed
+            dma_barrier();   // zeros written, raw rows of chunk 0 (and 1) landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
             else expand_raw(S, X, a, tr, rr, rc_act, rc_stage);
         } else {
@@ -666,7 +678,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         const int rc1 = min(a.rc, a.c - r1);
         const int rc_stage1 = ROWS ? rc1 : a.rc;
         const int off = ((ch + 1) & 1) * a.stage;
-        __syncthreads();
+        dma_barrier();
         // MODE 3: a whole next chunk is copied from inside the MFMA loop
         const bool ilv_next = ILV && ch + 1 < nchunks && rc1 == a.rc;
         if (ch + 1 < nchunks && !ilv_next) {
@@ -674,8 +686,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
                 if (use_map) {
                     // a wave copies and expands the same channels (wave, wave + 4, ...)
-                    if (ch + 2 < nchunks) stage_raw(Xb[ch & 1], a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
-                    expand_map_apply<FHM>(S + off, Xb[(ch + 1) & 1], emap, a, tr, rc1, rc_stage1);
+                    if (ch + 2 < nchunks) stage_raw(Xb(ch), a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
+                    expand_map_apply<FHM>(S + off, Xb(ch + 1), emap, a, tr, rc1, rc_stage1);
                 } else {
                     stage_raw(X, a, tr, rr, r1, rc1);
                 }
