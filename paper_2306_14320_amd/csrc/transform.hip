@@ -17,6 +17,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <type_traits>
 
 namespace im2win {
 namespace {
@@ -26,7 +27,7 @@ constexpr int kOutTargetBytes = 32 * 1024;   // output bytes per workgroup (targ
 constexpr int kLdsBudgetBytes = 64 * 1024;   // LDS per workgroup (cap)
 
 template <typename T, int V>
-struct alignas(16) Vec {
+struct alignas(V * sizeof(T)) Vec {
     T v[V];
 };
 
@@ -57,37 +58,50 @@ __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
     const int total = blk.nplanes * per_plane;
     const int64_t plane_len = (int64_t)a.h * a.w;
     const bool vec_in = a.vec_in && ((int64_t)blk.y_lo * a.w) % V == 0;
-    auto place = [&](T v, int f) {
+    // Element f of the footprint and the VV after it lie in one input row
+    // (VV divides W): the row's destinations are decoded once, and element t
+    // goes to the first one's LDS index + t*Fh in each destination row.
+    auto place = [&](const T* v, int f, auto vv) {
+        constexpr int VV = decltype(vv)::value;
         const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
         const int rem = f - pj * per_plane;
         const int r = (int)fast_div((uint32_t)rem, a.div_w);
         const int yy = blk.y_lo + r, xx = rem - r * a.w;
         int mf, ml;
         blk.rows_of(yy, a, &mf, &ml);
-        for (int m = mf; m <= ml; ++m)
-            lds[blk.lds_index(pj, m, xx + a.pw, yy + a.ph - m * a.sh, a)] = v;
+        for (int m = mf; m <= ml; ++m) {
+            T* d = lds + blk.lds_index(pj, m, xx + a.pw, yy + a.ph - m * a.sh, a);
+#pragma unroll
+            for (int t = 0; t < VV; ++t) d[t * a.fh] = v[t];
+        }
     };
-    if (vec_in) {
-        // footprint vectors; plane starts, row y_lo and per_plane are multiples of V
-        const int nv = total / V;
+    // footprint vectors of VV elements: plane starts, row y_lo and per_plane
+    // are multiples of VV (VV divides W)
+    auto vec_pass = [&](auto vv) {
+        constexpr int VV = decltype(vv)::value;
+        typedef Vec<T, VV> VT;
+        const int nv = total / VV;
         for (int i0 = threadIdx.x; i0 < nv; i0 += 8 * kThreads) {
-            Vec<T, V> v[8];
+            VT v[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int i = i0 + j * kThreads;
-                const int f = i * V;
+                const int f = i * VV;
                 const int pj = a.g > 1 ? (int)fast_div((uint32_t)f, a.div_plane) : 0;
                 const int64_t src = (blk.plane0 + pj) * plane_len + (int64_t)blk.y_lo * a.w + (f - pj * per_plane);
-                if (i < nv) v[j] = *reinterpret_cast<const Vec<T, V>*>(x + src);
+                if (i < nv) v[j] = *reinterpret_cast<const VT*>(x + src);
             }
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int i = i0 + j * kThreads;
-                if (i < nv)
-#pragma unroll
-                    for (int t = 0; t < V; ++t) place(v[j].v[t], i * V + t);
+                if (i < nv) place(v[j].v, i * VV, vv);
             }
         }
+    };
+    if (vec_in) {
+        vec_pass(std::integral_constant<int, V>());
+    } else if (V > 2 && a.w % 2 == 0) {
+        vec_pass(std::integral_constant<int, 2>());
     } else {
         for (int f0 = threadIdx.x; f0 < total; f0 += 8 * kThreads) {
             T v[8];
@@ -100,7 +114,7 @@ __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
             }
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if (f0 + j * kThreads < total) place(v[j], f0 + j * kThreads);
+                if (f0 + j * kThreads < total) place(&v[j], f0 + j * kThreads, std::integral_constant<int, 1>());
         }
     }
     __syncthreads();
