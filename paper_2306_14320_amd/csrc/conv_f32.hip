@@ -213,44 +213,51 @@ __device__ inline int raw_segment(int r, const RawRows& rr, int nseg, const Conv
 // Fused fp32: copy the input rows that channels [r0, r0 + rc_act) of the
 // tile use into X[rc][0 .. rtot*W), segment after segment (DMA; the rows of
 // one segment are contiguous in x).  16-byte copies when rows are whole
-// vectors, else one float per lane.
+// vectors, else one float per lane.  BLOCKS: the copy units (vectors or
+// floats) of all the chunk's channels, in blocks of 64, go to the waves
+// round-robin (raw_blocks); expand_raw uses the same assignment, so a wave
+// expands what it copied, and chunks of fewer than four channels keep every
+// wave busy.  Otherwise wave w copies channels w, w + 4, ... (the expansion
+// map reads raw rows only after a barrier).
+__device__ inline int raw_blocks(const ConvArgs& a, const RawRows& rr, int* units) {
+    *units = a.xvec ? (rr.rtot * a.w_in) >> 2 : rr.rtot * a.w_in;
+    return (*units + 63) >> 6;
+}
+
+template <bool BLOCKS>
 __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr, const RawRows& rr,
                                  int r0, int rc_act) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const float* x = static_cast<const float*>(a.src);
     const int64_t plane = (int64_t)a.h * a.w_in;
-    const int n = rr.rtot * a.w_in;
     const int nseg = tr.nseg, i0 = tr.i0;
-    if (a.xvec) {
-        const int nq = n >> 2;
-        for (int rc = wave; rc < rc_act; rc += 4) {
-            const float* xp = x + ((int64_t)i0 * a.c + r0 + rc) * plane;
-            float* l = X + rc * a.raw_pitch;
-            for (int c0 = 0; c0 < nq; c0 += 64) {
-                const int c = c0 + lane;
-                const int e = 4 * c;
-                const int r = (int)fast_div((uint32_t)e, a.div_w);
-                int yy;
-                const int sg = raw_segment(r, rr, nseg, a, &yy);
-                if (c < nq)
-                    __builtin_amdgcn_global_load_lds(xp + (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in),
-                                                     (lds_void*)(l + 4 * c0), 16, 0, 0);
-            }
+    int units;
+    const int nb = raw_blocks(a, rr, &units);
+    // units c0 .. c0 + 63 of channel rc
+    auto copy_block = [&](int rc, int c0) {
+        const float* xp = x + ((int64_t)i0 * a.c + r0 + rc) * plane;
+        float* l = X + rc * a.raw_pitch;
+        const int c = c0 + lane;
+        const int e = a.xvec ? 4 * c : c;
+        const int r = (int)fast_div((uint32_t)e, a.div_w);
+        int yy;
+        const int sg = raw_segment(r, rr, nseg, a, &yy);
+        const float* src = xp + (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in);
+        if (c < units) {
+            if (a.xvec)
+                __builtin_amdgcn_global_load_lds(src, (lds_void*)(l + 4 * c0), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds(src, (lds_void*)(l + c0), 4, 0, 0);
+        }
+    };
+    if constexpr (BLOCKS) {
+        for (int gb = wave; gb < rc_act * nb; gb += 4) {
+            const int rc = gb / nb;
+            copy_block(rc, (gb - rc * nb) * 64);
         }
     } else {
-        for (int rc = wave; rc < rc_act; rc += 4) {
-            const float* xp = x + ((int64_t)i0 * a.c + r0 + rc) * plane;
-            float* l = X + rc * a.raw_pitch;
-            for (int e0 = 0; e0 < n; e0 += 64) {
-                const int e = e0 + lane;
-                const int r = (int)fast_div((uint32_t)e, a.div_w);
-                int yy;
-                const int sg = raw_segment(r, rr, nseg, a, &yy);
-                if (e < n)
-                    __builtin_amdgcn_global_load_lds(xp + (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in),
-                                                     (lds_void*)(l + e0), 4, 0, 0);
-            }
-        }
+        for (int rc = wave; rc < rc_act; rc += 4)
+            for (int c0 = 0; c0 < units; c0 += 64) copy_block(rc, c0);
     }
 }
 
@@ -266,11 +273,15 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
     const int nseg = tr.nseg, len0 = tr.len0, len_mid = tr.len_mid, len_last = tr.len_last,
               m0 = tr.m0, m1 = tr.m1, qa0 = tr.qa0, d_second = tr.d_second, d_stride = tr.d_stride;
     const int vw = a.xvec ? 4 : 1;
-    const int n = rr.rtot * a.w_in / vw;
-    for (int rc = wave; rc < rc_act; rc += 4) {
+    int n;
+    const int nb = raw_blocks(a, rr, &n);
+    for (int gb = wave; gb < rc_act * nb; gb += 4) {
+        const int rc = gb / nb;
         const float* xl = X + rc * a.raw_pitch;
         float* sl = S + rc * a.sc;
-        for (int q = lane; q < n; q += 64) {
+        {
+            const int q = (gb - rc * nb) * 64 + lane;
+            if (q >= n) continue;
             const int e = q * vw;
             const int r = (int)fast_div((uint32_t)e, a.div_w);
             const int xx = e - r * a.w_in;
@@ -655,8 +666,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             rr = raw_rows(tr, a);
             for (int sg = 0; sg < 2; ++sg)
                 for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
-            stage_raw(X, a, tr, rr, 0, rc_act);
-            if (use_map && nchunks > 1) stage_raw(Xb(1), a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
+            stage_raw<!use_map>(X, a, tr, rr, 0, rc_act);
+            if (use_map && nchunks > 1) stage_raw<false>(Xb(1), a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
             stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
             dma_barrier();   // zeros written, raw rows of chunk 0 (and 1) landed
@@ -685,11 +696,11 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             if constexpr (RAW) {
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
                 if (use_map) {
-                    // a wave copies and expands the same channels (wave, wave + 4, ...)
-                    if (ch + 2 < nchunks) stage_raw(Xb(ch), a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
+                    // copies of chunk c+2; expansion of chunk c+1, whose copies the barrier published
+                    if (ch + 2 < nchunks) stage_raw<false>(Xb(ch), a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
                     expand_map_apply<FHM>(S + off, Xb(ch + 1), emap, a, tr, rc1, rc_stage1);
                 } else {
-                    stage_raw(X, a, tr, rr, r1, rc1);
+                    stage_raw<true>(X, a, tr, rr, r1, rc1);
                 }
             } else {
                 stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
@@ -715,8 +726,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             }
         }
         if constexpr (RAW) {
-            // Without the map: a wave expands the channels whose raw rows it
-            // copied itself (channels wave, wave + 4, ...), so waiting for its
+            // Without the map: a wave expands the raw-row blocks it copied
+            // itself (the same round-robin assignment), so waiting for its
             // own copies is enough; the next barrier publishes the strips.
             if (!use_map && ch + 1 < nchunks) {
                 __builtin_amdgcn_sched_barrier(0);
