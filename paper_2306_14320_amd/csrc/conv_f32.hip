@@ -133,9 +133,14 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         const int64_t plane_len = (int64_t)a.ho * a.row_len;
         const int ck0 = tr.ck0, ck_mid = tr.ck_mid, ck_total = tr.ck_total;
         const int start0 = m0 * a.row_len + qa0 - tr.shift0;
-        for (int rc = wave; rc < rc_act; rc += 4) {
+        // blocks of 64 chunks of all the chunk's channels, to the waves
+        // round-robin (chunks of fewer than four channels keep every wave busy)
+        const int nb = (ck_total + 63) >> 6;
+        for (int gb = wave; gb < rc_act * nb; gb += 4) {
+            const int rc = gb / nb;
             float* l = S + rc * a.sc;
-            for (int c0 = 0; c0 < ck_total; c0 += 64) {
+            {
+                const int c0 = (gb - rc * nb) * 64;
                 const int c = c0 + lane;
                 int sgi = 0, cs = c;
                 if (c >= ck0) {
