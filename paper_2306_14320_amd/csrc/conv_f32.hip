@@ -136,11 +136,11 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         // blocks of 64 chunks of all the chunk's channels, to the waves
         // round-robin (chunks of fewer than four channels keep every wave busy)
         const int nb = (ck_total + 63) >> 6;
-        for (int gb = wave; gb < rc_act * nb; gb += 4) {
-            const int rc = gb / nb;
+        for (int rc = 0; rc < rc_act; ++rc) {
             float* l = S + rc * a.sc;
-            {
-                const int c0 = (gb - rc * nb) * 64;
+            // block rc*nb + b goes to wave (rc*nb + b) % 4
+            for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+                const int c0 = b * 64;
                 const int c = c0 + lane;
                 int sgi = 0, cs = c;
                 if (c >= ck0) {
@@ -157,6 +157,25 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         return;
     }
     const int nruns = rc_act * nseg;
+    if (!FUSED && kDma && nruns < 4) {
+        // fewer runs than waves (one or two channels): blocks of 64 floats of
+        // the runs, counted run after run, to the waves round-robin (block gb
+        // goes to wave gb % 4); otherwise whole runs, below
+        const float* srcf = reinterpret_cast<const float*>(src);
+        int gstart = 0;   // blocks before the current run
+        for (int rc = 0; rc < rc_act; ++rc)
+            for (int s = 0; s < nseg; ++s) {
+                const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0, d_first, d_second, d_stride);
+                const int nbq = (sr.len + 63) >> 6;
+                const float* g = srcf + (((int64_t)(i0 + s) * a.c + r0 + rc) * a.ho + sr.m) * a.row_len + sr.q;
+                float* l = S + rc * a.sc + sr.off;
+                for (int b = (wave - gstart) & 3; b < nbq; b += 4)
+                    if (64 * b + lane < sr.len)
+                        __builtin_amdgcn_global_load_lds(g + 64 * b + lane, (lds_void*)(l + 64 * b), 4, 0, 0);
+                gstart += nbq;
+            }
+        return;
+    }
     for (int q = wave; q < nruns; q += 4) {
         const int rc = q / nseg, s = q - rc * nseg;
         const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0, d_first, d_second, d_stride);
@@ -256,10 +275,9 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
         }
     };
     if constexpr (BLOCKS) {
-        for (int gb = wave; gb < rc_act * nb; gb += 4) {
-            const int rc = gb / nb;
-            copy_block(rc, (gb - rc * nb) * 64);
-        }
+        // block rc*nb + b goes to wave (rc*nb + b) % 4
+        for (int rc = 0; rc < rc_act; ++rc)
+            for (int b = (wave - rc * nb) & 3; b < nb; b += 4) copy_block(rc, b * 64);
     } else {
         for (int rc = wave; rc < rc_act; rc += 4)
             for (int c0 = 0; c0 < units; c0 += 64) copy_block(rc, c0);
@@ -280,12 +298,12 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
     const int vw = a.xvec ? 4 : 1;
     int n;
     const int nb = raw_blocks(a, rr, &n);
-    for (int gb = wave; gb < rc_act * nb; gb += 4) {
-        const int rc = gb / nb;
+    for (int rc = 0; rc < rc_act; ++rc) {
         const float* xl = X + rc * a.raw_pitch;
         float* sl = S + rc * a.sc;
-        {
-            const int q = (gb - rc * nb) * 64 + lane;
+        // block rc*nb + b goes to wave (rc*nb + b) % 4, as in stage_raw
+        for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+            const int q = b * 64 + lane;
             if (q >= n) continue;
             const int e = q * vw;
             const int r = (int)fast_div((uint32_t)e, a.div_w);
