@@ -558,23 +558,30 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
 // MFMAs of chunk c, which a single wave per SIMD cannot otherwise overlap.
 // Chunks past the last are loaded again from the last one and written to the
 // stage no MFMA reads any more, so no step needs a branch.
-// Per-thread staging registers of one chunk's strips (fast kernels).
-template <int SVI>
+// Per-thread staging registers of one chunk (unfused fast kernel): strips
+// and packed filter pieces.
+template <int SVI, int FI>
 struct FastStage {
-    uint32_t sd[SVI][16];          // 8 channels x 4 positions per item
+    uint32_t sd[SVI][16];          // strips: 8 channels x 4 positions per item
+    u32x4 fd[FI];                  // packed filter pieces threadIdx.x + 256*i
 };
 
 // Unfused kernel for the common case: whole 16-channel chunks, whole tiles of
 // output channels, window-tensor planes and rows of whole 4-element groups.
-// The filter comes packed (packed_piece) and is copied by 16-byte DMA, one
-// chunk ahead; the strips pass through registers two chunks ahead.
+// The filter comes packed (packed_piece): a thread's pieces go to LDS
+// unchanged.  Strips and filter pieces pass through registers two chunks
+// ahead, so every global load is one the compiler waits for precisely, and
+// the chunk barrier only waits for the LDS stores.
 template <int FH, int FW, int BM, int BN, int TJ, int TP, int SVI>
 __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a) {
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
     constexpr int T = FH * FW;
-    using St = FastStage<SVI>;
+    constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
+    constexpr int FI = (kPieces + kConvThreads - 1) / kConvThreads;   // filter pieces per thread
+    static_assert(FI <= T, "one filter piece stored per tap");
+    using St = FastStage<SVI, FI>;
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -623,12 +630,27 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
         sdst[k] = ((q & 1) * a.cl_pb + lds_pos(cl, rn, a, it.s, it.e)) * 8;
     }
     const int nchunks = a.c / kRC;
-    // packed filter blocks of this tile of output channels
+    // packed filter blocks of this tile of output channels; this thread's
+    // pieces P = threadIdx.x + 256*i and their LDS positions (the last piece
+    // again, never stored, where P runs past the block)
     const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
+    int fpc[FI], fdst[FI];
+#pragma unroll
+    for (int i = 0; i < FI; ++i) {
+        const int P = threadIdx.x + kConvThreads * i;
+        const int Pc = P < kPieces ? P : kPieces - 1;
+        const int g = Pc >= kPlane ? 1 : 0;
+        fpc[i] = Pc * 8;
+        fdst[i] = f_off + (g * a.cl_fpb + Pc - g * kPlane) * 8;
+    }
 
     St st0, st1;
     auto load = [&](St& r, int ch) {
-        const int r0 = (ch < nchunks ? ch : nchunks - 1) * kRC;
+        const int chc = ch < nchunks ? ch : nchunks - 1;
+        const uint16_t* fb = fblk + (int64_t)chc * (16 * T * BM);
+#pragma unroll
+        for (int i = 0; i < FI; ++i) r.fd[i] = load16(fb + fpc[i]);
+        const int r0 = chc * kRC;
 #pragma unroll
         for (int k = 0; k < SVI; ++k) {
             const uint16_t* p = sp[k] + (int64_t)r0 * plane;
@@ -640,8 +662,12 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
             }
         }
     };
-    // strip position t (< 4) of every item: 16-bit transpose, one 16-byte store
+    // part t of the stores of one stage: filter piece t (t < FI), and strip
+    // position t (t < 4) of every item (16-bit transpose, one 16-byte store)
     auto part = [&](const St& r, uint16_t* stg, int t) {
+        const int ti = t < FI ? t : 0;   // (indices stay inside the arrays when t >= FI)
+        if (t < FI && threadIdx.x + kConvThreads * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
+        if (t >= 4) return;
 #pragma unroll
         for (int k = 0; k < SVI; ++k) {
             u32x4 o;
@@ -663,20 +689,18 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[jb][pb][v] = 0.0f;
 
-    // chunk 0 into stage 0 (filter by DMA); chunk 1's strips in flight
-    dma_filter<T, BM>(fblk, lds + f_off, a.cl_fpb);
+    // chunk 0 into stage 0; chunk 1 in flight
     load(st0, 0);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) part(st0, lds, t);
+    for (int t = 0; t < (T > 4 ? T : 4); ++t) part(st0, lds, t);
     load(st1, 1);
 
     auto step = [&](int ch, St& r_ld, St& r_st) {
         const uint16_t* cur = lds + (ch & 1) * a.stage;
         uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
-        // chunk ch complete in LDS (this wave's DMA and stores, then everyone's),
-        // and every wave done with chunk ch-1, whose stage is refilled below
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        if (ch + 1 < nchunks) dma_filter<T, BM>(fblk + (int64_t)(ch + 1) * (16 * T * BM), nxt + f_off, a.cl_fpb);
+        // chunk ch complete in LDS (this wave's stores, then everyone's), and
+        // every wave done with chunk ch-1, whose stage is refilled below
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
         load(r_ld, ch + 2);
         __builtin_amdgcn_sched_barrier(0);   // keep the copies at the head of the step
         const uint16_t* F = cur + f_off;
@@ -701,7 +725,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
         for (int t = 0; t < T; ++t) {
             if (t + 2 < T) ld(av[(t + 2) % 3], bv[(t + 2) % 3], t + 2);
             mm(av[t % 3], bv[t % 3]);
-            if (t < 4) part(r_st, nxt, t);
+            part(r_st, nxt, t);
         }
 #pragma unroll
         for (int t2 = T; t2 < 4; ++t2) part(r_st, nxt, t2);   // strip positions when T < 4
