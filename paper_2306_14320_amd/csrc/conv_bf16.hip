@@ -55,7 +55,6 @@ __device__ inline uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu
 __device__ inline uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) uint32_t lds_u32;
 
 __device__ inline u32x4 load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ inline u32x2 load8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
@@ -387,26 +386,6 @@ __global__ __launch_bounds__(256) void pack_filter_bf16_kernel(const uint16_t* _
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = uint32_t(s[(2 * e) * T]) | (uint32_t(s[(2 * e + 1) * T]) << 16);
         store16(wp + packed_index(j0 + jj, ch, g, t, T, bm, nchunks) * 8, o);
-    }
-}
-
-// Copy one chunk's packed filter block (2*T*BM pieces) into the filter planes
-// of an LDS stage by 16-byte DMA: one instruction moves 64 consecutive pieces,
-// which land in 64 consecutive positions of one plane (T*BM is a multiple of
-// 64).  The caller's next vmcnt(0) wait and barrier publish them.
-template <int T, int BM>
-__device__ inline void dma_filter(const uint16_t* blk, uint16_t* planes, int cl_fpb) {
-    constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
-    static_assert(kPlane % 64 == 0, "a DMA instruction stays inside one plane");
-    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-#pragma unroll
-    for (int p0 = 0; p0 < kPieces; p0 += kConvThreads) {
-        const int P0 = p0 + 64 * wave;
-        if (P0 < kPieces) {
-            const int g = P0 >= kPlane ? 1 : 0;
-            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint32_t*>(blk + (int64_t)(P0 + lane) * 8),
-                                             (lds_u32*)(planes + (g * cl_fpb + P0 - g * kPlane) * 8), 16, 0, 0);
-        }
     }
 }
 
@@ -754,16 +733,16 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
 // Fused kernel for the same common case, and x rows of an even number of
 // elements: the strips are built on chip from the input rows the tile uses.
 // An item is a pair of neighbouring input elements of one row for the 8
-// channels of one half: each wave copies its items into LDS with 4-byte DMA
-// (a DMA lane may read any address, so the 8 channels of an item land side
-// by side, 32 bytes per item), and after the MFMAs of the chunk it expands
-// them: transposed to two 8-channel positions and written to every strip
-// position that holds them, one per window row m with filter row
-// u = y + ph - m*sh.  These destinations do not change between chunks, so
-// they are computed once; the ones outside the tile's runs go to the lane's
-// own spare slot at the end of the strip plane.  A wave only reads items it
-// copied, so it waits for its own copies; the chunk barrier publishes the
-// strips.  Padding positions are zeroed once.
+// channels of one half.  Each thread loads its item (eight 4-byte loads, one
+// per channel) and its packed filter pieces two chunks ahead, in registers;
+// while the MFMAs of chunk c run it transposes the item of chunk c+1 to two
+// 8-channel positions and writes them to every strip position that holds
+// them, one per window row m with filter row u = y + ph - m*sh, and stores
+// its filter pieces.  The destinations do not change between chunks, so they
+// are computed once; the ones outside the tile's runs go to the lane's own
+// spare slot at the end of the strip plane.  Every global load is one the
+// compiler waits for, so the chunk barrier only waits for the LDS stores.
+// Padding positions are zeroed once.
 template <int FH>
 struct FusedMap {
     int dst[2][FH];   // element offsets in a stage of the two positions, per window-row slot
@@ -780,7 +759,6 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
     const int f_off = 2 * a.cl_pb * 8;
-    uint32_t* X = reinterpret_cast<uint32_t*>(lds + 2 * a.stage);   // 8 dwords per item
 
     const int jtile = blockIdx.x % a.num_jtiles;
     const int ptile = blockIdx.x / a.num_jtiles;
@@ -824,20 +802,17 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
         if (*s > tr.nseg - 1) *s = tr.nseg - 1;
         *yy = *s == 0 ? rr.ylo0 + r : a.ylo_mid + (r - rr.r0 - (*s - 1) * a.rmid);
     };
-    // DMA sources: instruction i (of 8 per item block of this thread's wave)
-    // covers items base + 8i .. +7, lane L: item base + 8i + L/8, channel L%8
-    int64_t dsrc[IPT][8];
+    // item sources: channel 0 of the thread's items (items past nitems load
+    // item q & 1 instead, a valid address, and are never expanded)
+    int64_t xbase[IPT];
 #pragma unroll
-    for (int j = 0; j < IPT; ++j)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            int q = wave * 64 + j * kConvThreads + 8 * i + (lane >> 3);
-            if (q >= nitems) q = q & 1;   // a valid address; the item is never expanded
-            int sg, yy, xx;
-            item_at(q, &sg, &yy, &xx);
-            dsrc[j][i] = ((int64_t)(tr.i0 + sg) * a.c + 8 * (q & 1) + (lane & 7)) * xplane +
-                         (int64_t)yy * a.w_in + xx;
-        }
+    for (int j = 0; j < IPT; ++j) {
+        int q = threadIdx.x + j * kConvThreads;
+        if (q >= nitems) q &= 1;
+        int sg, yy, xx;
+        item_at(q, &sg, &yy, &xx);
+        xbase[j] = ((int64_t)(tr.i0 + sg) * a.c + 8 * (q & 1)) * xplane + (int64_t)yy * a.w_in + xx;
+    }
     // expansion map of this thread's items
     FusedMap<FH> mp[IPT];
 #pragma unroll
@@ -874,40 +849,56 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
         }
     }
     const int nchunks = a.c / kRC;
-    // packed filter blocks of this tile of output channels
+    // packed filter blocks of this tile of output channels, and this thread's
+    // pieces P = threadIdx.x + 256*i (the last piece again, never stored,
+    // where P runs past the block)
+    constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
+    constexpr int FI = (kPieces + kConvThreads - 1) / kConvThreads;
+    static_assert(FI <= T && FH <= T, "one filter piece and one window-row slot stored per tap");
     const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
-    auto dma = [&](int ch) {
-        const int64_t off = (int64_t)(ch < nchunks ? ch : nchunks - 1) * kRC * xplane;
+    int fpc[FI], fdst[FI];
 #pragma unroll
-        for (int j = 0; j < IPT; ++j) {
-            if (wave * 64 + j * kConvThreads < nitems) {   // this wave's block has items
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    __builtin_amdgcn_global_load_lds(
-                        reinterpret_cast<const uint32_t*>(xsrc + dsrc[j][i] + off),
-                        (lds_u32*)(X + (wave * 64 + j * kConvThreads + 8 * i) * 8), 4, 0, 0);
-            }
-        }
+    for (int i = 0; i < FI; ++i) {
+        const int P = threadIdx.x + kConvThreads * i;
+        const int Pc = P < kPieces ? P : kPieces - 1;
+        const int g = Pc >= kPlane ? 1 : 0;
+        fpc[i] = Pc * 8;
+        fdst[i] = f_off + (g * a.cl_fpb + Pc - g * kPlane) * 8;
+    }
+    struct Stage {
+        uint32_t xd[IPT][8];   // item: 2 elements x 8 channels
+        u32x4 fd[FI];
     };
-    auto expand = [&](uint16_t* stg) {
+    auto load = [&](Stage& r, int ch) {
+        const int chc = ch < nchunks ? ch : nchunks - 1;
+        const uint16_t* fb = fblk + (int64_t)chc * (16 * T * BM);
+#pragma unroll
+        for (int i = 0; i < FI; ++i) r.fd[i] = load16(fb + fpc[i]);
+        const int64_t off = (int64_t)chc * kRC * xplane;
+#pragma unroll
+        for (int j = 0; j < IPT; ++j)
+#pragma unroll
+            for (int c8 = 0; c8 < 8; ++c8)
+                r.xd[j][c8] = *reinterpret_cast<const uint32_t*>(xsrc + xbase[j] + off + c8 * xplane);
+    };
+    // part t of the stores of one stage: filter piece t (t < FI), and window
+    // row slot t (t < FH) of both positions of every item
+    auto part = [&](const Stage& r, uint16_t* stg, int t) {
+        const int ti = t < FI ? t : 0;
+        if (t < FI && threadIdx.x + kConvThreads * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
+        if (t >= FH) return;
+        const int tu = t < FH ? t : 0;
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
-            const int q = threadIdx.x + j * kConvThreads;
-            if (q < nitems) {
-                const u32x4 v0 = *reinterpret_cast<const u32x4*>(X + q * 8);
-                const u32x4 v1 = *reinterpret_cast<const u32x4*>(X + q * 8 + 4);
-                const uint32_t d[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+            if (threadIdx.x + j * kConvThreads < nitems) {
                 u32x4 o0, o1;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    o0[e] = lo_pair(d[2 * e], d[2 * e + 1]);
-                    o1[e] = hi_pair(d[2 * e], d[2 * e + 1]);
+                    o0[e] = lo_pair(r.xd[j][2 * e], r.xd[j][2 * e + 1]);
+                    o1[e] = hi_pair(r.xd[j][2 * e], r.xd[j][2 * e + 1]);
                 }
-#pragma unroll
-                for (int i = 0; i < FH; ++i) {
-                    store16(stg + mp[j].dst[0][i], o0);
-                    store16(stg + mp[j].dst[1][i], o1);
-                }
+                store16(stg + mp[j].dst[0][tu], o0);
+                store16(stg + mp[j].dst[1][tu], o1);
             }
         }
     };
@@ -926,19 +917,20 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
         for (int st = 0; st < 2; ++st)
             for (int e = threadIdx.x; e < 2 * a.cl_pb; e += kConvThreads) store16(lds + st * a.stage + e * 8, z);
     }
-    dma_filter<T, BM>(fblk, lds + f_off, a.cl_fpb);
-    dma(0);
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");   // zeros before strips
-    expand(lds);
+    Stage st0, st1;
+    load(st0, 0);
+    load(st1, 1);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");   // zeros before strips
+#pragma unroll
+    for (int t = 0; t < T; ++t) part(st0, lds, t);
 
-    auto step = [&](int ch) {
+    auto step = [&](int ch, Stage& r_ld, Stage& r_st) {
         const uint16_t* cur = lds + (ch & 1) * a.stage;
         uint16_t* nxt = lds + ((ch + 1) & 1) * a.stage;
-        // the wave's own copies of chunk ch landed before its expansion (end
-        // of the previous step); the barrier publishes everyone's
+        // chunk ch complete in LDS (this wave's stores, then everyone's), and
+        // every wave done with chunk ch-1, whose stage is refilled below
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        dma(ch + 1);
-        if (ch + 1 < nchunks) dma_filter<T, BM>(fblk + (int64_t)(ch + 1) * (16 * T * BM), nxt + f_off, a.cl_fpb);
+        load(r_ld, ch + 2);
         __builtin_amdgcn_sched_barrier(0);
         const uint16_t* F = cur + f_off;
         auto ld = [&](bf16x8 (&av)[NJ], bf16x8 (&bv)[NP], int t) {
@@ -961,12 +953,15 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
         for (int t = 0; t < T; ++t) {
             if (t + 2 < T) ld(av[(t + 2) % 3], bv[(t + 2) % 3], t + 2);
             mm(av[t % 3], bv[t % 3]);
+            if (ch + 1 < nchunks) part(r_st, nxt, t);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of chunk ch+1
-        expand(nxt);
     };
-    for (int ch = 0; ch < nchunks; ++ch) step(ch);
+    int ch = 0;
+    for (; ch + 2 <= nchunks; ch += 2) {
+        step(ch, st0, st1);
+        step(ch + 1, st1, st0);
+    }
+    if (ch < nchunks) step(ch, st0, st1);
 
 #pragma unroll
     for (int jb = 0; jb < NJ; ++jb)
@@ -1004,7 +999,6 @@ void launch_fast_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int svi, hi
 template <int FH, int FW, int BM, int BN, int TJ, int TP>
 void launch_fused_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, hipStream_t stream) {
     auto kern = conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP>;
-    lds += kConvThreads * kBf16FusedItems * 32;   // raw row items
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
