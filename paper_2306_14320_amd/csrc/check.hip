@@ -264,9 +264,9 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
             // elements it holds (spare slots aside)
             const RawRows rw = raw_rows(tr, a);
             const int nitems = rw.rtot * (int)g.w;
-            if (nitems > kConvThreads * kBf16FusedItems || (g.w & 1))
+            if (nitems > kConvThreads * p.fused_ipt || p.fused_ipt > kBf16FusedItems || (g.w & 1))
                 r.fail("%s tile %lld: %d raw items, registers hold %d", what, (long long)t, nitems,
-                       kConvThreads * kBf16FusedItems);
+                       kConvThreads * p.fused_ipt);
             for (int q = 0; q < nitems && r.violations < 16; ++q) {
                 const int e0 = 2 * (q >> 1);
                 const int rr2 = e0 / (int)g.w, xx = e0 - rr2 * (int)g.w;

@@ -748,13 +748,13 @@ struct FusedMap {
     int dst[2][FH];   // element offsets in a stage of the two positions, per window-row slot
 };
 
-template <int FH, int FW, int BM, int BN, int TJ, int TP>
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int IPT>
 __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs a) {
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+    static_assert(IPT >= 1 && IPT <= kBf16FusedItems, "raw items per thread");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
     constexpr int T = FH * FW;
-    constexpr int IPT = kBf16FusedItems;   // items per thread
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -997,8 +997,9 @@ void launch_fast_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int svi, hi
 }
 
 template <int FH, int FW, int BM, int BN, int TJ, int TP>
-void launch_fused_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, hipStream_t stream) {
-    auto kern = conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP>;
+void launch_fused_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int ipt, hipStream_t stream) {
+    auto kern = ipt == 1 ? conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 1>
+                         : conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 2>;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
@@ -1009,9 +1010,11 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode
     const int svi = p.strip_items > kConvThreads ? 2 : 1;
     if constexpr (FVEC && FH <= 3) {
         if (smode == kStripFused && p.fused_fast) {
-            if (p.bm == 128) launch_fused_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, stream);
-            else if (p.bn == 128) launch_fused_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, stream);
-            else launch_fused_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, stream);
+            const int ipt = p.fused_ipt;
+            if (p.bn == 256) launch_fused_cfg<FH, FW, 128, 256, 64, 128>(a, blocks, p.lds_bytes, ipt, stream);
+            else if (p.bm == 128) launch_fused_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, ipt, stream);
+            else if (p.bn == 128) launch_fused_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, ipt, stream);
+            else launch_fused_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, ipt, stream);
             return;
         }
     }
@@ -1076,9 +1079,9 @@ ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
         // fused kernel from raw row items: whole 16-channel chunks, whole
         // tiles of output channels, even rows, filters of up to 3 rows,
         // and the items of every tile in the per-thread registers and LDS
+        const int64_t raw_items = raw_rows_bound(g, t.bn) * g.w;   // per chunk and tile
         const bool fused_fast = fvec && g.c % kRC == 0 && g.k % t.bm == 0 && g.w % 2 == 0 && g.fh <= 3 &&
-                                raw_rows_bound(g, t.bn) * g.w <= (int64_t)kConvThreads * kBf16FusedItems &&
-                                lds + kConvThreads * kBf16FusedItems * 32 <= kConvLdsMaxBytes;
+                                raw_items <= (int64_t)kConvThreads * kBf16FusedItems;
         ConvPlan p;
         p.kind = ConvPlan::kBf16Lds;
         p.bm = t.bm; p.bn = t.bn; p.rc = kRC; p.tc = (int)g.taps;
@@ -1088,6 +1091,7 @@ ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
         p.fvec = fvec ? 1 : 0;
         p.strip_items = svec ? vec_items : 0;
         p.fused_fast = fused_fast ? 1 : 0;
+        p.fused_ipt = raw_items > kConvThreads ? 2 : 1;
         p.fast = fvec && svec && g.c % kRC == 0 && g.k % t.bm == 0 ? 1 : 0;
         const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
         if (blocks >= 256) {
@@ -1098,11 +1102,13 @@ ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
         if (blocks > best_blocks) { best = p; best_blocks = blocks; }
     }
     if (best.kind == ConvPlan::kNone) return plan_conv_f32(g);
-    // The unfused fast kernel also has a 128 x 256 tile (4 waves of 64 x 128:
+    // The fast kernels also have a 128 x 256 tile (4 waves of 64 x 128:
     // fewer LDS reads per matrix-core instruction and half the filter copies
     // per pixel).  It only fits one workgroup per CU, as 128 x 128 does, so it
     // is taken when it needs no more rounds of workgroups over the CUs.
-    if (!fused && best.fast && best.bm == 128 && best.bn == 128) {
+    const int64_t raw256 = raw_rows_bound(g, 256) * g.w;
+    if (best.bm == 128 && best.bn == 128 &&
+        (fused ? best.fused_fast && raw256 <= (int64_t)kConvThreads * kBf16FusedItems : best.fast)) {
         ConvPlan q = best;
         q.bn = 256;
         const int64_t run_vec = strip_capacity(g, 256, 4);
@@ -1117,7 +1123,7 @@ ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
             q.stage = stage;
             q.lds_bytes = 2 * stage * 2;
             q.strip_items = vec_items;
-            q.fused_fast = 0;
+            q.fused_ipt = raw256 > kConvThreads ? 2 : 1;
             return q;
         }
     }

@@ -301,6 +301,7 @@ struct ConvPlan {
     int64_t strip_items = 0; // bf16, 16-byte strip loads: bound of the staging items per tile
     int fused_fast = 0;      // bf16: the fused kernel builds strips from raw row items
     int fast = 0;            // bf16 unfused: the fast kernel (16-byte strip loads, packed filter)
+    int fused_ipt = 1;       // bf16 fused kernel: raw items per thread
     int svec = 0;            // unfused: 16-byte strip copies
     int fvec = 0;            // 16-byte filter-row copies
     int64_t lds_bytes = 0;
@@ -320,7 +321,7 @@ constexpr int kBf16StripScalarItems = 8;
 constexpr int kBf16FilterScalarItems = 16;
 constexpr int kF32ExpandGroups = 10;  // fused fp32 expansion map: raw floats per channel / 64
 constexpr int kBf16Spare = 64;        // spare positions at the end of every strip plane
-constexpr int kBf16FusedItems = 1;    // fused kernel: raw items per thread (2 elements x 8 channels)
+constexpr int kBf16FusedItems = 2;    // fused kernel: at most this many raw items per thread (2 elements x 8 channels)
 constexpr int kIlvSlots = 8;          // fp32 copies issued inside the MFMA loop: per lane and channel / chunk
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
