@@ -964,6 +964,8 @@ int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const
     else if (g.fh == 3 && g.fw == 3) launch_tile<float, 3, 3>(p, a, blocks, fused, stream);
     else if (g.fh == 3 && g.fw == 5) launch_tile<float, 3, 5>(p, a, blocks, fused, stream);
     else if (g.fh == 7 && g.fw == 7) launch_tile<float, 7, 7>(p, a, blocks, fused, stream);
+    else if (g.fh == 5 && g.fw == 5) launch_tile<float, 5, 5>(p, a, blocks, fused, stream);
+    else if (g.fh == 11 && g.fw == 11) launch_tile<float, 11, 11>(p, a, blocks, fused, stream);
     else if (g.fh == 1 && g.fw == 1) launch_tile<float, 1, 1>(p, a, blocks, fused, stream);
     else launch_tile<float, 0, 0>(p, a, blocks, fused, stream);
     return 0;
