@@ -23,7 +23,7 @@ namespace im2win {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kOutTargetBytes = 32 * 1024;   // output bytes per workgroup (target)
+constexpr int kOutTargetBytes = 24 * 1024;   // output bytes per workgroup (target)
 constexpr int kLdsBudgetBytes = 64 * 1024;   // LDS per workgroup (cap)
 
 template <typename T, int V>
@@ -181,12 +181,18 @@ XformPlan plan_transform(const Geometry& g) {
     const int64_t row_bytes = g.row_len * e;
     const int64_t plane_out = g.ho * row_bytes;
     int64_t tm, gp;
+    // the split is balanced: the last tile of a plane (or the last group of
+    // planes) is as large as the others, up to one row (plane)
     if (plane_out >= kOutTargetBytes / 2) {
         gp = 1;
         tm = std::max<int64_t>(1, std::min<int64_t>(g.ho, kOutTargetBytes / row_bytes));
+        const int64_t tiles = (g.ho + tm - 1) / tm;
+        tm = (g.ho + tiles - 1) / tiles;
     } else {
         tm = g.ho;
         gp = std::max<int64_t>(1, std::min<int64_t>(nc, kOutTargetBytes / plane_out));
+        const int64_t groups = (nc + gp - 1) / gp;
+        gp = (nc + groups - 1) / groups;
     }
     p.lds_bytes = (gp * tm * g.row_len + 2 * vec) * e;
     // the LDS kernel indexes a workgroup's run and footprint with 32-bit integers
