@@ -83,6 +83,13 @@ def parse():
     ap.add_argument("--table1", action="store_true",
                     help="time the paper's twelve benchmark layers (Table 1: batch 128, fp32, no "
                          "padding) instead: one line per layer, then a summary line")
+    ap.add_argument("--baselines", action="store_true",
+                    help="compare the im2win path with the paper's comparison systems on the GPU "
+                         "(im2col = unfold + GEMM, and direct convolution) and the vendor library "
+                         "convolution: times, speedups and peak device memory per workload (with "
+                         "--table1: per Table 1 layer), then a summary line")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="with --baselines: run every layer at this batch instead of its own")
     return ap.parse_args()
 
 
@@ -354,6 +361,142 @@ def table1_sweep(steps, warmup):
     }), flush=True)
 
 
+# ---------------------------------------------------------------------------
+# Comparison systems (Sec. IV-B, Fig. 4; Sec. IV-C, Fig. 6), on the GPU
+# ---------------------------------------------------------------------------
+
+def im2col_conv2d(x, w, stride, padding):
+    """im2col-based convolution: the framework's unfold (the im2col matrix,
+    N x C*Fh*Fw x Ho*Wo) and one batched GEMM with the filter as K x C*Fh*Fw
+    (the filter operand is shared by the batch).  fp32 in and out; bf16 inputs
+    give a bf16 GEMM result, returned widened to fp32."""
+    import torch
+    import torch.nn.functional as F
+    n, k = x.shape[0], w.shape[0]
+    fh, fw = w.shape[2], w.shape[3]
+    cols = F.unfold(x, (fh, fw), padding=padding, stride=stride)
+    a = w.reshape(k, -1).unsqueeze(0).expand(n, -1, -1)
+    y = torch.bmm(a, cols)
+    ho = (x.shape[2] + 2 * padding[0] - fh) // stride[0] + 1
+    wo = (x.shape[3] + 2 * padding[1] - fw) // stride[1] + 1
+    return y.view(n, k, ho, wo).float()
+
+
+def _time_calls(fn, stream, budget_s=1.0, max_reps=50):
+    """Mean duration of back-to-back calls between two events on `stream`
+    (after two warm-up calls), with as many calls as fit in about budget_s."""
+    import torch
+    fn(); fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    fn()
+    torch.cuda.synchronize()
+    one = time.perf_counter() - t0
+    reps = max(1, min(max_reps, int(budget_s / max(one, 1e-6))))
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e-3 / reps, reps
+
+
+def _peak_bytes(fn, resident_bytes):
+    """Device bytes at the peak of one call: what the call allocates (work
+    buffers, outputs) plus the inputs already resident (x and w)."""
+    import torch
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    out = fn()
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated() - base
+    del out
+    return peak + resident_bytes
+
+
+def compare_baselines(wl, n=None):
+    """One workload: the im2win path (transform + conv2d, as Alg. 2 / 3 call
+    the transformation first; and the fused path) against im2col + GEMM, the
+    direct convolution (no transformation) and the vendor library's conv2d,
+    all on the same device inputs; times, speedups and peak device memory."""
+    import dataclasses
+    import torch
+    import torch.nn.functional as F
+    import paper_2306_14320_amd as P
+    import workloads
+    if n is not None and n != wl.n:
+        wl = dataclasses.replace(wl, n=n)
+    dev = "cuda:0"
+    stride, pad = (wl.sh, wl.sw), (wl.ph, wl.pw)
+    d = P.desc_for((wl.n, wl.c, wl.h, wl.w), (wl.k, wl.c, wl.fh, wl.fw), stride, pad,
+                   workloads.torch_dtype(wl.dtype))
+    ho, wo = P.im2win_output_shape(d)
+    x = workloads.make_input(wl).to(dev)
+    w = workloads.make_filter(wl).to(dev)
+    stream = torch.cuda.current_stream()
+    resident = x.numel() * x.element_size() + w.numel() * w.element_size()
+    paths = {
+        "im2win": lambda: P.conv2d(P.transform(x, d), w, d),
+        "im2win_fused": lambda: P.conv2d_fused(x, w, d),
+        "im2col_gemm": lambda: im2col_conv2d(x, w, stride, pad),
+        "direct": lambda: P.direct_conv2d(x, w, d),
+        "vendor_conv2d": lambda: F.conv2d(x, w, stride=stride, padding=pad),
+    }
+    conv_flops = 2 * wl.n * wl.k * wl.c * ho * wo * wl.fh * wl.fw
+    res = {}
+    for name, fn in paths.items():
+        try:
+            t, reps = _time_calls(fn, stream)
+            mem = _peak_bytes(fn, resident)
+            res[name] = {"ms": round(t * 1e3, 4), "GFLOP_per_s": round(conv_flops / t / 1e9, 1),
+                         "peak_bytes": mem, "reps": reps}
+        except Exception as e:   # a comparison system that cannot run this shape is reported, not fatal
+            res[name] = {"error": f"{type(e).__name__}: {e}"[:200]}
+        torch.cuda.empty_cache()
+    ours = res["im2win"]
+    line = {"workload": wl.label(), "dtype": wl.dtype, "conv_flops": conv_flops, "paths": res}
+    if "ms" in ours:
+        line["speedup_vs"] = {k: round(v["ms"] / ours["ms"], 3) for k, v in res.items()
+                              if k != "im2win" and "ms" in v}
+        line["im2col_peak_over_im2win"] = (round(res["im2col_gemm"]["peak_bytes"] / ours["peak_bytes"], 4)
+                                           if "peak_bytes" in res["im2col_gemm"] else None)
+    return line
+
+
+def baselines_sweep(table1, batch):
+    import torch
+    import workloads
+    wls = workloads.TABLE1 if table1 else workloads.WORKLOADS
+    lines = []
+    for wl in wls:
+        line = compare_baselines(wl, batch)
+        line["sweep"] = "baselines-table1" if table1 else "baselines"
+        print(json.dumps(line), flush=True)
+        lines.append(line)
+        torch.cuda.empty_cache()
+    ok = [l for l in lines if "speedup_vs" in l]
+
+    def mean(key):
+        v = [l["speedup_vs"][key] for l in ok if key in l["speedup_vs"]]
+        return round(sum(v) / len(v), 3) if v else None
+    mem = [l["im2col_peak_over_im2win"] for l in ok if l.get("im2col_peak_over_im2win")]
+    print(json.dumps({
+        "sweep": "baselines-table1" if table1 else "baselines", "layers": len(lines),
+        "batch": batch or ("per layer" if not table1 else workloads.TABLE1_BATCH),
+        "mean_speedup_vs_im2col_gemm": mean("im2col_gemm"),
+        "mean_speedup_vs_direct": mean("direct"),
+        "mean_speedup_vs_vendor_conv2d": mean("vendor_conv2d"),
+        "mean_speedup_fused_vs_im2col_gemm": round(
+            sum(l["paths"]["im2col_gemm"]["ms"] / l["paths"]["im2win_fused"]["ms"] for l in ok
+                if "ms" in l["paths"]["im2col_gemm"] and "ms" in l["paths"]["im2win_fused"]) / max(len(ok), 1), 3),
+        "im2col_peak_over_im2win_mean": round(sum(mem) / len(mem), 4) if mem else None,
+        "im2col_peak_over_im2win_max": round(max(mem), 4) if mem else None,
+        "memory_reduction_vs_im2col_mean": round(sum(1 - 1 / m for m in mem) / len(mem), 4) if mem else None,
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -370,6 +513,9 @@ def main():
     if args.profile_call:
         profile_call(workloads.BY_NAME[args.workload] if args.workload else workloads.HEADLINE,
                      args.profile_call, args.steps, args.warmup)
+        return
+    if args.baselines:
+        baselines_sweep(args.table1, args.batch)
         return
     if args.table1:
         table1_sweep(args.steps, args.warmup)

@@ -74,6 +74,7 @@ def load_library():
         "im2win_transform": [D, P, P, SZ, P],
         "im2win_conv2d": [D, P, SZ, P, P, P],
         "im2win_conv2d_fused": [D, P, P, P, P],
+        "im2win_direct_conv2d": [D, P, P, P, P],
         "im2win_selftest": [],
         "im2win_check_plan": [D],
     }
@@ -124,6 +125,11 @@ def im2win_conv2d(desc: im2win_desc, ws: int, ws_bytes: int, w: int, y: int, str
 
 def im2win_conv2d_fused(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
     _check(load_library().im2win_conv2d_fused(ctypes.byref(desc), x, w, y, stream))
+
+
+def im2win_direct_conv2d(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
+    """Comparison baseline (include/im2win_baseline.h): direct convolution, no transformation."""
+    _check(load_library().im2win_direct_conv2d(ctypes.byref(desc), x, w, y, stream))
 
 
 def im2win_last_error() -> str:
@@ -207,4 +213,14 @@ def conv2d_fused(x: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.T
     if y is None:
         y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=x.device)
     im2win_conv2d_fused(desc, _dev(x, "x"), _dev(w, "w"), _dev(y, "y"), _stream(stream))
+    return y
+
+
+def direct_conv2d(x: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
+                  stream=None) -> torch.Tensor:
+    """Comparison baseline: direct convolution (no data transformation); returns y."""
+    ho, wo = im2win_output_shape(desc)
+    if y is None:
+        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=x.device)
+    im2win_direct_conv2d(desc, _dev(x, "x"), _dev(w, "w"), _dev(y, "y"), _stream(stream))
     return y

@@ -2,12 +2,14 @@
 // the host, problem geometry, and kernel dispatch.  Every check runs before
 // the first HIP call, so a rejected call enqueues nothing.
 #include "im2win.h"
+#include "im2win_baseline.h"
 
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 
 #include "common.h"
+#include "direct.h"
 
 namespace {
 
@@ -188,6 +190,17 @@ int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, floa
     rc = g.elem == 4 ? im2win::launch_conv_f32(g, true, x, w, y, s, msg, sizeof msg)
                      : im2win::launch_conv_bf16(g, true, x, w, y, s, msg, sizeof msg);
     return after_launch(rc, "conv2d_fused", msg);
+}
+
+int im2win_direct_conv2d(const im2win_desc* d, const void* x, const void* w, float* y,
+                         void* stream) {
+    im2win::Geometry g;
+    int rc = geometry(d, &g);
+    if (rc) return rc;
+    if (!x || !w || !y) return fail(IM2WIN_ENULL, "%s is NULL", !x ? "x" : !w ? "w" : "y");
+    char msg[256] = "";
+    rc = im2win::launch_direct_conv(g, x, w, y, static_cast<hipStream_t>(stream), msg, sizeof msg);
+    return after_launch(rc, "direct_conv2d", msg);
 }
 
 const char* im2win_last_error(void) { return g_err; }

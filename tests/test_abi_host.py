@@ -2,6 +2,7 @@
 every declared symbol, size queries agree with the oracle, invalid arguments
 are rejected before any HIP call, and every launch plan stays in bounds."""
 import ctypes
+import glob
 import os
 import random
 import re
@@ -14,7 +15,7 @@ import workloads
 import paper_2306_14320_amd as P
 from conftest import ROOT
 
-HEADER = os.path.join(ROOT, "include", "im2win.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def _desc(s: Shape, dtype=P.IM2WIN_F32):
@@ -30,10 +31,10 @@ def _wl_dtype(wl):
 
 
 def test_library_exports_every_declared_symbol():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     declared = set(re.findall(r"^\s*(?:int|const char\s*\*)\s*(im2win_\w+)\s*\(", text, re.M))
     assert {"im2win_workspace_bytes", "im2win_transform", "im2win_conv2d",
-            "im2win_conv2d_fused", "im2win_last_error"} <= declared
+            "im2win_conv2d_fused", "im2win_last_error", "im2win_direct_conv2d"} <= declared
     lib = ctypes.CDLL(P.LIB_PATH)
     for name in sorted(declared):
         assert hasattr(lib, name), name
@@ -89,6 +90,7 @@ def test_invalid_descriptor_rejected(field, value):
     assert _code(P.im2win_transform, d, FAKE, FAKE, 1 << 30, 0) == P.IM2WIN_EINVAL
     assert _code(P.im2win_conv2d, d, FAKE, 1 << 30, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
     assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_direct_conv2d, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
     assert P.im2win_last_error() != ""
 
 
@@ -104,6 +106,10 @@ def test_null_misaligned_and_short_workspace_rejected():
     assert _code(P.im2win_conv2d, d, FAKE, need, FAKE, FAKE + 8, 0) == P.IM2WIN_EALIGN
     assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, 0, 0) == P.IM2WIN_ENULL
     assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE + 2, FAKE, 0) == P.IM2WIN_EALIGN
+    for i in range(3):   # the direct baseline checks nulls (its pointers need no 16-byte alignment)
+        args = [FAKE, FAKE, FAKE]
+        args[i] = 0
+        assert _code(P.im2win_direct_conv2d, d, *args, 0) == P.IM2WIN_ENULL
     lib = P.load_library()
     assert lib.im2win_workspace_bytes(None, None) == P.IM2WIN_ENULL
     assert lib.im2win_workspace_bytes(ctypes.byref(d), None) == P.IM2WIN_ENULL
@@ -113,6 +119,7 @@ def test_oversized_problem_rejected():
     d = _desc(Shape(1 << 20, 4, 1024, 1024, 4, 3, 3, 1, 1, 1, 1))   # N*Ho*Wo >= 2^31
     assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EOVERFLOW
     assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
+    assert _code(P.im2win_direct_conv2d, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
 
 
 @pytest.mark.parametrize("wl", workloads.WORKLOADS, ids=lambda wl: wl.name)
