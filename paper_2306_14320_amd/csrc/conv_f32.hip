@@ -713,9 +713,10 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         const int rc_stage1 = ROWS ? rc1 : a.rc;
         const int off = ((ch + 1) & 1) * a.stage;
         dma_barrier();
-        // MODE 3: a whole next chunk is copied from inside the MFMA loop
-        const bool ilv_next = ILV && ch + 1 < nchunks && rc1 == a.rc;
-        if (ch + 1 < nchunks && !ilv_next) {
+        // MODE 3: a whole next chunk is copied from inside the MFMA loop (its
+        // plans have whole chunks only, so no chunk is staged here)
+        const bool ilv_next = ILV && ch + 1 < nchunks;
+        if (!ILV && ch + 1 < nchunks) {
             if constexpr (RAW) {
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
                 if (use_map) {
@@ -946,7 +947,7 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     const int64_t segs = p.bn / ((int64_t)g.ho * g.wo) + 2;
     // (byte offsets below 2^32); the filter-row split keeps the copies
     // before the MFMAs (its MODE 3 build holds too many registers)
-    a.ilv = (!fused && p.svec && p.fvec && p.split == 0 && p.sc / 4 <= 64 * kIlvSlots &&
+    a.ilv = (!fused && p.svec && p.fvec && p.split == 0 && g.c % p.rc == 0 && p.sc / 4 <= 64 * kIlvSlots &&
              (int64_t)p.bm * (p.fp / 4) <= (int64_t)kConvThreads * kIlvSlots &&
              segs * g.c * plane < (1ll << 30) && (int64_t)p.bm * g.c * g.fh * g.fw < (1ll << 30)) ? 1 : 0;
     return a;
