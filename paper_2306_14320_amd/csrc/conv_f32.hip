@@ -874,25 +874,31 @@ int choose_split(const Geometry& g) {
 
 }  // namespace
 
+// compute units of the MI355X (gfx950), for the tile-count cost below
+constexpr int64_t kCUs = 256;
+
 ConvPlan plan_conv_f32(const Geometry& g) {
-    // Tiles in order of preference; the first that gives every CU a
-    // workgroup is taken, else the one with the most workgroups.  (Larger
-    // tiles give each wave more independent accumulators and stage the
-    // filter less often; measured on the resnet 3x3 layer, 64x256 with 392
-    // workgroups beats 64x128 with 784.)  Both
-    // pipeline stages together are sized for 80 KB of LDS (two workgroups per
-    // CU); only shapes that fit nothing there use up to the full 160 KB.
-    const TileCfg small_k[] = {{64, 256}, {64, 128}, {64, 64}};
-    const TileCfg large_k[] = {{128, 128}, {64, 128}, {64, 64}};
-    const TileCfg* cfgs = g.k <= 64 ? small_k : large_k;
+    // Every tile shape that fits is costed and the cheapest is taken.  The
+    // cost of a shape is the work of one tile (bm x bn outputs over the whole
+    // reduction, padding included) times the number of tiles the busiest CU
+    // runs, ceil(tiles / 256), divided by the shape's relative matrix-core
+    // efficiency (measured on the 3x3 to 11x11 layers: a 64x256 tile keeps
+    // four 32x32 accumulators per wave and stages the filter least often; the
+    // 64x64 tile has one accumulator per wave).  A CU that runs only one tile
+    // has one wave per SIMD and reaches about half the rate, so a busiest-CU
+    // count of one costs double.  Both pipeline stages together are sized for
+    // 80 KB of LDS (two workgroups per CU); only shapes that fit nothing there
+    // use up to the full 160 KB.
+    struct Cand { TileCfg t; double eff; };
+    const Cand cands[] = {{{64, 256}, 1.0}, {{128, 128}, 0.85}, {{64, 128}, 0.87}, {{64, 64}, 0.7}};
     const int split = choose_split(g);
     const int step = split ? 1 : 2;
     const int64_t rc_max = std::min<int64_t>(split ? g.c : ((g.c + 1) & ~int64_t(1)), 32);
     for (const int64_t budget : {int64_t(kConvLdsPipelinedBytes), int64_t(kConvLdsMaxBytes)}) {
         ConvPlan best;
-        int64_t best_blocks = 0;
-        for (int ci = 0; ci < 3; ++ci) {
-            const TileCfg t = cfgs[ci];
+        double best_cost = 0.0;
+        for (const Cand& cd : cands) {
+            const TileCfg t = cd.t;
             const bool vec = strips_vec(g);
             const int64_t cap = strip_capacity(g, t.bn, vec ? 4 : 0);
             // largest chunk that fits; among those that keep the filter rows
@@ -916,9 +922,10 @@ ConvPlan plan_conv_f32(const Geometry& g) {
             }
             if (pv.kind != ConvPlan::kNone) p = pv;
             if (p.kind == ConvPlan::kNone) continue;
-            const int64_t blocks = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
-            if (blocks >= 256) return p;
-            if (blocks > best_blocks) { best = p; best_blocks = blocks; }
+            const int64_t tiles = ((g.npix + t.bn - 1) / t.bn) * ((g.k + t.bm - 1) / t.bm);
+            const int64_t per_cu = (tiles + kCUs - 1) / kCUs;
+            const double cost = double(per_cu) * (per_cu == 1 ? 2.0 : 1.0) * t.bm * t.bn / cd.eff;
+            if (best.kind == ConvPlan::kNone || cost < best_cost) { best = p; best_cost = cost; }
         }
         if (best.kind != ConvPlan::kNone) return best;
     }
