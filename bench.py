@@ -117,6 +117,9 @@ def run_workload(wl, steps, warmup, with_cpu):
     ho, wo = P.im2win_output_shape(d)
     ws_bytes = P.im2win_workspace_bytes(d)
     col_bytes = P.im2win_im2col_bytes(d)
+    dt = P.desc_for((wl.n, wl.c, wl.h, wl.w), (wl.k, wl.c, wl.fh, wl.fw), (wl.sh, wl.sw),
+                    (wl.ph, wl.pw), workloads.torch_dtype(wl.dtype), layout=P.IM2WIN_ROWS_TRIMMED)
+    trimmed_bytes = P.im2win_workspace_bytes(dt)
     x = workloads.make_input(wl).to(dev)
     w = workloads.make_filter(wl).to(dev)
     ws = torch.empty(P.workspace_shape(d), dtype=x.dtype, device=dev)
@@ -202,7 +205,9 @@ def run_workload(wl, steps, warmup, with_cpu):
             "transform_plus_conv2d_GFLOP_per_s": round(conv_flops / (t_xf + t_cv) / 1e9, 1),
         },
         "workspace": {"im2win_bytes": ws_bytes, "im2col_bytes": col_bytes,
-                      "im2win_over_im2col": round(ws_bytes / col_bytes, 4)},
+                      "im2win_over_im2col": round(ws_bytes / col_bytes, 4),
+                      "im2win_trimmed_bytes": trimmed_bytes,
+                      "im2win_trimmed_over_im2col": round(trimmed_bytes / col_bytes, 4)},
         "conv_flops": conv_flops,
     }
     if with_cpu:
@@ -348,11 +353,13 @@ def table1_sweep(steps, warmup):
         lines.append(line)
         torch.cuda.empty_cache()
     ratios = [l["workspace"]["im2col_bytes"] / l["workspace"]["im2win_bytes"] for l in lines]
+    ratios_t = [l["workspace"]["im2col_bytes"] / l["workspace"]["im2win_trimmed_bytes"] for l in lines]
     flops = sum(l["conv_flops"] for l in lines)
     t = {k: sum(l["kernels"][k]["ms"] for l in lines) * 1e-3 for k in ("transform", "conv2d", "conv2d_fused")}
     print(json.dumps({
         "sweep": "table1", "layers": len(lines), "batch": workloads.TABLE1_BATCH, "dtype": "f32",
         "im2col_over_im2win_mean": round(sum(ratios) / len(ratios), 4),
+        "im2col_over_im2win_trimmed_mean": round(sum(ratios_t) / len(ratios_t), 4),
         "conv2d_GFLOP_per_s": round(flops / t["conv2d"] / 1e9, 1),
         "conv2d_fused_GFLOP_per_s": round(flops / t["conv2d_fused"] / 1e9, 1),
         "transform_plus_conv2d_GFLOP_per_s": round(flops / (t["transform"] + t["conv2d"]) / 1e9, 1),
@@ -437,8 +444,11 @@ def compare_baselines(wl, n=None):
     w = workloads.make_filter(wl).to(dev)
     stream = torch.cuda.current_stream()
     resident = x.numel() * x.element_size() + w.numel() * w.element_size()
+    dt = P.desc_for((wl.n, wl.c, wl.h, wl.w), (wl.k, wl.c, wl.fh, wl.fw), stride, pad,
+                    workloads.torch_dtype(wl.dtype), layout=P.IM2WIN_ROWS_TRIMMED)
     paths = {
         "im2win": lambda: P.conv2d(P.transform(x, d), w, d),
+        "im2win_trimmed": lambda: P.conv2d(P.transform(x, dt), w, dt),
         "im2win_fused": lambda: P.conv2d_fused(x, w, d),
         "im2col_gemm": lambda: im2col_conv2d(x, w, stride, pad),
         "direct": lambda: P.direct_conv2d(x, w, d),

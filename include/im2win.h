@@ -14,8 +14,8 @@
  *      x  input   N x C x H x W
  *      w  filter  K x C x Fh x Fw
  *      y  output  N x K x Ho x Wo, always fp32
- *      ws window tensor N x C x Ho x (Wp*Fh), same dtype as x
- *    with Wp = W + 2*pad_w,
+ *      ws window tensor N x C x Ho x (Wr*Fh), same dtype as x
+ *    with Wr the row width of d->layout (Wp = W + 2*pad_w by default),
  *         Ho = floor((H + 2*pad_h - Fh) / stride_h) + 1,
  *         Wo = floor((W + 2*pad_w - Fw) / stride_w) + 1.
  *  - Padding is symmetric zero padding (not in the paper; the convolution is
@@ -58,6 +58,24 @@ typedef enum {
     IM2WIN_BF16 = 1   /* bfloat16; products and sums in fp32 */
 } im2win_dtype;
 
+/*
+ * Width Wr of the window tensor's rows, in input columns (each row holds
+ * Wr*Fh elements).
+ *  - PADDED: Wr = Wp = W + 2*pad_w, every column of the padded input
+ *    (Sec. III-A sizes the tensor with the full input width).
+ *  - TRIMMED: Wr = Wt = (Wo-1)*stride_w + Fw, only the columns some window
+ *    reads (the padded layout also holds the trailing columns the last
+ *    window does not reach).  Then the window tensor is never larger than
+ *    the im2col matrix when Fw >= stride_w: im2col - im2win =
+ *    N*C*Fh*Ho*(Wo-1)*(Fw - stride_w) elements.
+ * Both layouts give the same convolution; a window tensor must be read with
+ * the layout it was written with.
+ */
+typedef enum {
+    IM2WIN_ROWS_PADDED = 0,
+    IM2WIN_ROWS_TRIMMED = 1
+} im2win_layout;
+
 /* Problem description (all fields by value, nothing retained). */
 typedef struct {
     int64_t n, c, h, w;          /* input N x C x H x W */
@@ -65,11 +83,12 @@ typedef struct {
     int64_t stride_h, stride_w;  /* >= 1 */
     int64_t pad_h, pad_w;        /* >= 0, zero padding on both sides */
     int32_t dtype;               /* an im2win_dtype */
+    int32_t layout;              /* an im2win_layout; 0 (zero-initialised) = PADDED */
 } im2win_desc;
 
 enum {
     IM2WIN_OK = 0,
-    IM2WIN_EINVAL = -1,      /* bad shape, stride, padding, dtype, or Ho/Wo < 1 */
+    IM2WIN_EINVAL = -1,      /* bad shape, stride, padding, dtype, layout, or Ho/Wo < 1 */
     IM2WIN_ENULL = -2,       /* a required pointer is NULL */
     IM2WIN_EWORKSPACE = -3,  /* ws_bytes is smaller than im2win_workspace_bytes() */
     IM2WIN_EHIP = -4,        /* the HIP runtime reported an error at launch */
@@ -78,10 +97,11 @@ enum {
 };
 
 /*
- * Size in bytes of the window tensor, N*C*Ho*(Wp*Fh)*sizeof(dtype)
- * (Sec. III-A size analysis: N x C x Ho x (Wi*Hf), with the padded width).
- * Unlike Alg. 1, which falls back to the input size when Fh <= stride, this
- * is always the full N x C x Ho x Wp*Fh tensor that im2win_transform writes.
+ * Size in bytes of the window tensor, N*C*Ho*(Wr*Fh)*sizeof(dtype)
+ * (Sec. III-A size analysis: N x C x Ho x (Wi*Hf), with the row width Wr of
+ * d->layout in place of Wi).  Unlike Alg. 1, which falls back to the input
+ * size when Fh <= stride, this is always the full N x C x Ho x Wr*Fh tensor
+ * that im2win_transform writes.
  * Host only; `bytes` receives the size.  Errors: EINVAL, ENULL, EOVERFLOW.
  */
 int im2win_workspace_bytes(const im2win_desc* d, size_t* bytes);
@@ -102,7 +122,7 @@ int im2win_output_shape(const im2win_desc* d, int64_t* ho, int64_t* wo);
 /*
  * The im2win transformation (Alg. 1, Eq. 2) with zero padding:
  *   ws[i][r][m][k*Fh + u] = x[i][r][m*stride_h + u - pad_h][k - pad_w]
- * for k < Wp, u < Fh, and +0 where the source lies in the padding.  Each row
+ * for k < Wr, u < Fh, and +0 where the source lies in the padding.  Each row
  * of the window tensor holds, column by column, the Fh input rows that the
  * windows of output row m cover, so the window of output column n is the
  * contiguous run [n*stride_w*Fh, (n*stride_w + Fw)*Fh) of that row.

@@ -30,17 +30,19 @@ def _load():
         lib.oracle_out_extent.restype = i64
         lib.oracle_out_extent.argtypes = [i64, i64, i64, i64]
         lib.oracle_im2win_elems.restype = i64
-        lib.oracle_im2win_elems.argtypes = [p]
+        lib.oracle_im2win_elems.argtypes = [p, ctypes.c_int]
+        lib.oracle_row_width.restype = i64
+        lib.oracle_row_width.argtypes = [p, ctypes.c_int]
         lib.oracle_im2col_elems.restype = i64
         lib.oracle_im2col_elems.argtypes = [p]
         lib.oracle_im2win.restype = None
-        lib.oracle_im2win.argtypes = [p, p, p, ctypes.c_int]
+        lib.oracle_im2win.argtypes = [p, p, p, ctypes.c_int, ctypes.c_int]
         lib.oracle_direct_conv.restype = None
         lib.oracle_direct_conv.argtypes = [p, p, p, p, p]
         lib.oracle_direct_conv_at.restype = None
         lib.oracle_direct_conv_at.argtypes = [p, p, p, p, i64, p, p]
         lib.oracle_window_conv.restype = None
-        lib.oracle_window_conv.argtypes = [p, p, p, p]
+        lib.oracle_window_conv.argtypes = [p, p, p, p, ctypes.c_int]
         lib.oracle_im2col.restype = None
         lib.oracle_im2col.argtypes = [p, p, p]
         _lib = lib
@@ -78,6 +80,14 @@ class Shape:
         return self.w + 2 * self.pw
 
     @property
+    def wt(self) -> int:
+        """Trimmed row width: the columns some window reads."""
+        return int(_load().oracle_row_width(_ptr(self.vec()), 1))
+
+    def win_shape_of(self, trimmed: bool):
+        return (self.n, self.c, self.ho, (self.wt if trimmed else self.wp) * self.fh)
+
+    @property
     def out_shape(self):
         return (self.n, self.k, self.ho, self.wo)
 
@@ -96,10 +106,10 @@ def out_extent(size: int, f: int, s: int, pad: int) -> int:
     return int(_load().oracle_out_extent(size, f, s, pad))
 
 
-def im2win_elems(shp: Shape) -> int:
-    """Elements of the window tensor N x C x Ho x (Wp*Fh)."""
+def im2win_elems(shp: Shape, trimmed: bool = False) -> int:
+    """Elements of the window tensor N x C x Ho x (Wr*Fh), Wr = Wp or the trimmed width."""
     v = shp.vec()
-    return int(_load().oracle_im2win_elems(_ptr(v)))
+    return int(_load().oracle_im2win_elems(_ptr(v), int(trimmed)))
 
 
 def im2col_elems(shp: Shape) -> int:
@@ -108,14 +118,15 @@ def im2col_elems(shp: Shape) -> int:
     return int(_load().oracle_im2col_elems(_ptr(v)))
 
 
-def im2win(shp: Shape, x: np.ndarray) -> np.ndarray:
-    """Window tensor of x (2-, 4- or 8-byte elements, copied bit for bit)."""
+def im2win(shp: Shape, x: np.ndarray, trimmed: bool = False) -> np.ndarray:
+    """Window tensor of x (2-, 4- or 8-byte elements, copied bit for bit), with
+    rows of the padded width Wp, or of the trimmed width when asked."""
     x = np.ascontiguousarray(x)
     assert x.shape == (shp.n, shp.c, shp.h, shp.w), x.shape
     assert x.itemsize in (2, 4, 8)
-    out = np.empty(shp.win_shape, dtype=x.dtype)
+    out = np.empty(shp.win_shape_of(trimmed), dtype=x.dtype)
     v = shp.vec()
-    _load().oracle_im2win(_ptr(v), _ptr(x), _ptr(out), x.itemsize)
+    _load().oracle_im2win(_ptr(v), _ptr(x), _ptr(out), x.itemsize, int(trimmed))
     return out
 
 
@@ -151,13 +162,13 @@ def direct_conv_at(shp: Shape, x: np.ndarray, w: np.ndarray, idx: np.ndarray):
     return y, ya
 
 
-def window_conv(shp: Shape, win: np.ndarray, w: np.ndarray) -> np.ndarray:
+def window_conv(shp: Shape, win: np.ndarray, w: np.ndarray, trimmed: bool = False) -> np.ndarray:
     """Alg. 2 (basic im2win-based convolution) over a window tensor, fp64."""
     win, w = _f64(win), _f64(w)
-    assert win.shape == shp.win_shape
+    assert win.shape == shp.win_shape_of(trimmed)
     y = np.empty(shp.out_shape, dtype=np.float64)
     v = shp.vec()
-    _load().oracle_window_conv(_ptr(v), _ptr(win), _ptr(w), _ptr(y))
+    _load().oracle_window_conv(_ptr(v), _ptr(win), _ptr(w), _ptr(y), int(trimmed))
     return y
 
 

@@ -51,12 +51,20 @@ int64_t oracle_out_extent(int64_t in, int64_t f, int64_t s, int64_t pad) {
     return span / s + 1;
 }
 
-/* Elements of the window tensor: N x C x Ho x (Wp * Fh)  (Sec. III-A, size
- * analysis, with the padded width Wp in place of Wi). */
-int64_t oracle_im2win_elems(const int64_t *shp) {
+/* Columns per window-tensor row.  trimmed = 0: the padded width Wp, every
+ * column of the padded input (Sec. III-A sizes the rows with the input width).
+ * trimmed = 1: only the columns some window reads; the last window starts at
+ * column (Wo-1)*sw and spans Fw columns, so (Wo-1)*sw + Fw. */
+int64_t oracle_row_width(const int64_t *shp, int trimmed) {
+    if (!trimmed) return W_ + 2 * PW_;
+    return (oracle_out_extent(W_, FW_, SW_, PW_) - 1) * SW_ + FW_;
+}
+
+/* Elements of the window tensor: N x C x Ho x (Wr * Fh)  (Sec. III-A, size
+ * analysis, with the row width Wr in place of Wi). */
+int64_t oracle_im2win_elems(const int64_t *shp, int trimmed) {
     int64_t ho = oracle_out_extent(H_, FH_, SH_, PH_);
-    int64_t wp = W_ + 2 * PW_;
-    return N_ * C_ * ho * wp * FH_;
+    return N_ * C_ * ho * oracle_row_width(shp, trimmed) * FH_;
 }
 
 /* Elements of the im2col matrix for the same convolution: per image a
@@ -68,13 +76,13 @@ int64_t oracle_im2col_elems(const int64_t *shp) {
 }
 
 /* The im2win transformation, Alg. 1 with zero padding:
- *   win[i][r][m][k*Fh + u] = Ipad[i][r][m*sh + u][k],  k < Wp, u < Fh,
+ *   win[i][r][m][k*Fh + u] = Ipad[i][r][m*sh + u][k],  k < Wr, u < Fh,
  * where Ipad is the input with ph zero rows and pw zero columns on each side.
  * A pure copy of `elem_bytes`-sized elements (4 for fp32, 2 for bf16, 8 for fp64), so the
  * result is unique and any implementation must reproduce it bit for bit. */
-void oracle_im2win(const int64_t *shp, const void *x, void *win, int elem_bytes) {
+void oracle_im2win(const int64_t *shp, const void *x, void *win, int elem_bytes, int trimmed) {
     const int64_t ho = oracle_out_extent(H_, FH_, SH_, PH_);
-    const int64_t wp = W_ + 2 * PW_;
+    const int64_t wp = oracle_row_width(shp, trimmed);   /* Wr */
     const int64_t row = wp * FH_;
     const unsigned char *src = (const unsigned char *)x;
     unsigned char *dst = (unsigned char *)win;
@@ -152,14 +160,15 @@ void oracle_direct_conv_at(const int64_t *shp, const double *x, const double *w,
 }
 
 /* Basic im2win-based convolution (Alg. 2) evaluated on a window tensor `win`
- * (N x C x Ho x Wp*Fh, as produced by the transformation):
+ * (N x C x Ho x Wr*Fh, as produced by the transformation):
  *   O[i][j][m][n] = sum_r sum_u sum_v win[i][r][m][(n*sw + v)*Fh + u] * F[j][r][u][v]
  * The window of output column n begins at input column n*sw, which sits at
  * offset n*sw*Fh of the row. */
-void oracle_window_conv(const int64_t *shp, const double *win, const double *w, double *y) {
+void oracle_window_conv(const int64_t *shp, const double *win, const double *w, double *y,
+                        int trimmed) {
     const int64_t ho = oracle_out_extent(H_, FH_, SH_, PH_);
     const int64_t wo = oracle_out_extent(W_, FW_, SW_, PW_);
-    const int64_t row = (W_ + 2 * PW_) * FH_;
+    const int64_t row = oracle_row_width(shp, trimmed) * FH_;
 #pragma omp parallel for collapse(2) schedule(dynamic)
     for (int64_t i = 0; i < N_; ++i)
         for (int64_t j = 0; j < K_; ++j)

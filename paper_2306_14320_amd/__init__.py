@@ -22,6 +22,7 @@ import torch  # imported first: libim2win then binds to the HIP runtime torch ha
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libim2win.so")
 
 IM2WIN_F32, IM2WIN_BF16 = 0, 1
+IM2WIN_ROWS_PADDED, IM2WIN_ROWS_TRIMMED = 0, 1   # im2win_layout
 IM2WIN_OK = 0
 IM2WIN_EINVAL = -1
 IM2WIN_ENULL = -2
@@ -38,14 +39,14 @@ class im2win_desc(ctypes.Structure):
         ("k", ctypes.c_int64), ("fh", ctypes.c_int64), ("fw", ctypes.c_int64),
         ("stride_h", ctypes.c_int64), ("stride_w", ctypes.c_int64),
         ("pad_h", ctypes.c_int64), ("pad_w", ctypes.c_int64),
-        ("dtype", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
     ]
 
     def __repr__(self):
         return ("im2win_desc(n=%d, c=%d, h=%d, w=%d, k=%d, fh=%d, fw=%d, stride=(%d,%d), "
-                "pad=(%d,%d), dtype=%d)" % (self.n, self.c, self.h, self.w, self.k, self.fh,
-                                            self.fw, self.stride_h, self.stride_w, self.pad_h,
-                                            self.pad_w, self.dtype))
+                "pad=(%d,%d), dtype=%d, layout=%d)" % (self.n, self.c, self.h, self.w, self.k, self.fh,
+                                                       self.fw, self.stride_h, self.stride_w, self.pad_h,
+                                                       self.pad_w, self.dtype, self.layout))
 
 
 class Im2winError(RuntimeError):
@@ -157,8 +158,10 @@ def _pair(v):
     return (v, v) if isinstance(v, int) else tuple(v)
 
 
-def desc_for(x_shape, w_shape, stride=1, padding=0, dtype=torch.float32) -> im2win_desc:
-    """Descriptor for input N x C x H x W, filter K x C x Fh x Fw."""
+def desc_for(x_shape, w_shape, stride=1, padding=0, dtype=torch.float32,
+             layout=None) -> im2win_desc:
+    """Descriptor for input N x C x H x W, filter K x C x Fh x Fw (window-tensor
+    rows of the padded width unless layout=IM2WIN_ROWS_TRIMMED)."""
     n, c, h, w = x_shape
     k, c2, fh, fw = w_shape
     if c2 != c:
@@ -167,7 +170,8 @@ def desc_for(x_shape, w_shape, stride=1, padding=0, dtype=torch.float32) -> im2w
     ph, pw = _pair(padding)
     if dtype not in _DTYPES:
         raise ValueError(f"unsupported dtype {dtype} (float32 or bfloat16)")
-    return im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, _DTYPES[dtype])
+    return im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, _DTYPES[dtype],
+                       IM2WIN_ROWS_PADDED if layout is None else layout)
 
 
 def _stream(stream):
@@ -182,9 +186,17 @@ def _dev(t, name):
     return t.data_ptr()
 
 
+def row_width(desc: im2win_desc) -> int:
+    """Columns per window-tensor row: Wp, or (Wo-1)*stride_w + Fw when trimmed."""
+    _, wo = im2win_output_shape(desc)
+    if desc.layout == IM2WIN_ROWS_TRIMMED:
+        return (wo - 1) * desc.stride_w + desc.fw
+    return desc.w + 2 * desc.pad_w
+
+
 def workspace_shape(desc: im2win_desc):
     ho, _ = im2win_output_shape(desc)
-    return (desc.n, desc.c, ho, (desc.w + 2 * desc.pad_w) * desc.fh)
+    return (desc.n, desc.c, ho, row_width(desc) * desc.fh)
 
 
 def transform(x: torch.Tensor, desc: im2win_desc, ws: torch.Tensor = None, stream=None) -> torch.Tensor:

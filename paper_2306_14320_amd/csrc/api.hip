@@ -53,6 +53,8 @@ int geometry(const im2win_desc* d, im2win::Geometry* g) {
                     (long long)d->pad_w);
     if (d->dtype != IM2WIN_F32 && d->dtype != IM2WIN_BF16)
         return fail(IM2WIN_EINVAL, "unknown dtype %d", (int)d->dtype);
+    if (d->layout != IM2WIN_ROWS_PADDED && d->layout != IM2WIN_ROWS_TRIMMED)
+        return fail(IM2WIN_EINVAL, "unknown window-tensor layout %d", (int)d->layout);
     const int64_t lim = int64_t(1) << 30;
     if (d->n > kI31 || d->c > lim || d->h > lim || d->w > lim || d->k > lim || d->fh > lim ||
         d->fw > lim || d->stride_h > lim || d->stride_w > lim || d->pad_h > lim || d->pad_w > lim)
@@ -67,12 +69,14 @@ int geometry(const im2win_desc* d, im2win::Geometry* g) {
     g->ph = d->pad_h; g->pw = d->pad_w;
     g->ho = (hp - d->fh) / d->stride_h + 1;
     g->wo = (wp - d->fw) / d->stride_w + 1;
-    g->wp = wp;
+    // row width of the window tensor: every padded column, or only those
+    // some window reads ((Wo-1)*sw + Fw <= Wp)
+    g->wp = d->layout == IM2WIN_ROWS_TRIMMED ? (g->wo - 1) * d->stride_w + d->fw : wp;
     g->elem = d->dtype == IM2WIN_F32 ? 4 : 2;
 
     // Quantities the kernels hold in 32-bit integers, and element counts.
     int64_t t, t2;
-    if (!mul_le(wp, d->fh, kI31 / 2, &g->row_len) || !mul_le(g->ho, g->row_len, kI31, &t) ||
+    if (!mul_le(g->wp, d->fh, kI31 / 2, &g->row_len) || !mul_le(g->ho, g->row_len, kI31, &t) ||
         !mul_le(d->fh, d->fw, kI31, &g->taps) || !mul_le(d->h, d->w, kI31, &t) ||
         !mul_le(d->k * 1, d->c, kI31, &t) || !mul_le(t, g->taps, kI31, &t2) ||
         !mul_le(g->ho, g->wo, kI31, &t) || !mul_le(d->n, t, kI31, &g->npix))

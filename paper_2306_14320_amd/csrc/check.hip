@@ -51,7 +51,8 @@ void check_transform(const Geometry& g, Report& r) {
         if (next_out > ws_elems)
             r.fail("transform block %lld: writes up to %lld of %lld", (long long)b,
                    (long long)next_out, (long long)ws_elems);
-        if (a.g > 1 && (int64_t)blk.nrin * g.w != (int64_t)a.div_plane.d)
+        // (an empty footprint, rows of padding only, divides nothing)
+        if (a.g > 1 && blk.nrin > 0 && (int64_t)blk.nrin * g.w != (int64_t)a.div_plane.d)
             r.fail("transform block %lld: footprint per plane %lld, divisor %u", (long long)b,
                    (long long)blk.nrin * g.w, a.div_plane.d);
         // replay the scatter: every LDS write inside the run, each element of
@@ -73,6 +74,7 @@ void check_transform(const Geometry& g, Report& r) {
             int mf, ml;
             blk.rows_of(yy, a, &mf, &ml);
             for (int m = mf; m <= ml; ++m) {
+                if (xx + a.pw >= a.wp) break;   // past the row's end (trimmed rows): skipped
                 const int u = yy + a.ph - m * a.sh;
                 const int li = blk.lds_index(pj, m, xx + a.pw, u, a) - blk.shift;
                 if (u < 0 || u >= a.fh || li < 0 || li >= blk.olen) {
@@ -171,7 +173,7 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                 }
                 const int m_st = tr.seg_m(sg), q_st = tr.seg_q(sg), len = tr.seg_len(sg), off = tr.seg_off(sg);
                 const int m_end = sg == tr.nseg - 1 ? tr.m1 : (int)g.ho - 1;
-                for (int xx = 0; xx < g.w; ++xx)
+                for (int xx = 0; xx < g.w && xx + g.pw < g.wp; ++xx)   // (trimmed rows end early)
                     for (int m = m_st; m <= m_end; ++m) {
                         const int u = yy + (int)g.ph - m * (int)g.sh;
                         if (u < 0 || u >= g.fh) continue;
@@ -284,6 +286,7 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
                     const int u = yy + (int)g.ph - m * (int)g.sh;
                     if (u < 0 || u >= g.fh) continue;
                     for (int h = 0; h < 2; ++h) {
+                        if (xx + h + g.pw >= g.wp) continue;   // past a trimmed row's end
                         const int e_in = m * (int)g.row_len + (xx + h + (int)g.pw) * (int)g.fh + u;
                         const int rel = e_in - (m_st * (int)g.row_len + q_st);
                         if (rel >= 0 && rel < len) put(sg, e_in, cl_pos(cl, tr, a, sg, e_in));

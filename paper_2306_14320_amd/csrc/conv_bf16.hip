@@ -842,7 +842,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
                 for (int h = 0; h < 2; ++h) {
                     const int e_in = m * a.row_len + (xx + h + a.pw) * a.fh + u;
                     const int rel = e_in - (m_st * a.row_len + q_st);
-                    if (xx + h < a.w_in && (unsigned)rel < (unsigned)len)
+                    // (columns past a trimmed row's end are skipped)
+                    if (xx + h < a.w_in && (unsigned)rel < (unsigned)len && xx + h + a.pw < a.wp)
                         mp[j].dst[h][i] = (g * a.cl_pb + cl_pos(cl, tr, a, sg, e_in)) * 8;
                 }
             }

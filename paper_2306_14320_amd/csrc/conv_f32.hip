@@ -290,8 +290,11 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
 // (the on-chip form of the transformation's scatter).  Positions in the
 // padding are never written; they were zeroed once.  An odd last chunk under
 // the channel split gets one zero channel.
-__device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
-                                  const RawRows& rr, int rc_act, int rc_stage) {
+// TRIM: rows end before the input does (trimmed layout), so input columns
+// from wp - pw on are skipped.
+template <bool TRIM>
+__device__ inline void expand_raw_cols(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
+                                       const RawRows& rr, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int nseg = tr.nseg, len0 = tr.len0, len_mid = tr.len_mid, len_last = tr.len_last,
               m0 = tr.m0, m1 = tr.m1, qa0 = tr.qa0, d_second = tr.d_second, d_stride = tr.d_stride;
@@ -317,6 +320,8 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
             if (m_lo < sr.m) m_lo = sr.m;
             int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
             if (m_hi > m_end) m_hi = m_end;
+            // elements of the vector that land in a row
+            const int nv = TRIM ? min(vw, a.wp - a.pw - xx) : vw;
             float v[4];
             if (vw == 4) {
                 const float4 f = *reinterpret_cast<const float4*>(xl + e);
@@ -330,11 +335,17 @@ __device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, c
                 float* d = sl + sr.off + rel;
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (j < vw && (unsigned)(rel + j * a.fh) < (unsigned)sr.len) d[j * a.fh] = v[j];
+                    if (j < nv && (unsigned)(rel + j * a.fh) < (unsigned)sr.len) d[j * a.fh] = v[j];
             }
         }
     }
     if (rc_stage > rc_act) zero_channels(S, a, tr, rc_act, rc_stage);
+}
+
+__device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
+                                  const RawRows& rr, int rc_act, int rc_stage) {
+    if (a.wp - a.pw < a.w_in) expand_raw_cols<true>(S, X, a, tr, rr, rc_act, rc_stage);
+    else expand_raw_cols<false>(S, X, a, tr, rr, rc_act, rc_stage);
 }
 
 // Fused fp32, small tiles: the destinations of every raw element that a lane
@@ -383,7 +394,7 @@ __device__ inline void expand_map_build(ExpandMap<FH>& mp, const ConvArgs& a, co
                 const int m = m_lo + i;
                 const int u = yy + a.ph - m * a.sh;
                 const int rel = (m - sr.m) * a.row_len + (xx + a.pw) * a.fh + u - sr.q;
-                if (m <= m_hi && (unsigned)rel < (unsigned)sr.len) mp.dst[k][i] = sr.off + rel;
+                if (m <= m_hi && (unsigned)rel < (unsigned)sr.len && xx + a.pw < a.wp) mp.dst[k][i] = sr.off + rel;
             }
         }
     }

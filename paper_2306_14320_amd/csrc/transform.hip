@@ -31,7 +31,9 @@ struct alignas(V * sizeof(T)) Vec {
     T v[V];
 };
 
-template <typename T, int V>
+// TRIM: the rows are narrower than the input reaches (trimmed layout), so
+// input columns past the row's last window are skipped.
+template <typename T, int V, bool TRIM>
 __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     T* lds = reinterpret_cast<T*>(smem);
@@ -72,7 +74,8 @@ __global__ __launch_bounds__(kThreads) void transform_lds_kernel(XformArgs a) {
         for (int m = mf; m <= ml; ++m) {
             T* d = lds + blk.lds_index(pj, m, xx + a.pw, yy + a.ph - m * a.sh, a);
 #pragma unroll
-            for (int t = 0; t < VV; ++t) d[t * a.fh] = v[t];
+            for (int t = 0; t < VV; ++t)
+                if (!TRIM || xx + a.pw + t < a.wp) d[t * a.fh] = v[t];
         }
     };
     // footprint vectors of VV elements: plane starts, row y_lo and per_plane
@@ -159,9 +162,13 @@ __global__ __launch_bounds__(kThreads) void transform_direct_kernel(XformArgs a,
 }
 
 template <typename T, int V>
-void launch(const XformArgs& a, const XformPlan& p, int64_t nrows_total, hipStream_t stream) {
-    if (p.use_lds)
-        hipLaunchKernelGGL((transform_lds_kernel<T, V>), dim3((unsigned)p.blocks), dim3(kThreads),
+void launch(const XformArgs& a, const XformPlan& p, int64_t nrows_total, bool trim,
+            hipStream_t stream) {
+    if (p.use_lds && trim)
+        hipLaunchKernelGGL((transform_lds_kernel<T, V, true>), dim3((unsigned)p.blocks), dim3(kThreads),
+                           (size_t)p.lds_bytes, stream, a);
+    else if (p.use_lds)
+        hipLaunchKernelGGL((transform_lds_kernel<T, V, false>), dim3((unsigned)p.blocks), dim3(kThreads),
                            (size_t)p.lds_bytes, stream, a);
     else
         hipLaunchKernelGGL((transform_direct_kernel<T>), dim3((unsigned)p.blocks), dim3(kThreads),
@@ -249,8 +256,9 @@ int launch_transform(const Geometry& g, const void* x, void* ws, hipStream_t str
         return -5;
     }
     const XformArgs a = transform_args(g, p, x, ws);
-    if (g.elem == 4) launch<uint32_t, 4>(a, p, g.n * g.c * g.ho, stream);
-    else launch<uint16_t, 8>(a, p, g.n * g.c * g.ho, stream);
+    const bool trim = g.w + g.pw > g.wp;   // some input columns lie past a row's end
+    if (g.elem == 4) launch<uint32_t, 4>(a, p, g.n * g.c * g.ho, trim, stream);
+    else launch<uint16_t, 8>(a, p, g.n * g.c * g.ho, trim, stream);
     return 0;
 }
 

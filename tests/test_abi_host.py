@@ -122,10 +122,31 @@ def test_oversized_problem_rejected():
     assert _code(P.im2win_direct_conv2d, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
 
 
+@pytest.mark.parametrize("layout", [P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED], ids=["padded", "trimmed"])
 @pytest.mark.parametrize("wl", workloads.WORKLOADS, ids=lambda wl: wl.name)
-def test_launch_plans_in_bounds_on_workloads(wl):
+def test_launch_plans_in_bounds_on_workloads(wl, layout):
     d = _desc(_wl_shape(wl), _wl_dtype(wl))
+    d.layout = layout
     assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+
+
+@pytest.mark.parametrize("s", SHAPES, ids=str)
+@pytest.mark.parametrize("dtype", [P.IM2WIN_F32, P.IM2WIN_BF16])
+def test_trimmed_sizes_agree_with_oracle(s, dtype):
+    d = _desc(s, dtype)
+    d.layout = P.IM2WIN_ROWS_TRIMMED
+    e = 4 if dtype == P.IM2WIN_F32 else 2
+    assert P.im2win_workspace_bytes(d) == oracle.im2win_elems(s, trimmed=True) * e
+    assert P.workspace_shape(d) == s.win_shape_of(True)
+    assert P.im2win_output_shape(d) == (s.ho, s.wo)
+
+
+def test_unknown_layout_rejected():
+    d = _desc(GOOD)
+    d.layout = 2
+    assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert "layout" in P.im2win_last_error()
 
 
 def test_launch_plans_in_bounds_on_random_shapes():
@@ -138,7 +159,7 @@ def test_launch_plans_in_bounds_on_random_shapes():
         if h + 2 * ph < fh or w + 2 * pw < fw:
             continue
         for dt in (P.IM2WIN_F32, P.IM2WIN_BF16):
-            d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, dt)
+            d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, dt, checked % 2)
             assert P.im2win_check_plan(d) == 0, (d, P.im2win_last_error())
             checked += 1
 
@@ -154,5 +175,6 @@ def test_launch_plans_in_bounds_on_paper_layers():
         co, hf, wf = layer["filter"]
         st = layer["stride"]
         for dt in (P.IM2WIN_F32, P.IM2WIN_BF16):
-            d = P.im2win_desc(2, ci, hi, wi, co, hf, wf, st, st, 0, 0, dt)
-            assert P.im2win_check_plan(d) == 0, (layer["name"], P.im2win_last_error())
+            for layout in (P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED):
+                d = P.im2win_desc(2, ci, hi, wi, co, hf, wf, st, st, 0, 0, dt, layout)
+                assert P.im2win_check_plan(d) == 0, (layer["name"], P.im2win_last_error())

@@ -217,6 +217,76 @@ def test_window_conv_of_im2win_equals_direct_conv(s):
                                rtol=0, atol=1e-12)
 
 
+# --------------------------------------------------------------------------
+# Trimmed rows: only the columns some window reads, (Wo-1)*sw + Fw of them
+# --------------------------------------------------------------------------
+
+# shapes whose padded rows hold columns no window reaches (the trimmed rows are
+# shorter), beside ones where both widths agree
+TRIM_SHAPES = SMALL_SHAPES + [
+    Shape(2, 3, 12, 10, 2, 3, 2, 1, 3, 1, 1),         # Wo=4: Wt = 11 of Wp = 12
+    Shape(1, 2, 9, 28, 3, 3, 5, 2, 2, 1, 2),          # rect-like: 31 of 32
+    Shape(1, 2, 9, 17, 2, 2, 2, 1, 4, 0, 0),          # Fw < sw: 14 of 17
+]
+
+
+@pytest.mark.parametrize("s", TRIM_SHAPES, ids=_ids(TRIM_SHAPES))
+def test_trimmed_width_is_the_last_window_end(s):
+    """The trimmed row ends where the last window ends: the last output
+    column's window covers padded columns [(Wo-1)*sw, (Wo-1)*sw + Fw), and the
+    padded input has W + 2*pw >= that many columns (floor in Wo)."""
+    last = max(n * s.sw + v for n in range(s.wo) for v in range(s.fw)) + 1
+    assert s.wt == last <= s.wp
+    assert oracle.im2win_elems(s, trimmed=True) == s.n * s.c * s.ho * last * s.fh
+
+
+@pytest.mark.parametrize("s", TRIM_SHAPES, ids=_ids(TRIM_SHAPES))
+def test_trimmed_windows_match_unfold(s):
+    """Every window of the trimmed tensor equals the im2col column that torch's
+    unfold builds, and every element of a trimmed row is the zero-padded input
+    (no column is dropped that a window reads, none is added)."""
+    x = _rand((s.n, s.c, s.h, s.w)).astype(np.float32)
+    win = oracle.im2win(s, x, trimmed=True)
+    assert win.shape == (s.n, s.c, s.ho, s.wt * s.fh)
+    cols = F.unfold(torch.from_numpy(x), (s.fh, s.fw), stride=(s.sh, s.sw),
+                    padding=(s.ph, s.pw)).numpy().reshape(s.n, s.c, s.fh, s.fw, s.ho, s.wo)
+    for m in range(s.ho):
+        for n in range(s.wo):
+            for u in range(s.fh):
+                for v in range(s.fw):
+                    np.testing.assert_array_equal(win[:, :, m, (n * s.sw + v) * s.fh + u], cols[:, :, u, v, m, n])
+    xp = F.pad(torch.from_numpy(x), (s.pw, s.pw, s.ph, s.ph)).numpy()
+    for m in range(s.ho):
+        strip = xp[:, :, m * s.sh:m * s.sh + s.fh, :s.wt]          # N x C x Fh x Wt
+        np.testing.assert_array_equal(win[:, :, m, :], strip.transpose(0, 1, 3, 2).reshape(s.n, s.c, -1))
+
+
+@pytest.mark.parametrize("s", TRIM_SHAPES, ids=_ids(TRIM_SHAPES))
+def test_trimmed_window_conv_equals_conv2d(s):
+    """Alg. 2 over the trimmed tensor gives torch's fp64 conv2d."""
+    x, w = _rand((s.n, s.c, s.h, s.w)), _rand((s.k, s.c, s.fh, s.fw))
+    win = oracle.im2win(s, x, trimmed=True)
+    ref = F.conv2d(torch.from_numpy(x), torch.from_numpy(w), stride=(s.sh, s.sw), padding=(s.ph, s.pw)).numpy()
+    np.testing.assert_allclose(oracle.window_conv(s, win, w, trimmed=True), ref, rtol=0, atol=1e-12)
+
+
+def test_trimmed_size_never_exceeds_im2col_when_fw_at_least_sw():
+    """im2col - trimmed = N*C*Fh*Ho*(Wo-1)*(Fw - sw): no larger than im2col
+    whenever Fw >= sw (equal when Wo = 1 or Fw = sw), larger only when Fw < sw."""
+    rng = np.random.default_rng(77)
+    for _ in range(2000):
+        fh, fw, sh, sw = (int(v) for v in rng.integers(1, 8, size=4))
+        ph, pw = (int(v) for v in rng.integers(0, 4, size=2))
+        h = int(rng.integers(max(1, fh - 2 * ph), 40))
+        w = int(rng.integers(max(1, fw - 2 * pw), 60))
+        s = Shape(int(rng.integers(1, 4)), int(rng.integers(1, 9)), h, w, 1, fh, fw, sh, sw, ph, pw)
+        diff = oracle.im2col_elems(s) - oracle.im2win_elems(s, trimmed=True)
+        assert diff == s.n * s.c * s.fh * s.ho * (s.wo - 1) * (s.fw - s.sw)
+        if fw >= sw:
+            assert diff >= 0
+        assert oracle.im2win_elems(s, trimmed=True) <= oracle.im2win_elems(s)
+
+
 def _literal_alg2(s, win, w):
     """Alg. 2 with the window offset exactly as printed, n*s*Wf + v*Hf + u."""
     y = np.zeros(s.out_shape)
