@@ -147,7 +147,7 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                     r.fail("%s tile %lld: 16-byte run %d misplaced (shift %d)", what, (long long)t, s, shift);
             }
         }
-        if (a.ilv && (tr.ck_total > 64 * kIlvSlots || 4 * (int64_t)tr.ck_total > p.sc))
+        if (!fused && a.ilv && (tr.ck_total > 64 * kIlvSlots || 4 * (int64_t)tr.ck_total > p.sc))
             r.fail("conv tile %lld: %d 16-byte strip copies, in-loop issue covers %d (slot %lld)", (long long)t,
                    tr.ck_total, 64 * kIlvSlots, (long long)p.sc);
         if (fused && !bf16 && g.elem == 4) {
@@ -158,6 +158,17 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
             if ((int64_t)rw.rtot * g.w > a.raw_pitch || (a.raw_pitch & 3) || (a.raw_off & 3))
                 r.fail("fused conv tile %lld: %d raw rows of %lld, LDS pitch %d", (long long)t, rw.rtot,
                        (long long)g.w, a.raw_pitch);
+            // copies from per-lane offsets computed once: every copy unit of
+            // a channel has a slot, and the byte offsets of the units (from
+            // the channel's plane in the tile's first image) stay below 2^32
+            if (a.ilv) {
+                const int units = a.xvec ? rw.rtot * (int)g.w / 4 : rw.rtot * (int)g.w;
+                const int64_t span = (int64_t)tr.nseg * g.c * g.h * g.w;
+                if (units > 64 * kF32ExpandGroups || 4 * span >= (int64_t(1) << 32) || g.c % p.rc != 0 ||
+                    !p.fvec || p.bm * (p.fp / 4) > (int64_t)kConvThreads * kIlvSlots)
+                    r.fail("fused conv tile %lld: %d raw copy units (slots %d), offsets up to %lld bytes",
+                           (long long)t, units, 64 * kF32ExpandGroups, (long long)(4 * span));
+            }
             std::vector<uint8_t> hit(tr.extent > 0 ? tr.extent : 1, 0);
             for (int rr = 0; rr < rw.rtot && r.violations < 16; ++rr) {
                 int yy, sg;

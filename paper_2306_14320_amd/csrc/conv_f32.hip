@@ -584,6 +584,21 @@ struct IlvCopies {
             f_off[i] = c < f_total && col < creal ? (uint32_t)(4 * (jj * a.c * a.taps + 4 * col)) : kIlvNone;
         }
     }
+    // the filter part of init() alone (the fused kernel stages no strips)
+    __device__ void init_filter(const ConvArgs& a, int j0) {
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        f_base = static_cast<const char*>(a.w) + 4 * (int64_t)j0 * a.c * a.taps;
+        const int cpr = a.fp >> 2, creal = (a.rc * a.taps) >> 2;
+        f_total = min(a.k - j0, a.bm) * cpr;
+#pragma unroll
+        for (int i = 0; i < kIlvSlots; ++i) {
+            const int c = wave * 64 + kConvThreads * i + lane;
+            const int jj = (int)fast_div((uint32_t)c, a.div_fp);
+            const int col = c - jj * cpr;
+            f_off[i] = c < f_total && col < creal ? (uint32_t)(4 * (jj * a.c * a.taps + 4 * col)) : kIlvNone;
+        }
+    }
     // filter rows of the whole chunk starting at channel r0 into F
     __device__ void filter(float* F, const ConvArgs& a, int r0) const {
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -612,10 +627,60 @@ struct IlvCopies {
     }
 };
 
+// MODE 4 raw-row copies: the byte offsets of this lane's copy units of one
+// channel's raw rows from that channel's plane in the tile's first image
+// (the same for every channel), computed once per kernel.  stage_raw<false>
+// issues the same copies with the offsets worked out per chunk.
+struct RawCopies {
+    uint32_t off[kExpandK];
+    int units = 0;
+    __device__ void init(const ConvArgs& a, const TileRuns& tr, const RawRows& rr) {
+        const int lane = threadIdx.x & 63;
+        const int64_t plane = (int64_t)a.h * a.w_in;
+        raw_blocks(a, rr, &units);
+#pragma unroll
+        for (int k = 0; k < kExpandK; ++k) {
+            const int c = 64 * k + lane;
+            const int e = a.xvec ? 4 * c : c;
+            const int r = (int)fast_div((uint32_t)e, a.div_w);
+            int yy;
+            const int sg = raw_segment(r, rr, tr.nseg, a, &yy);
+            const int64_t o = (int64_t)sg * a.c * plane + (int64_t)yy * a.w_in + (e - r * a.w_in);
+            off[k] = c < units ? (uint32_t)(4 * o) : kIlvNone;
+        }
+    }
+    // channels r0 + wave, r0 + wave + 4, ... of the chunk into X
+    __device__ void copy(float* X, const ConvArgs& a, int i0, int r0, int rc_act) const {
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int64_t plane = (int64_t)a.h * a.w_in;
+        for (int rc = wave; rc < rc_act; rc += 4) {
+            const char* b = reinterpret_cast<const char*>(static_cast<const float*>(a.src) +
+                                                          ((int64_t)i0 * a.c + r0 + rc) * plane);
+            float* l = X + rc * a.raw_pitch;
+#pragma unroll
+            for (int k = 0; k < kExpandK; ++k) {
+                uint32_t o = off[k];
+                asm volatile("" : "+v"(o));   // widened here, not held widened across the loop
+                if (64 * k < units && o != kIlvNone) {
+                    if (a.xvec)
+                        __builtin_amdgcn_global_load_lds(reinterpret_cast<const float*>(b + o),
+                                                         (lds_void*)(l + 4 * 64 * k), 16, 0, 0);
+                    else
+                        __builtin_amdgcn_global_load_lds(reinterpret_cast<const float*>(b + o),
+                                                         (lds_void*)(l + 64 * k), 4, 0, 0);
+                }
+            }
+        }
+    }
+};
+
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, int MODE>
 __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
-    constexpr bool FUSED = MODE == 1 || MODE == 2;
+    constexpr bool FUSED = MODE == 1 || MODE == 2 || MODE == 4;
     constexpr bool ILV = MODE == 3;
+    // MODE 4: MODE 2 with the filter-row and raw-row copies from per-lane
+    // offsets computed once
+    constexpr bool FASTCP = MODE == 4;
     static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
@@ -680,7 +745,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     RawRows rr{};
     // the map holds FH destinations per element: kept for filters of up to
     // three rows (larger ones expand with the per-element decode)
-    constexpr bool use_map = RAW && MODE == 2;
+    constexpr bool use_map = RAW && (MODE == 2 || MODE == 4);
     static_assert(!use_map || (FH > 0 && FH <= 3), "expansion map for filters of up to 3 rows");
     constexpr int FHM = use_map ? FH : 1;
     ExpandMap<FHM> emap;
@@ -713,6 +778,9 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     }
     IlvCopies ilv;
     if constexpr (ILV) ilv.init(a, tr, j0);
+    if constexpr (FASTCP) ilv.init_filter(a, j0);
+    RawCopies rcp;
+    if constexpr (FASTCP) rcp.init(a, tr, rr);
 
     for (int ch = 0; ch < nchunks; ++ch) {
         const int r0 = ch * a.rc;
@@ -728,7 +796,12 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         // plans have whole chunks only, so no chunk is staged here)
         const bool ilv_next = ILV && ch + 1 < nchunks;
         if (!ILV && ch + 1 < nchunks) {
-            if constexpr (RAW) {
+            if constexpr (FASTCP) {
+                // whole chunks only (the plan asks C % rc == 0)
+                ilv.filter(F + off, a, r1);
+                if (ch + 2 < nchunks) rcp.copy(Xb(ch), a, tr.i0, r1 + a.rc, a.rc);
+                expand_map_apply<FHM>(S + off, Xb(ch + 1), emap, a, tr, rc1, rc_stage1);
+            } else if constexpr (RAW) {
                 stage<TIn, FUSED, true>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
                 if (use_map) {
                     // copies of chunk c+2; expansion of chunk c+1, whose copies the barrier published
@@ -801,7 +874,9 @@ void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipS
     if (!fused && a.svec && a.fvec && a.ilv) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, kIlvMode>;
     if (fused) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 1>;
     if constexpr (sizeof(TIn) == 4 && FH > 0 && FH <= 3)
-        if (fused && a.raw_pitch <= kExpandMaxRaw) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
+        if (fused && a.raw_pitch <= kExpandMaxRaw)
+            kern = a.ilv ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 4>
+                         : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
     if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch) * 4;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -968,6 +1043,12 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     a.ilv = (!fused && p.svec && p.fvec && p.split == 0 && g.c % p.rc == 0 && p.sc / 4 <= 64 * kIlvSlots &&
              (int64_t)p.bm * (p.fp / 4) <= (int64_t)kConvThreads * kIlvSlots &&
              segs * g.c * plane < (1ll << 30) && (int64_t)p.bm * g.c * g.fh * g.fw < (1ll << 30)) ? 1 : 0;
+    // fused fp32 with the expansion map (MODE 4): filter-row and raw-row
+    // copies from offsets computed once per lane (byte offsets below 2^32:
+    // the input planes of the tile's images, the filter rows of the tile)
+    if (fused && g.elem == 4 && g.fh <= 3 && p.raw_pitch <= kExpandMaxRaw)
+        a.ilv = (p.fvec && g.c % p.rc == 0 && (int64_t)p.bm * (p.fp / 4) <= (int64_t)kConvThreads * kIlvSlots &&
+                 segs * g.c * g.h * g.w < (1ll << 30) && g.k * g.c * g.fh * g.fw < (1ll << 30)) ? 1 : 0;
     return a;
 }
 
