@@ -758,6 +758,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     // wait for every copy in flight)
     const int xstride = a.rc * a.raw_pitch + kExpandMaxRaw;
     auto Xb = [&](int k) { return X + (k & 1) * xstride; };
+    IlvCopies ilv;
+    RawCopies rcp;
     {
         const int rc_act = min(a.rc, a.c);
         const int rc_stage = ROWS ? rc_act : a.rc;
@@ -765,9 +767,18 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             rr = raw_rows(tr, a);
             for (int sg = 0; sg < 2; ++sg)
                 for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
-            stage_raw<!use_map>(X, a, tr, rr, 0, rc_act);
-            if (use_map && nchunks > 1) stage_raw<false>(Xb(1), a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
-            stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
+            if constexpr (FASTCP) {
+                // whole chunks only: rc_act = rc_stage = rc
+                ilv.init_filter(a, j0);
+                rcp.init(a, tr, rr);
+                rcp.copy(X, a, tr.i0, 0, a.rc);
+                if (nchunks > 1) rcp.copy(Xb(1), a, tr.i0, a.rc, a.rc);
+                ilv.filter(F, a, 0);
+            } else {
+                stage_raw<!use_map>(X, a, tr, rr, 0, rc_act);
+                if (use_map && nchunks > 1) stage_raw<false>(Xb(1), a, tr, rr, a.rc, min(a.rc, a.c - a.rc));
+                stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
+            }
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
             dma_barrier();   // zeros written, raw rows of chunk 0 (and 1) landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
@@ -776,11 +787,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, rc_stage);
         }
     }
-    IlvCopies ilv;
     if constexpr (ILV) ilv.init(a, tr, j0);
-    if constexpr (FASTCP) ilv.init_filter(a, j0);
-    RawCopies rcp;
-    if constexpr (FASTCP) rcp.init(a, tr, rr);
 
     for (int ch = 0; ch < nchunks; ++ch) {
         const int r0 = ch * a.rc;
