@@ -192,6 +192,29 @@ void check_conv_variant(const Geometry& g, const ConvPlan& p, bool fused, Report
                         if (rel >= 0 && rel < len) ++hit[off + rel];
                     }
             }
+            // without the expansion map the kernel places raw elements through
+            // per-row entries (raw_row_entry): they must write exactly the
+            // positions of the model above, inside the strips, and fit the
+            // LDS the plan reserves for them
+            const bool map = g.fh <= 3 && a.raw_pitch <= 64 * kF32ExpandGroups;
+            if (!map) {
+                if (rw.rtot > a.raw_pitch / (int)g.w)
+                    r.fail("fused conv tile %lld: %d raw-row entries, LDS holds %lld", (long long)t, rw.rtot,
+                           (long long)(a.raw_pitch / g.w));
+                std::vector<uint8_t> hit2(hit.size(), 0);
+                for (int rr = 0; rr < rw.rtot && r.violations < 16; ++rr) {
+                    const RawRowEntry en = raw_row_entry(a, tr, rw, rr);
+                    if (en.lo < 0 || en.hi > tr.extent || en.lo > en.hi)
+                        r.fail("fused conv tile %lld: raw row %d run [%d, %d) outside the strips", (long long)t, rr,
+                               en.lo, en.hi);
+                    for (int xx = 0; xx < g.w && xx + g.pw < g.wp; ++xx)
+                        for (int i = 0; i < en.cnt; ++i) {
+                            const int d = en.base + (xx + (int)g.pw) * (int)g.fh + i * ((int)g.row_len - (int)g.sh);
+                            if (d >= en.lo && d < en.hi) ++hit2[d];
+                        }
+                }
+                if (hit2 != hit) r.fail("fused conv tile %lld: raw-row entries place elements elsewhere", (long long)t);
+            }
             for (int sg = 0; sg < tr.nseg && r.violations < 16; ++sg) {
                 const int m_st = tr.seg_m(sg), q_st = tr.seg_q(sg), len = tr.seg_len(sg), off = tr.seg_off(sg);
                 for (int e = 0; e < len; ++e) {
@@ -449,7 +472,8 @@ void check_conv(const Geometry& g, bool fused_plan, Report& r) {
                    kConvThreads * kIlvSlots);
         // raw rows: two buffers with 768 floats of slack each when the map is used
         const int64_t mx = 64 * kF32ExpandGroups;
-        const int64_t rawf = (g.fh <= 3 && p.raw_pitch <= mx) ? 2 * (p.rc * p.raw_pitch + mx) : p.rc * p.raw_pitch;
+        const int64_t rawf = (g.fh <= 3 && p.raw_pitch <= mx) ? 2 * (p.rc * p.raw_pitch + mx)
+                                                              : p.rc * p.raw_pitch + 4 * (p.raw_pitch / g.w);
         if (g.elem == 4 && p.lds_bytes + 4 * rawf > kConvLdsMaxBytes)
             r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * rawf));
         if (g.elem == 4 && g.fh <= 3 && p.sc < p.strip_cap + g.fh + 64)

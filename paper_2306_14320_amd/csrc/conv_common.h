@@ -352,6 +352,43 @@ inline int64_t strip_capacity(const Geometry& g, int bn, int vc) {
     return cap + (vc - 1) * (1 + nseg);
 }
 
+// Fused fp32 with the per-element expansion (filters of more than three
+// rows, or long raw rows): where raw row r of a tile goes in the strips.
+// Element xx of the row lands at base + (xx + pw)*fh + i*(row_len - sh) for
+// i < cnt (window rows m_lo + i, filter row yy + ph - m*sh), each position
+// kept only inside [lo, hi), the run of the row's segment.  The kernel
+// computes the entries once per tile; the plan checker replays them.
+struct RawRowEntry {
+    int base, cnt, lo, hi;
+};
+
+__host__ __device__ inline RawRowEntry raw_row_entry(const ConvArgs& a, const TileRuns& tr,
+                                                     const RawRows& rr, int r) {
+    int sg, yy;
+    if (r < rr.r0) {
+        sg = 0;
+        yy = rr.ylo0 + r;
+    } else {
+        sg = 1 + (int)fast_div((uint32_t)(r - rr.r0), a.div_rmid);
+        if (sg > tr.nseg - 1) sg = tr.nseg - 1;
+        yy = a.ylo_mid + (r - rr.r0 - (sg - 1) * a.rmid);
+    }
+    const SegRun sr = seg_run(sg, tr.nseg, tr.len0, tr.len_mid, tr.len_last, tr.m0, tr.qa0, 0,
+                              tr.d_second, tr.d_stride);
+    const int m_end = sg == tr.nseg - 1 ? tr.m1 : a.ho - 1;
+    const int t = yy + a.ph - a.fh + 1;   // m*sh >= t
+    int m_lo = t <= 0 ? 0 : (int)fast_div((uint32_t)(t + a.sh - 1), a.div_sh);
+    if (m_lo < sr.m) m_lo = sr.m;
+    int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
+    if (m_hi > m_end) m_hi = m_end;
+    RawRowEntry e;
+    e.base = sr.off + (m_lo - sr.m) * a.row_len + (yy + a.ph - m_lo * a.sh) - sr.q;
+    e.cnt = m_hi - m_lo + 1;
+    e.lo = sr.off;
+    e.hi = sr.off + sr.len;
+    return e;
+}
+
 // Upper bound of RawRows::rtot over all tiles of `bn` pixels: the window
 // rows a tile spans, each segment adding the filter height.
 // Upper bound of RawRows::rtot over all tiles of `bn` pixels.  A segment of

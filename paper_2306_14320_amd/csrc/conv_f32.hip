@@ -291,14 +291,14 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
 // padding are never written; they were zeroed once.  An odd last chunk under
 // the channel split gets one zero channel.
 // TRIM: rows end before the input does (trimmed layout), so input columns
-// from wp - pw on are skipped.
+// from wp - pw on are skipped.  RT holds the tile's raw-row entries
+// (raw_row_entry), written once per kernel.
 template <bool TRIM>
-__device__ inline void expand_raw_cols(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
-                                       const RawRows& rr, int rc_act, int rc_stage) {
+__device__ inline void expand_raw_cols(float* S, const float* X, const int4* RT, const ConvArgs& a,
+                                       const TileRuns& tr, const RawRows& rr, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nseg = tr.nseg, len0 = tr.len0, len_mid = tr.len_mid, len_last = tr.len_last,
-              m0 = tr.m0, m1 = tr.m1, qa0 = tr.qa0, d_second = tr.d_second, d_stride = tr.d_stride;
     const int vw = a.xvec ? 4 : 1;
+    const int dstep = a.row_len - a.sh;   // next window row: one row on, sh filter rows up
     int n;
     const int nb = raw_blocks(a, rr, &n);
     for (int rc = 0; rc < rc_act; ++rc) {
@@ -311,15 +311,7 @@ __device__ inline void expand_raw_cols(float* S, const float* X, const ConvArgs&
             const int e = q * vw;
             const int r = (int)fast_div((uint32_t)e, a.div_w);
             const int xx = e - r * a.w_in;
-            int yy;
-            const int sg = raw_segment(r, rr, nseg, a, &yy);
-            const SegRun sr = seg_run(sg, nseg, len0, len_mid, len_last, m0, qa0, 0, d_second, d_stride);
-            const int m_end = sg == nseg - 1 ? m1 : a.ho - 1;
-            const int t = yy + a.ph - a.fh + 1;   // m*sh >= t
-            int m_lo = t <= 0 ? 0 : (int)fast_div((uint32_t)(t + a.sh - 1), a.div_sh);
-            if (m_lo < sr.m) m_lo = sr.m;
-            int m_hi = (int)fast_div((uint32_t)(yy + a.ph), a.div_sh);
-            if (m_hi > m_end) m_hi = m_end;
+            const int4 en = RT[r];   // base, cnt, lo, hi
             // elements of the vector that land in a row
             const int nv = TRIM ? min(vw, a.wp - a.pw - xx) : vw;
             float v[4];
@@ -329,23 +321,22 @@ __device__ inline void expand_raw_cols(float* S, const float* X, const ConvArgs&
             } else {
                 v[0] = xl[e];
             }
-            for (int m = m_lo; m <= m_hi; ++m) {
-                const int u = yy + a.ph - m * a.sh;
-                const int rel = (m - sr.m) * a.row_len + (xx + a.pw) * a.fh + u - sr.q;
-                float* d = sl + sr.off + rel;
+            int d = en.x + (xx + a.pw) * a.fh;
+            const unsigned span = (unsigned)(en.w - en.z);
+            for (int i = 0; i < en.y; ++i, d += dstep) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (j < nv && (unsigned)(rel + j * a.fh) < (unsigned)sr.len) d[j * a.fh] = v[j];
+                    if (j < nv && (unsigned)(d + j * a.fh - en.z) < span) sl[d + j * a.fh] = v[j];
             }
         }
     }
     if (rc_stage > rc_act) zero_channels(S, a, tr, rc_act, rc_stage);
 }
 
-__device__ inline void expand_raw(float* S, const float* X, const ConvArgs& a, const TileRuns& tr,
-                                  const RawRows& rr, int rc_act, int rc_stage) {
-    if (a.wp - a.pw < a.w_in) expand_raw_cols<true>(S, X, a, tr, rr, rc_act, rc_stage);
-    else expand_raw_cols<false>(S, X, a, tr, rr, rc_act, rc_stage);
+__device__ inline void expand_raw(float* S, const float* X, const int4* RT, const ConvArgs& a,
+                                  const TileRuns& tr, const RawRows& rr, int rc_act, int rc_stage) {
+    if (a.wp - a.pw < a.w_in) expand_raw_cols<true>(S, X, RT, a, tr, rr, rc_act, rc_stage);
+    else expand_raw_cols<false>(S, X, RT, a, tr, rr, rc_act, rc_stage);
 }
 
 // Fused fp32, small tiles: the destinations of every raw element that a lane
@@ -756,6 +747,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     // (selected by arithmetic on the LDS base: a pointer picked from an array
     // loses its address space, and reads through it become flat loads that
     // wait for every copy in flight)
+    // without the map: the raw-row entries of the tile after the raw rows
+    int4* RT = reinterpret_cast<int4*>(X + a.rc * a.raw_pitch);
     const int xstride = a.rc * a.raw_pitch + kExpandMaxRaw;
     auto Xb = [&](int k) { return X + (k & 1) * xstride; };
     IlvCopies ilv;
@@ -780,9 +773,14 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
                 stage<TIn, FUSED, true>(S, F, a, tr, j0, 0, rc_act, rc_stage);
             }
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
-            dma_barrier();   // zeros written, raw rows of chunk 0 (and 1) landed
+            else
+                for (int r = threadIdx.x; r < rr.rtot; r += kConvThreads) {
+                    const RawRowEntry en = raw_row_entry(a, tr, rr, r);
+                    RT[r] = make_int4(en.base, en.cnt, en.lo, en.hi);
+                }
+            dma_barrier();   // zeros and row entries written, raw rows of chunk 0 (and 1) landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
-            else expand_raw(S, X, a, tr, rr, rc_act, rc_stage);
+            else expand_raw(S, X, RT, a, tr, rr, rc_act, rc_stage);
         } else {
             stage<TIn, FUSED>(S, F, a, tr, j0, 0, rc_act, rc_stage);
         }
@@ -847,7 +845,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             if (!use_map && ch + 1 < nchunks) {
                 __builtin_amdgcn_sched_barrier(0);
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-                expand_raw(S + off, X, a, tr, rr, rc1, rc_stage1);
+                expand_raw(S + off, X, RT, a, tr, rr, rc1, rc_stage1);
             }
         }
     }
@@ -868,10 +866,12 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
 
 // LDS floats of the raw rows of the fused fp32 kernel: with the expansion
 // map (filters of up to 3 rows, raw rows of up to kExpandMaxRaw floats) two
-// buffers, each with kExpandMaxRaw floats of slack for the map's reads.
-int64_t raw_floats(int fh, int rc, int64_t raw_pitch) {
+// buffers, each with kExpandMaxRaw floats of slack for the map's reads;
+// without it one buffer and the tile's raw-row entries (4 ints per row, at
+// most raw_pitch / W rows).
+int64_t raw_floats(int fh, int rc, int64_t raw_pitch, int64_t w) {
     if (fh <= 3 && raw_pitch <= kExpandMaxRaw) return 2 * (rc * raw_pitch + kExpandMaxRaw);
-    return rc * raw_pitch;
+    return rc * raw_pitch + 4 * (raw_pitch / w);
 }
 
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP>
@@ -884,7 +884,7 @@ void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipS
         if (fused && a.raw_pitch <= kExpandMaxRaw)
             kern = a.ilv ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 4>
                          : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
-    if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch) * 4;
+    if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch, a.w_in) * 4;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
@@ -1002,7 +1002,7 @@ ConvPlan plan_conv_f32(const Geometry& g) {
                 const bool fv = filter_vec(g, rc);
                 const int64_t lds = f32_layout(g, t.bm, rc, cap, fv, split, &sc, &fp, &st);
                 const int64_t raw = g.elem == 4 ? raw_pitch_f32(g, t.bn) : 0;
-                if (lds + (raw ? raw_floats((int)g.fh, rc, raw) : 0) * 4 > budget) continue;
+                if (lds + (raw ? raw_floats((int)g.fh, rc, raw, g.w) : 0) * 4 > budget) continue;
                 ConvPlan q;
                 q.kind = ConvPlan::kF32Lds;
                 q.bm = t.bm; q.bn = t.bn; q.rc = rc; q.tc = (int)g.taps; q.split = split;
