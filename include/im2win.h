@@ -23,10 +23,13 @@
  *    dilation, no groups).
  *  - Device pointers (x, w, ws, y) are owned by the caller.  Each must be
  *    16-byte aligned and the buffers must not overlap.  The only device
- *    memory the library holds itself: bf16 convolutions that run on its fast
- *    kernels (C a multiple of 16, K a multiple of 64, filter 3x3, 3x5 or 1x1,
- *    among other shape conditions) first rewrite w into the order those
- *    kernels copy to on-chip memory, in a buffer of K*C*Fh*Fw*2 bytes that
+ *    memory the library holds itself: some convolutions first rewrite w into
+ *    the order their kernels copy to on-chip memory -- bf16 ones that run on
+ *    the fast kernels (C a multiple of 16, K a multiple of 64, filter 3x3, 3x5
+ *    or 1x1, among other shape conditions; K*C*Fh*Fw*2 bytes), and fp32 ones
+ *    whose per-chunk filter rows are not whole 16-byte vectors (C*Fh*Fw
+ *    floats per output channel rounded up to the kernel's tile and row
+ *    stride, about K*C*Fh*Fw*4 bytes) -- in a buffer that
  *    the library keeps per stream (the default stream once per device),
  *    taken from the device's stream-ordered memory pool (hipMallocAsync on
  *    that stream) and replaced, stream-ordered, only when a larger filter

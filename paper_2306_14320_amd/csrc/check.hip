@@ -466,6 +466,19 @@ void check_conv(const Geometry& g, bool fused_plan, Report& r) {
             r.fail("conv: channel split with an odd chunk of %d", p.rc);
         if (p.fvec && (((g.c * g.taps) & 3) || ((p.rc * g.taps) & 3) || (p.fp & 3)))
             r.fail("conv: 16-byte filter rows with misaligned rows (fp %lld)", (long long)p.fp);
+        // repacked filter (rows not whole vectors): blocks of bm*fp floats,
+        // copied in 16-byte units to the 16-byte aligned LDS filter rows of a
+        // stage; the buffer holds every (tile of output channels, chunk) block
+        const ConvArgs af = conv_args_f32(g, p, nullptr, nullptr, nullptr, false);
+        if (af.fpack) {
+            const int64_t nch = (g.c + p.rc - 1) / p.rc;
+            const int64_t jt_last = (g.k - 1) / p.bm, blk_last = jt_last * nch + (nch - 1);
+            if (((int64_t)p.bm * p.fp) % 4 || (p.rc * p.sc) % 4 || p.stage % 4 ||
+                (blk_last + 1) * p.bm * p.fp != (int64_t)af.num_jtiles * nch * p.bm * p.fp ||
+                (int64_t)p.bm * p.fp > p.stage - p.rc * p.sc)
+                r.fail("conv: repacked filter blocks of %lld floats do not fit the stage (fp %lld)",
+                       (long long)(p.bm * p.fp), (long long)p.fp);
+        }
         if (conv_args_f32(g, p, nullptr, nullptr, nullptr, false).ilv &&
             (!p.fvec || p.bm * (p.fp / 4) > (int64_t)kConvThreads * kIlvSlots))
             r.fail("conv: %lld 16-byte filter copies per chunk, in-loop issue covers %d", (long long)(p.bm * (p.fp / 4)),

@@ -1166,7 +1166,7 @@ struct PackBuffers {
     std::map<std::pair<int, hipStream_t>, std::pair<void*, size_t>> bufs;
 };
 
-static hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out) {
+hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out) {
     static PackBuffers pb;
     int dev = -1;
     if (stream == nullptr) {

@@ -55,7 +55,14 @@ struct ConvArgs {
     int cl_pb;             // positions per strip plane (one plane per 8-channel half)
     int cl_fpb;            // positions per filter plane
     int ilv;               // fp32 unfused: copies issued from inside the MFMA loop
+    int fpack;             // fp32: w is the filter repacked into chunk blocks (pack_filter_f32_kernel)
 };
+
+// Device buffer of at least `bytes` for a repacked filter, one per stream (the
+// legacy default stream once per device), taken from the stream-ordered pool
+// and replaced, stream-ordered, only when a larger one is needed; held until
+// the process ends.  Calls on one stream reuse it in stream order.
+hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out);
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
 struct TileRuns {
@@ -454,6 +461,7 @@ inline ConvArgs make_conv_args(const Geometry& g, const void* src, const void* w
     a.cl_pb = 0;
     a.cl_fpb = 0;
     a.ilv = 0;
+    a.fpack = 0;
     return a;
 }
 

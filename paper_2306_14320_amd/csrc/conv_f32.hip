@@ -76,7 +76,19 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
     const int kreal = rc_act * a.taps;
     const int nrows_f = min(a.k - j0, a.bm);
     constexpr bool kDma = sizeof(TIn) == 4;
-    if (kDma && a.fvec) {
+    if (kDma && a.fpack) {
+        // the repacked filter holds this tile's chunk as one block laid out
+        // like the LDS rows (zeros past the chunk's taps and past K): 16-byte
+        // copies of a contiguous range
+        const int nchunks = (a.c + a.rc - 1) / a.rc;
+        const float* blk = static_cast<const float*>(a.w) +
+                           ((int64_t)(j0 / a.bm) * nchunks + r0 / a.rc) * a.bm * a.fp;
+        const int units = (a.bm * a.fp) >> 2;
+        for (int c0 = wave * 64; c0 < units; c0 += kConvThreads) {
+            const int c = c0 + lane;
+            if (c < units) __builtin_amdgcn_global_load_lds(blk + 4 * c, (lds_void*)(F + 4 * c0), 16, 0, 0);
+        }
+    } else if (kDma && a.fvec) {
         // filter rows are whole 16-byte chunks (C*T and the chunk's rc*T are
         // multiples of 4): one DMA instruction fills 64 consecutive 16-byte
         // chunks of the row-major tile (rows of stride fp, a multiple of 4)
@@ -116,8 +128,9 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
     if (rc_stage > rc_act) {
         if (!FILTER_ONLY) zero_channels(S, a, tr, rc_act, rc_stage);
         const int nz = (rc_stage - rc_act) * a.taps;
-        for (int jj = wave; jj < a.bm; jj += 4)
-            for (int e = lane; e < nz; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
+        if (!(kDma && a.fpack))   // (the repacked blocks hold these zeros)
+            for (int jj = wave; jj < a.bm; jj += 4)
+                for (int e = lane; e < nz; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
     }
     if (FILTER_ONLY) return;
     const TIn* src = static_cast<const TIn*>(a.src);
@@ -864,6 +877,27 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         }
 }
 
+// fp32 filters whose chunk rows are not whole 16-byte vectors (rc*Fh*Fw not
+// a multiple of 4): w (K x C x Fh x Fw) rewritten into one block per (tile of
+// bm output channels, chunk of rc input channels), each laid out exactly like
+// the tile's LDS filter rows: row jj holds the chunk's rc*Fh*Fw taps of output
+// channel j0 + jj, then zeros up to the row stride fp; rows past K are zero.
+// The convolution then stages a chunk with 16-byte copies of one block.
+__global__ __launch_bounds__(256) void pack_filter_f32_kernel(const float* __restrict__ w, float* __restrict__ wp,
+                                                              int k, int c, int taps, int bm, int rc, int fp,
+                                                              int nchunks, int64_t total) {
+    const int64_t per_blk = (int64_t)bm * fp;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t blk = i / per_blk;
+        const int e = (int)(i - blk * per_blk);
+        const int jj = e / fp, col = e - jj * fp;
+        const int jt = (int)(blk / nchunks), ch = (int)(blk - (int64_t)jt * nchunks);
+        const int j = jt * bm + jj, r0 = ch * rc;
+        const int kreal = min(rc, c - r0) * taps;
+        wp[i] = (j < k && col < kreal) ? w[((int64_t)j * c + r0) * taps + col] : 0.0f;
+    }
+}
+
 // LDS floats of the raw rows of the fused fp32 kernel: with the expansion
 // map (filters of up to 3 rows, raw rows of up to kExpandMaxRaw floats) two
 // buffers, each with kExpandMaxRaw floats of slack for the map's reads;
@@ -1050,6 +1084,8 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     a.ilv = (!fused && p.svec && p.fvec && p.split == 0 && g.c % p.rc == 0 && p.sc / 4 <= 64 * kIlvSlots &&
              (int64_t)p.bm * (p.fp / 4) <= (int64_t)kConvThreads * kIlvSlots &&
              segs * g.c * plane < (1ll << 30) && (int64_t)p.bm * g.c * g.fh * g.fw < (1ll << 30)) ? 1 : 0;
+    // fp32 filter rows that are not whole vectors: copied from a repacked filter
+    a.fpack = (g.elem == 4 && !p.fvec) ? 1 : 0;
     // fused fp32 with the expansion map (MODE 4): filter-row and raw-row
     // copies from offsets computed once per lane (byte offsets below 2^32:
     // the input planes of the tile's images, the filter rows of the tile)
@@ -1061,11 +1097,27 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
 
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
                          const void* w, float* y, hipStream_t stream, char* err, size_t errlen) {
-    const ConvArgs a = conv_args_f32(g, p, src, w, y, fused);
+    ConvArgs a = conv_args_f32(g, p, src, w, y, fused);
     const int64_t blocks = ((g.npix + p.bn - 1) / p.bn) * a.num_jtiles;
     if (blocks > 0x7fffffff) {
         snprintf(err, errlen, "conv: grid of %lld workgroups is too large", (long long)blocks);
         return -5;
+    }
+    if (a.fpack) {
+        const int64_t nchunks = (g.c + p.rc - 1) / p.rc;
+        const int64_t total = (int64_t)a.num_jtiles * nchunks * p.bm * p.fp;
+        void* wpack = nullptr;
+        const hipError_t e = packed_filter_buffer(stream, (size_t)total * 4, &wpack);
+        if (e != hipSuccess) {
+            snprintf(err, errlen, "conv: packed-filter buffer of %lld bytes: %s", (long long)total * 4,
+                     hipGetErrorString(e));
+            return -4;
+        }
+        const int64_t pblocks = std::min<int64_t>((total + 255) / 256, 65536);
+        hipLaunchKernelGGL(pack_filter_f32_kernel, dim3((unsigned)pblocks), dim3(256), 0, stream,
+                           static_cast<const float*>(w), static_cast<float*>(wpack), (int)g.k, (int)g.c,
+                           (int)g.taps, p.bm, p.rc, (int)p.fp, (int)nchunks, total);
+        a.w = wpack;
     }
     if (g.elem == 2) launch_tile<uint16_t, 0, 0>(p, a, blocks, fused, stream);
     else if (g.fh == 3 && g.fw == 3) launch_tile<float, 3, 3>(p, a, blocks, fused, stream);
