@@ -486,7 +486,7 @@ void check_conv(const Geometry& g, bool fused_plan, Report& r) {
         // raw rows: two buffers with 768 floats of slack each when the map is used
         const int64_t mx = 64 * kF32ExpandGroups;
         const int64_t rawf = (g.fh <= 3 && p.raw_pitch <= mx) ? 2 * (p.rc * p.raw_pitch + mx)
-                                                              : p.rc * p.raw_pitch + 4 * (p.raw_pitch / g.w);
+                                                              : p.rc * p.raw_pitch + 6 * (p.raw_pitch / g.w);
         if (g.elem == 4 && p.lds_bytes + 4 * rawf > kConvLdsMaxBytes)
             r.fail("conv: fused plan uses %lld bytes of LDS", (long long)(p.lds_bytes + 4 * rawf));
         if (g.elem == 4 && g.fh <= 3 && p.sc < p.strip_cap + g.fh + 64)

@@ -297,6 +297,35 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
     }
 }
 
+// stage_raw<true> with the source row offsets of the tile read from RS
+// (RS[r] = segment * C*H*W + yy*W of raw row r, from the channel's plane in
+// the tile's first image; written once per kernel): the same copies, without
+// the per-unit segment arithmetic.
+__device__ inline void stage_raw_rows(float* X, const int64_t* RS, const ConvArgs& a, const TileRuns& tr,
+                                      const RawRows& rr, int r0, int rc_act) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float* x = static_cast<const float*>(a.src);
+    const int64_t plane = (int64_t)a.h * a.w_in;
+    int units;
+    const int nb = raw_blocks(a, rr, &units);
+    for (int rc = 0; rc < rc_act; ++rc) {
+        const float* xp = x + ((int64_t)tr.i0 * a.c + r0 + rc) * plane;
+        float* l = X + rc * a.raw_pitch;
+        // block rc*nb + b goes to wave (rc*nb + b) % 4, as in stage_raw
+        for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+            const int c0 = b * 64, c = c0 + lane;
+            if (c >= units) continue;
+            const int e = a.xvec ? 4 * c : c;
+            const int r = (int)fast_div((uint32_t)e, a.div_w);
+            const float* src = xp + RS[r] + (e - r * a.w_in);
+            if (a.xvec)
+                __builtin_amdgcn_global_load_lds(src, (lds_void*)(l + 4 * c0), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds(src, (lds_void*)(l + c0), 4, 0, 0);
+        }
+    }
+}
+
 // Fused fp32: write every raw element x[yy][xx] of channel rc to the strip
 // positions that hold it, one per window row m with filter row
 // u = yy + ph - m*sh in [0, Fh): position (m, k = xx + pw, u) of the run
@@ -762,6 +791,8 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
     // wait for every copy in flight)
     // without the map: the raw-row entries of the tile after the raw rows
     int4* RT = reinterpret_cast<int4*>(X + a.rc * a.raw_pitch);
+    // and their source row offsets (at most raw_pitch / W rows each)
+    int64_t* RS = reinterpret_cast<int64_t*>(RT + a.raw_pitch / a.w_in);
     const int xstride = a.rc * a.raw_pitch + kExpandMaxRaw;
     auto Xb = [&](int k) { return X + (k & 1) * xstride; };
     IlvCopies ilv;
@@ -790,6 +821,9 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
                 for (int r = threadIdx.x; r < rr.rtot; r += kConvThreads) {
                     const RawRowEntry en = raw_row_entry(a, tr, rr, r);
                     RT[r] = make_int4(en.base, en.cnt, en.lo, en.hi);
+                    int yy;
+                    const int sg = raw_segment(r, rr, tr.nseg, a, &yy);
+                    RS[r] = (int64_t)sg * a.c * ((int64_t)a.h * a.w_in) + (int64_t)yy * a.w_in;
                 }
             dma_barrier();   // zeros and row entries written, raw rows of chunk 0 (and 1) landed
             if (use_map) expand_map_apply<FHM>(S, X, emap, a, tr, rc_act, rc_stage);
@@ -826,7 +860,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
                     if (ch + 2 < nchunks) stage_raw<false>(Xb(ch), a, tr, rr, r1 + a.rc, min(a.rc, a.c - r1 - a.rc));
                     expand_map_apply<FHM>(S + off, Xb(ch + 1), emap, a, tr, rc1, rc_stage1);
                 } else {
-                    stage_raw<true>(X, a, tr, rr, r1, rc1);
+                    stage_raw_rows(X, RS, a, tr, rr, r1, rc1);
                 }
             } else {
                 stage<TIn, FUSED>(S + off, F + off, a, tr, j0, r1, rc1, rc_stage1);
@@ -901,11 +935,11 @@ __global__ __launch_bounds__(256) void pack_filter_f32_kernel(const float* __res
 // LDS floats of the raw rows of the fused fp32 kernel: with the expansion
 // map (filters of up to 3 rows, raw rows of up to kExpandMaxRaw floats) two
 // buffers, each with kExpandMaxRaw floats of slack for the map's reads;
-// without it one buffer and the tile's raw-row entries (4 ints per row, at
-// most raw_pitch / W rows).
+// without it one buffer and, per raw row of the tile (at most raw_pitch / W),
+// its expansion entry (4 ints) and its source offset (one int64).
 int64_t raw_floats(int fh, int rc, int64_t raw_pitch, int64_t w) {
     if (fh <= 3 && raw_pitch <= kExpandMaxRaw) return 2 * (rc * raw_pitch + kExpandMaxRaw);
-    return rc * raw_pitch + 4 * (raw_pitch / w);
+    return rc * raw_pitch + 6 * (raw_pitch / w);
 }
 
 template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP>
