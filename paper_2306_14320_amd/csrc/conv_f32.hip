@@ -571,7 +571,9 @@ __device__ inline void compute_chunk(f32x16 (&acc)[NJ][NP], const float* F, cons
 // expanded after the MFMAs); 2 fused fp32 with the expansion map and
 // double-buffered raw rows (filters of up to 3 rows, small tiles);
 // 3 unfused with 16-byte strips and filter rows whose copies are issued from
-// inside the MFMA loop, from per-lane offsets computed once.
+// inside the MFMA loop, from per-lane offsets computed once; 4 as 2, with the
+// filter-row and raw-row copies from per-lane offsets computed once (whole
+// chunks, 16-byte filter rows).
 
 // MODE 3 copies of one tile: the 16-byte strip copies of one channel and the
 // filter-row copies of one whole chunk, as in stage(), from per-lane byte
