@@ -166,6 +166,7 @@ def run_workload(wl, steps, warmup, with_cpu):
         torch.cuda.synchronize()
         per[name] = a.elapsed_time(b) * 1e-3 / steps
     t_xf, t_cv, t_fu = per["transform"], per["conv2d"], per["conv2d_fused"]
+    single = single_launch_times(launch, stream)
 
     conv_flops = 2 * wl.n * wl.k * wl.c * ho * wo * wl.fh * wl.fw
     e = x.element_size()
@@ -203,6 +204,7 @@ def run_workload(wl, steps, warmup, with_cpu):
             "conv2d_fused": {"ms": round(t_fu * 1e3, 4), "GFLOP_per_s": round(conv_flops / t_fu / 1e9, 1),
                              "mfma_frac": round(conv_flops / t_fu / 1e12 / peak, 4)},
             "transform_plus_conv2d_GFLOP_per_s": round(conv_flops / (t_xf + t_cv) / 1e9, 1),
+            "single_launch_ms": single,
         },
         "workspace": {"im2win_bytes": ws_bytes, "im2col_bytes": col_bytes,
                       "im2win_over_im2col": round(ws_bytes / col_bytes, 4),
@@ -212,6 +214,38 @@ def run_workload(wl, steps, warmup, with_cpu):
     }
     if with_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, conv_flops)
+    return out
+
+
+def single_launch_times(launch, stream, warm_reps=21, cold_reps=11):
+    """Each kernel timed launch by launch (an event pair around every launch on
+    its stream): the median over warm_reps warm launches and the best of the
+    first five (the paper reports the best of five runs, Sec. IV-B), and the
+    median over cold_reps launches that each follow a 1 GiB device write, which
+    evicts the inputs from the 256 MB Infinity Cache."""
+    import statistics
+    import torch
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0")
+    out = {}
+    for name, fn in launch.items():
+        times = {}
+        for mode, reps in (("warm", warm_reps), ("cold", cold_reps)):
+            evs = []
+            for _ in range(reps):
+                if mode == "cold":
+                    flush.zero_()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn()
+                b.record(stream)
+                evs.append((a, b))
+            torch.cuda.synchronize()
+            times[mode] = [a.elapsed_time(b) for a, b in evs]
+        out[name] = {"warm_median": round(statistics.median(times["warm"]), 4),
+                     "warm_best_of_5": round(min(times["warm"][:5]), 4),
+                     "cold_median": round(statistics.median(times["cold"]), 4)}
+    del flush
+    torch.cuda.empty_cache()
     return out
 
 
