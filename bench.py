@@ -264,9 +264,24 @@ def cpu_baseline(wl, conv_flops):
         oracle.direct_conv(s, x, w)
         total += time.perf_counter() - t0
         reps += 1
+    # the oracle's transformation of the same input (bytes: x read once, the
+    # window tensor written), one run
+    xr = workloads.make_input(wl).numpy()
+    t0 = time.perf_counter()
+    win = oracle.im2win(s, xr)
+    t_xf = time.perf_counter() - t0
+    xf_bytes = xr.nbytes + win.nbytes
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": round(conv_flops * reps / total / 1e9, 3), "unit": "GFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"full workload (N={wl.n}), {reps} run(s), {total:.1f} s"}
+            "cores": oracle.num_threads(), "kind": "oracle", "cpu_model": model,
+            "transform_GB_per_s": round(xf_bytes / t_xf / 1e9, 2),
+            "sample": f"full workload (N={wl.n}), {reps} run(s) of the convolution, {total:.1f} s; "
+                      f"one run of the transformation, {t_xf:.2f} s"}
 
 
 def profile_call(wl, call, steps, warmup):
