@@ -244,6 +244,41 @@ def test_bf16_error_against_unrounded_data():
     assert rel < 1e-2
 
 
+def test_repacked_filters_share_the_stream_buffer():
+    """fp32 filters whose chunk rows are not whole 16-byte vectors (7x7, 5x5,
+    11x11) are repacked per call into the same per-stream buffer as the bf16
+    fast kernels' filters: fp32 and bf16 convolutions interleaved on two
+    streams, with a larger filter replacing a stream's buffer in the middle,
+    each result against the oracle."""
+    cases = [
+        (1, "f32", (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3)),
+        (2, "bf16", (2, 32, 14, 14, 64, 3, 3, 1, 1, 1, 1)),
+        (1, "f32", (1, 6, 24, 24, 96, 5, 5, 1, 1, 0, 0)),
+        (2, "f32", (1, 3, 47, 47, 96, 11, 11, 4, 4, 0, 0)),
+        (1, "bf16", (1, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)),
+        (2, "f32", (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3)),
+    ]
+    streams = {1: torch.cuda.Stream(device=DEV), 2: torch.cuda.Stream(device=DEV)}
+    runs = []
+    for i, (sid, dtype, shape) in enumerate(cases):
+        wl, x_cpu, w_cpu = workloads.random_case(800 + i, *shape, dtype=dtype)
+        _label("repacked-filter stream", wl)
+        d = _desc(wl)
+        assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+        stream = streams[sid]
+        with torch.cuda.stream(stream):
+            x, w = x_cpu.to(DEV), w_cpu.to(DEV)
+            y_fused = P.conv2d_fused(x, w, d, stream=stream)
+            y = P.conv2d(P.transform(x, d, stream=stream), w, d, stream=stream)
+        runs.append((wl, x_cpu, w_cpu, y, y_fused))
+    torch.cuda.synchronize()
+    for wl, x_cpu, w_cpu, y, y_fused in runs:
+        ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
+        for what, out in (("unfused", y), ("fused", y_fused)):
+            _assert_close(out.cpu().numpy().astype(np.float64), ref, ref_abs, wl.c * wl.fh * wl.fw, wl.dtype,
+                          f"{wl.name} {what}")
+
+
 def test_bf16_packed_filter_per_stream():
     """The bf16 fast kernels read a repacked filter that the library keeps per
     stream: two streams with different filters in flight at once, then a
