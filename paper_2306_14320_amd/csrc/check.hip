@@ -287,6 +287,8 @@ void check_conv_bf16_variant(const Geometry& g, const ConvPlan& p, bool fused, R
             }
             src[pos] = (int64_t)s * plane + e;
         };
+        // (capacities of the 4-wave kernels; the 8-wave 128 x 256 kernels hold
+        // at least as many items per workgroup)
         const int64_t items = a.svec ? 2 * (int64_t)tr.ck_total : 2 * (int64_t)tr.strip_len;
         const int64_t cap_items = (int64_t)kConvThreads *
                                   (a.svec ? (p.strip_items > kConvThreads ? 2 : 1) : kBf16StripScalarItems);

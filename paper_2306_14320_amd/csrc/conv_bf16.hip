@@ -542,7 +542,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_kernel(ConvArgs a) {
 template <int SVI, int FI>
 struct FastStage {
     uint32_t sd[SVI][16];          // strips: 8 channels x 4 positions per item
-    u32x4 fd[FI];                  // packed filter pieces threadIdx.x + 256*i
+    u32x4 fd[FI];                  // packed filter pieces threadIdx.x + NT*i
 };
 
 // Unfused kernel for the common case: whole 16-channel chunks, whole tiles of
@@ -551,14 +551,16 @@ struct FastStage {
 // unchanged.  Strips and filter pieces pass through registers two chunks
 // ahead, so every global load is one the compiler waits for precisely, and
 // the chunk barrier only waits for the LDS stores.
-template <int FH, int FW, int BM, int BN, int TJ, int TP, int SVI>
-__global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a) {
-    static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+// NT threads per workgroup: 256 (4 waves), or 512 (8 waves, two per SIMD
+// when one workgroup fills a CU).
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int SVI, int NT>
+__global__ __launch_bounds__(NT) void conv_bf16_fast_kernel(ConvArgs a) {
+    static_assert((BM / TJ) * (BN / TP) == NT / 64, "one wave per TJ x TP block");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
     constexpr int T = FH * FW;
     constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
-    constexpr int FI = (kPieces + kConvThreads - 1) / kConvThreads;   // filter pieces per thread
+    constexpr int FI = (kPieces + NT - 1) / NT;   // filter pieces per thread
     static_assert(FI <= T, "one filter piece stored per tap");
     using St = FastStage<SVI, FI>;
 
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
     const int nitems = 2 * rn.ck_total;
 #pragma unroll
     for (int k = 0; k < SVI; ++k) {
-        int q = threadIdx.x + k * kConvThreads;
+        int q = threadIdx.x + k * NT;
         if (q >= nitems) q &= 1;          // repeat an item: same values, same place
         const ItemAt it = vec_item(q >> 1, rn, a);
         sp[k] = src + ((int64_t)(rn.i0 + it.s) * a.c + 8 * (q & 1)) * plane + it.e;
@@ -610,13 +612,13 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
     }
     const int nchunks = a.c / kRC;
     // packed filter blocks of this tile of output channels; this thread's
-    // pieces P = threadIdx.x + 256*i and their LDS positions (the last piece
+    // pieces P = threadIdx.x + NT*i and their LDS positions (the last piece
     // again, never stored, where P runs past the block)
     const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
     int fpc[FI], fdst[FI];
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
-        const int P = threadIdx.x + kConvThreads * i;
+        const int P = threadIdx.x + NT * i;
         const int Pc = P < kPieces ? P : kPieces - 1;
         const int g = Pc >= kPlane ? 1 : 0;
         fpc[i] = Pc * 8;
@@ -645,7 +647,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fast_kernel(ConvArgs a
     // position t (t < 4) of every item (16-bit transpose, one 16-byte store)
     auto part = [&](const St& r, uint16_t* stg, int t) {
         const int ti = t < FI ? t : 0;   // (indices stay inside the arrays when t >= FI)
-        if (t < FI && threadIdx.x + kConvThreads * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
+        if (t < FI && threadIdx.x + NT * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
         if (t >= 4) return;
 #pragma unroll
         for (int k = 0; k < SVI; ++k) {
@@ -748,9 +750,10 @@ struct FusedMap {
     int dst[2][FH];   // element offsets in a stage of the two positions, per window-row slot
 };
 
-template <int FH, int FW, int BM, int BN, int TJ, int TP, int IPT>
-__global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs a) {
-    static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+// NT threads per workgroup, as for the fast kernel.
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int IPT, int NT>
+__global__ __launch_bounds__(NT) void conv_bf16_fused_kernel(ConvArgs a) {
+    static_assert((BM / TJ) * (BN / TP) == NT / 64, "one wave per TJ x TP block");
     static_assert(IPT >= 1 && IPT <= kBf16FusedItems, "raw items per thread");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
@@ -807,7 +810,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     int64_t xbase[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
-        int q = threadIdx.x + j * kConvThreads;
+        int q = threadIdx.x + j * NT;
         if (q >= nitems) q &= 1;
         int sg, yy, xx;
         item_at(q, &sg, &yy, &xx);
@@ -817,7 +820,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     FusedMap<FH> mp[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
-        const int q = threadIdx.x + j * kConvThreads;
+        const int q = threadIdx.x + j * NT;
         const int g = q & 1;
         const int spare = (g * a.cl_pb + a.cl_pb - kBf16Spare + lane) * 8;
 #pragma unroll
@@ -851,16 +854,16 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     }
     const int nchunks = a.c / kRC;
     // packed filter blocks of this tile of output channels, and this thread's
-    // pieces P = threadIdx.x + 256*i (the last piece again, never stored,
+    // pieces P = threadIdx.x + NT*i (the last piece again, never stored,
     // where P runs past the block)
     constexpr int kPlane = T * BM, kPieces = 2 * kPlane;
-    constexpr int FI = (kPieces + kConvThreads - 1) / kConvThreads;
+    constexpr int FI = (kPieces + NT - 1) / NT;
     static_assert(FI <= T && FH <= T, "one filter piece and one window-row slot stored per tap");
     const uint16_t* fblk = static_cast<const uint16_t*>(a.w) + (int64_t)jtile * nchunks * (16 * T * BM);
     int fpc[FI], fdst[FI];
 #pragma unroll
     for (int i = 0; i < FI; ++i) {
-        const int P = threadIdx.x + kConvThreads * i;
+        const int P = threadIdx.x + NT * i;
         const int Pc = P < kPieces ? P : kPieces - 1;
         const int g = Pc >= kPlane ? 1 : 0;
         fpc[i] = Pc * 8;
@@ -886,12 +889,12 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     // row slot t (t < FH) of both positions of every item
     auto part = [&](const Stage& r, uint16_t* stg, int t) {
         const int ti = t < FI ? t : 0;
-        if (t < FI && threadIdx.x + kConvThreads * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
+        if (t < FI && threadIdx.x + NT * t < kPieces) store16(stg + fdst[ti], r.fd[ti]);
         if (t >= FH) return;
         const int tu = t < FH ? t : 0;
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
-            if (threadIdx.x + j * kConvThreads < nitems) {
+            if (threadIdx.x + j * NT < nitems) {
                 u32x4 o0, o1;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -916,7 +919,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_bf16_fused_kernel(ConvArgs 
     {
         const u32x4 z = {0u, 0u, 0u, 0u};
         for (int st = 0; st < 2; ++st)
-            for (int e = threadIdx.x; e < 2 * a.cl_pb; e += kConvThreads) store16(lds + st * a.stage + e * 8, z);
+            for (int e = threadIdx.x; e < 2 * a.cl_pb; e += NT) store16(lds + st * a.stage + e * 8, z);
     }
     Stage st0, st1;
     load(st0, 0);
@@ -988,22 +991,22 @@ void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int smode, int s
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
 }
 
-template <int FH, int FW, int BM, int BN, int TJ, int TP>
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int NT = kConvThreads>
 void launch_fast_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int svi, hipStream_t stream) {
-    auto kern = svi == 1 ? conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 1>
-                         : conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 2>;
+    auto kern = svi == 1 ? conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 1, NT>
+                         : conv_bf16_fast_kernel<FH, FW, BM, BN, TJ, TP, 2, NT>;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), (size_t)lds, stream, a);
 }
 
-template <int FH, int FW, int BM, int BN, int TJ, int TP>
+template <int FH, int FW, int BM, int BN, int TJ, int TP, int NT = kConvThreads>
 void launch_fused_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, int ipt, hipStream_t stream) {
-    auto kern = ipt == 1 ? conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 1>
-                         : conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 2>;
+    auto kern = ipt == 1 ? conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 1, NT>
+                         : conv_bf16_fused_kernel<FH, FW, BM, BN, TJ, TP, 2, NT>;
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(NT), (size_t)lds, stream, a);
 }
 
 template <int FH, int FW, bool FVEC>
@@ -1012,7 +1015,8 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode
     if constexpr (FVEC && FH <= 3) {
         if (smode == kStripFused && p.fused_fast) {
             const int ipt = p.fused_ipt;
-            if (p.bn == 256) launch_fused_cfg<FH, FW, 128, 256, 64, 128>(a, blocks, p.lds_bytes, ipt, stream);
+            // (8 waves of 64 x 64; the plan holds at most 512 raw items then)
+            if (p.bn == 256) launch_fused_cfg<FH, FW, 128, 256, 64, 64, 512>(a, blocks, p.lds_bytes, 1, stream);
             else if (p.bm == 128) launch_fused_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, ipt, stream);
             else if (p.bn == 128) launch_fused_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, ipt, stream);
             else launch_fused_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, ipt, stream);
@@ -1021,7 +1025,10 @@ void launch_tile(const ConvPlan& p, const ConvArgs& a, int64_t blocks, int smode
     }
     if constexpr (FVEC) {
         if (smode == kStripVec && p.fast) {
-            if (p.bn == 256) launch_fast_cfg<FH, FW, 128, 256, 64, 128>(a, blocks, p.lds_bytes, svi, stream);
+            // the 128 x 256 tile runs one workgroup per CU: 8 waves of 64 x 64,
+            // two per SIMD
+            if (p.bn == 256)
+                launch_fast_cfg<FH, FW, 128, 256, 64, 64, 512>(a, blocks, p.lds_bytes, p.strip_items > 512 ? 2 : 1, stream);
             else if (p.bm == 128) launch_fast_cfg<FH, FW, 128, 128, 64, 64>(a, blocks, p.lds_bytes, svi, stream);
             else if (p.bn == 128) launch_fast_cfg<FH, FW, 64, 128, 32, 64>(a, blocks, p.lds_bytes, svi, stream);
             else launch_fast_cfg<FH, FW, 64, 64, 32, 32>(a, blocks, p.lds_bytes, svi, stream);
@@ -1103,10 +1110,10 @@ ConvPlan plan_conv_bf16(const Geometry& g, bool fused) {
         if (blocks > best_blocks) { best = p; best_blocks = blocks; }
     }
     if (best.kind == ConvPlan::kNone) return plan_conv_f32(g);
-    // The fast kernels also have a 128 x 256 tile (4 waves of 64 x 128:
-    // fewer LDS reads per matrix-core instruction and half the filter copies
-    // per pixel).  It only fits one workgroup per CU, as 128 x 128 does, so it
-    // is taken when it needs no more rounds of workgroups over the CUs.
+    // The fast kernels also have a 128 x 256 tile (8 waves of 64 x 64, two per
+    // SIMD: half the filter copies per pixel).  It only fits one workgroup per
+    // CU, as 128 x 128 does, so it is taken when it needs no more rounds of
+    // workgroups over the CUs.
     const int64_t raw256 = raw_rows_bound(g, 256) * g.w;
     if (best.bm == 128 && best.bn == 128 &&
         (fused ? best.fused_fast && raw256 <= (int64_t)kConvThreads * kBf16FusedItems : best.fast)) {
