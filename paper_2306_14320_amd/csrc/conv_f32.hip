@@ -58,7 +58,7 @@ __device__ inline void dma_run(const float* g, float* l, int len, int lane) {
 // Zero the strips of channel slots [c0, c1) over the tile's extent.
 __device__ inline void zero_channels(float* S, const ConvArgs& a, const TileRuns& tr, int c0, int c1) {
     for (int c = c0; c < c1; ++c)
-        for (int e = threadIdx.x; e < tr.extent; e += kConvThreads) S[c * a.sc + e] = 0.0f;
+        for (int e = threadIdx.x; e < tr.extent; e += (int)blockDim.x) S[c * a.sc + e] = 0.0f;
 }
 
 // Stage one channel chunk [r0, r0 + rc_act) of one tile into S (strips,
@@ -73,6 +73,7 @@ template <typename TIn, bool FUSED, bool FILTER_ONLY = false>
 __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRuns& tr, int j0,
                              int r0, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nw = (int)(blockDim.x >> 6);   // waves (a power of two)
     const int kreal = rc_act * a.taps;
     const int nrows_f = min(a.k - j0, a.bm);
     constexpr bool kDma = sizeof(TIn) == 4;
@@ -84,7 +85,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         const float* blk = static_cast<const float*>(a.w) +
                            ((int64_t)(j0 / a.bm) * nchunks + r0 / a.rc) * a.bm * a.fp;
         const int units = (a.bm * a.fp) >> 2;
-        for (int c0 = wave * 64; c0 < units; c0 += kConvThreads) {
+        for (int c0 = wave * 64; c0 < units; c0 += (int)blockDim.x) {
             const int c = c0 + lane;
             if (c < units) __builtin_amdgcn_global_load_lds(blk + 4 * c, (lds_void*)(F + 4 * c0), 16, 0, 0);
         }
@@ -96,7 +97,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         const int64_t wrow = (int64_t)a.c * a.taps;
         const int cpr = a.fp >> 2, creal = kreal >> 2;
         const int total = nrows_f * cpr;
-        for (int c0 = wave * 64; c0 < total; c0 += kConvThreads) {
+        for (int c0 = wave * 64; c0 < total; c0 += (int)blockDim.x) {
             const int c = c0 + lane;
             const int jj = (int)fast_div((uint32_t)c, a.div_fp);
             const int col = c - jj * cpr;
@@ -109,7 +110,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         const float* w = static_cast<const float*>(a.w) + ((int64_t)j0 * a.c + r0) * a.taps;
         const int64_t wrow = (int64_t)a.c * a.taps;
         const int total = nrows_f * a.fp;
-        for (int e0 = wave * 64; e0 < total; e0 += kConvThreads) {
+        for (int e0 = wave * 64; e0 < total; e0 += (int)blockDim.x) {
             const int e = e0 + lane;
             const int jj = (int)fast_div((uint32_t)e, a.div_fp);
             const int col = e - jj * a.fp;
@@ -118,7 +119,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         }
     } else {
         const TIn* w = static_cast<const TIn*>(a.w);
-        for (int jj = wave; jj < nrows_f; jj += 4) {
+        for (int jj = wave; jj < nrows_f; jj += nw) {
             const TIn* g = w + ((int64_t)(j0 + jj) * a.c + r0) * a.taps;
             for (int e = lane; e < kreal; e += 64) F[jj * a.fp + e] = to_f32(g[e]);
         }
@@ -129,7 +130,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         if (!FILTER_ONLY) zero_channels(S, a, tr, rc_act, rc_stage);
         const int nz = (rc_stage - rc_act) * a.taps;
         if (!(kDma && a.fpack))   // (the repacked blocks hold these zeros)
-            for (int jj = wave; jj < a.bm; jj += 4)
+            for (int jj = wave; jj < a.bm; jj += nw)
                 for (int e = lane; e < nz; e += 64) F[jj * a.fp + kreal + e] = 0.0f;
     }
     if (FILTER_ONLY) return;
@@ -151,8 +152,8 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         const int nb = (ck_total + 63) >> 6;
         for (int rc = 0; rc < rc_act; ++rc) {
             float* l = S + rc * a.sc;
-            // block rc*nb + b goes to wave (rc*nb + b) % 4
-            for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+            // block rc*nb + b goes to wave (rc*nb + b) % nw
+            for (int b = (wave - rc * nb) & (nw - 1); b < nb; b += nw) {
                 const int c0 = b * 64;
                 const int c = c0 + lane;
                 int sgi = 0, cs = c;
@@ -170,7 +171,7 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
         return;
     }
     const int nruns = rc_act * nseg;
-    if (!FUSED && kDma && nruns < 4) {
+    if (!FUSED && kDma && nruns < nw) {
         // fewer runs than waves (one or two channels): blocks of 64 floats of
         // the runs, counted run after run, to the waves round-robin (block gb
         // goes to wave gb % 4); otherwise whole runs, below
@@ -182,14 +183,14 @@ __device__ inline void stage(float* S, float* F, const ConvArgs& a, const TileRu
                 const int nbq = (sr.len + 63) >> 6;
                 const float* g = srcf + (((int64_t)(i0 + s) * a.c + r0 + rc) * a.ho + sr.m) * a.row_len + sr.q;
                 float* l = S + rc * a.sc + sr.off;
-                for (int b = (wave - gstart) & 3; b < nbq; b += 4)
+                for (int b = (wave - gstart) & (nw - 1); b < nbq; b += nw)
                     if (64 * b + lane < sr.len)
                         __builtin_amdgcn_global_load_lds(g + 64 * b + lane, (lds_void*)(l + 64 * b), 4, 0, 0);
                 gstart += nbq;
             }
         return;
     }
-    for (int q = wave; q < nruns; q += 4) {
+    for (int q = wave; q < nruns; q += nw) {
         const int rc = q / nseg, s = q - rc * nseg;
         const SegRun sr = seg_run(s, nseg, len0, len_mid, len_last, m0, qa0, d_first, d_second, d_stride);
         float* l = S + rc * a.sc + sr.off;
@@ -265,6 +266,7 @@ template <bool BLOCKS>
 __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr, const RawRows& rr,
                                  int r0, int rc_act) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nw = (int)(blockDim.x >> 6);   // waves (a power of two)
     const float* x = static_cast<const float*>(a.src);
     const int64_t plane = (int64_t)a.h * a.w_in;
     const int nseg = tr.nseg, i0 = tr.i0;
@@ -290,9 +292,9 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
     if constexpr (BLOCKS) {
         // block rc*nb + b goes to wave (rc*nb + b) % 4
         for (int rc = 0; rc < rc_act; ++rc)
-            for (int b = (wave - rc * nb) & 3; b < nb; b += 4) copy_block(rc, b * 64);
+            for (int b = (wave - rc * nb) & (nw - 1); b < nb; b += nw) copy_block(rc, b * 64);
     } else {
-        for (int rc = wave; rc < rc_act; rc += 4)
+        for (int rc = wave; rc < rc_act; rc += nw)
             for (int c0 = 0; c0 < units; c0 += 64) copy_block(rc, c0);
     }
 }
@@ -304,6 +306,7 @@ __device__ inline void stage_raw(float* X, const ConvArgs& a, const TileRuns& tr
 __device__ inline void stage_raw_rows(float* X, const int64_t* RS, const ConvArgs& a, const TileRuns& tr,
                                       const RawRows& rr, int r0, int rc_act) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nw = (int)(blockDim.x >> 6);   // waves (a power of two)
     const float* x = static_cast<const float*>(a.src);
     const int64_t plane = (int64_t)a.h * a.w_in;
     int units;
@@ -311,8 +314,8 @@ __device__ inline void stage_raw_rows(float* X, const int64_t* RS, const ConvArg
     for (int rc = 0; rc < rc_act; ++rc) {
         const float* xp = x + ((int64_t)tr.i0 * a.c + r0 + rc) * plane;
         float* l = X + rc * a.raw_pitch;
-        // block rc*nb + b goes to wave (rc*nb + b) % 4, as in stage_raw
-        for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+        // block rc*nb + b goes to wave (rc*nb + b) % nw, as in stage_raw
+        for (int b = (wave - rc * nb) & (nw - 1); b < nb; b += nw) {
             const int c0 = b * 64, c = c0 + lane;
             if (c >= units) continue;
             const int e = a.xvec ? 4 * c : c;
@@ -339,6 +342,7 @@ template <bool TRIM>
 __device__ inline void expand_raw_cols(float* S, const float* X, const int4* RT, const ConvArgs& a,
                                        const TileRuns& tr, const RawRows& rr, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nw = (int)(blockDim.x >> 6);   // waves (a power of two)
     const int vw = a.xvec ? 4 : 1;
     const int dstep = a.row_len - a.sh;   // next window row: one row on, sh filter rows up
     int n;
@@ -346,8 +350,8 @@ __device__ inline void expand_raw_cols(float* S, const float* X, const int4* RT,
     for (int rc = 0; rc < rc_act; ++rc) {
         const float* xl = X + rc * a.raw_pitch;
         float* sl = S + rc * a.sc;
-        // block rc*nb + b goes to wave (rc*nb + b) % 4, as in stage_raw
-        for (int b = (wave - rc * nb) & 3; b < nb; b += 4) {
+        // block rc*nb + b goes to wave (rc*nb + b) % nw, as in stage_raw
+        for (int b = (wave - rc * nb) & (nw - 1); b < nb; b += nw) {
             const int q = b * 64 + lane;
             if (q >= n) continue;
             const int e = q * vw;
@@ -437,8 +441,9 @@ template <int FH>
 __device__ inline void expand_map_apply(float* S, const float* X, const ExpandMap<FH>& mp,
                                         const ConvArgs& a, const TileRuns& tr, int rc_act, int rc_stage) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nw = (int)(blockDim.x >> 6);   // waves (a power of two)
     const int ngroups = a.raw_pitch >> 6;   // raw pitch is a multiple of 64
-    for (int rc = wave; rc < rc_act; rc += 4) {
+    for (int rc = wave; rc < rc_act; rc += nw) {
         const float* xl = X + rc * a.raw_pitch + lane;
         float* sl = S + rc * a.sc;
         float v[kExpandK];   // all reads in flight before the first write (the
@@ -709,14 +714,17 @@ struct RawCopies {
     }
 };
 
-template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, int MODE>
-__global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
+// NT threads: 256 (4 waves), or 512 (8 waves, two per SIMD) for the generic
+// modes 0 and 1 when the tile's LDS leaves room for one workgroup per CU.
+template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int TP, int MODE, int NT = kConvThreads>
+__global__ __launch_bounds__(NT) void conv_f32_kernel(ConvArgs a) {
     constexpr bool FUSED = MODE == 1 || MODE == 2 || MODE == 4;
     constexpr bool ILV = MODE == 3;
     // MODE 4: MODE 2 with the filter-row and raw-row copies from per-lane
     // offsets computed once
     constexpr bool FASTCP = MODE == 4;
-    static_assert((BM / TJ) * (BN / TP) == kConvThreads / 64, "4 waves per workgroup");
+    static_assert((BM / TJ) * (BN / TP) == NT / 64, "one wave per TJ x TP block");
+    static_assert(NT == kConvThreads || MODE == 0 || MODE == 1, "8 waves only for the generic modes");
     constexpr int NJ = TJ / 32, NP = TP / 32;
     constexpr int WAVES_P = BN / TP;
 
@@ -805,7 +813,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
         if constexpr (RAW) {
             rr = raw_rows(tr, a);
             for (int sg = 0; sg < 2; ++sg)
-                for (int e = threadIdx.x; e < a.rc * a.sc; e += kConvThreads) S[sg * a.stage + e] = 0.0f;
+                for (int e = threadIdx.x; e < a.rc * a.sc; e += (int)blockDim.x) S[sg * a.stage + e] = 0.0f;
             if constexpr (FASTCP) {
                 // whole chunks only: rc_act = rc_stage = rc
                 ilv.init_filter(a, j0);
@@ -820,7 +828,7 @@ __global__ __launch_bounds__(kConvThreads) void conv_f32_kernel(ConvArgs a) {
             }
             if (use_map) expand_map_build<FHM>(emap, a, tr, rr);
             else
-                for (int r = threadIdx.x; r < rr.rtot; r += kConvThreads) {
+                for (int r = threadIdx.x; r < rr.rtot; r += (int)blockDim.x) {
                     const RawRowEntry en = raw_row_entry(a, tr, rr, r);
                     RT[r] = make_int4(en.base, en.cnt, en.lo, en.hi);
                     int yy;
@@ -948,16 +956,31 @@ template <typename TIn, int FH, int FW, bool ROWS, int BM, int BN, int TJ, int T
 void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipStream_t stream) {
     auto kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 0>;
     constexpr int kIlvMode = sizeof(TIn) == 4 && FH > 0 ? 3 : 0;
-    if (!fused && a.svec && a.fvec && a.ilv) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, kIlvMode>;
+    bool generic = true;   // mode 0 or 1
+    if (!fused && a.svec && a.fvec && a.ilv) {
+        kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, kIlvMode>;
+        generic = kIlvMode == 0;
+    }
     if (fused) kern = conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 1>;
     if constexpr (sizeof(TIn) == 4 && FH > 0 && FH <= 3)
-        if (fused && a.raw_pitch <= kExpandMaxRaw)
+        if (fused && a.raw_pitch <= kExpandMaxRaw) {
             kern = a.ilv ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 4>
                          : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ, TP, 2>;
+            generic = false;
+        }
     if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch, a.w_in) * 4;
+    // one workgroup per CU: 8 waves of half the wave tile, two per SIMD
+    constexpr int TJ8 = TJ >= 64 ? TJ / 2 : TJ, TP8 = TJ >= 64 ? TP : TP / 2;
+    int threads = kConvThreads;
+    if constexpr (TJ8 >= 32 && TP8 >= 32 && (BM / TJ8) * (BN / TP8) == 8)
+        if (generic && lds > kConvLdsPipelinedBytes) {
+            kern = fused ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ8, TP8, 1, 512>
+                         : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ8, TP8, 0, 512>;
+            threads = 512;
+        }
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kConvThreads), (size_t)lds, stream, a);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(threads), (size_t)lds, stream, a);
 }
 
 template <typename TIn, int FH, int FW, bool ROWS>
