@@ -969,11 +969,14 @@ void launch_cfg(const ConvArgs& a, int64_t blocks, int64_t lds, bool fused, hipS
             generic = false;
         }
     if (fused && sizeof(TIn) == 4) lds += raw_floats(a.fh, a.rc, a.raw_pitch, a.w_in) * 4;
-    // one workgroup per CU: 8 waves of half the wave tile, two per SIMD
+    // 8 waves of half the wave tile: for one workgroup per CU (two waves per
+    // SIMD instead of one), and for the generic fused kernel, whose staging
+    // and expansion the extra waves hide (measured faster on every layer it
+    // runs; the unfused generic kernel gained nothing at two workgroups per CU)
     constexpr int TJ8 = TJ >= 64 ? TJ / 2 : TJ, TP8 = TJ >= 64 ? TP : TP / 2;
     int threads = kConvThreads;
     if constexpr (TJ8 >= 32 && TP8 >= 32 && (BM / TJ8) * (BN / TP8) == 8)
-        if (generic && lds > kConvLdsPipelinedBytes) {
+        if (generic && (fused || lds > kConvLdsPipelinedBytes)) {
             kern = fused ? conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ8, TP8, 1, 512>
                          : conv_f32_kernel<TIn, FH, FW, ROWS, BM, BN, TJ8, TP8, 0, 512>;
             threads = 512;
