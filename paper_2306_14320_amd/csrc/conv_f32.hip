@@ -8,7 +8,8 @@
 // one strip and are read from the same on-chip copy (the reuse the paper's
 // loop order is built around, Sec. III-B).
 //
-// Workgroup = 4 waves computing a BM (channels) x BN (pixels) tile of Y.
+// Workgroup = 4 waves (8 for the generic kernels in the cases launch_cfg
+// names) computing a BM (channels) x BN (pixels) tile of Y.
 // Pixels are tiled in flattened (i, m, n) order, so a tile reads a few
 // window-tensor rows, which for one channel are contiguous in memory (one run
 // per image).  Per chunk of input channels:
