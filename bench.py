@@ -15,7 +15,7 @@ launch durations, from which the roofline fractions are computed, come from a
 second timed region per kernel: as many back-to-back launches as timed steps,
 on the same stream, between two HIP events.
 
-Prints one JSON line (rank 0, N=1).  `--gpus N` with N > 1 exits: this build
+Prints one JSON line (rank 0, N=1).  `--gpus N` with N > 1 exits: the library
 runs on one GPU.
 """
 import argparse
@@ -559,7 +559,7 @@ def baselines_sweep(table1, batch):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
               "multi-GPU path", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
