@@ -75,34 +75,36 @@ int64_t oracle_im2col_elems(const int64_t *shp) {
     return N_ * (C_ * FH_ * FW_) * (ho * wo);
 }
 
-/* The im2win transformation, Alg. 1 with zero padding:
- *   win[i][r][m][k*Fh + u] = Ipad[i][r][m*sh + u][k],  k < Wr, u < Fh,
+/* The im2win transformation (Sec. III-A, Eq. 2 read through the copy
+ * relation of Alg. 1) with zero padding, written as the value of each element
+ * of the window tensor, computed from its flat index e:
+ *   e = (((i*C + r)*Ho + m)*Wr + k)*Fh + u   (u fastest: a row holds the Fh
+ *                                            input rows column by column)
+ *   win[e] = Ipad[i][r][m*sh + u][k],  k < Wr, u < Fh,
  * where Ipad is the input with ph zero rows and pw zero columns on each side.
- * A pure copy of `elem_bytes`-sized elements (4 for fp32, 2 for bf16, 8 for fp64), so the
- * result is unique and any implementation must reproduce it bit for bit. */
+ * A pure copy of `elem_bytes`-sized elements (4 for fp32, 2 for bf16, 8 for
+ * fp64), so the result is unique and any implementation must reproduce it bit
+ * for bit. */
 void oracle_im2win(const int64_t *shp, const void *x, void *win, int elem_bytes, int trimmed) {
     const int64_t ho = oracle_out_extent(H_, FH_, SH_, PH_);
-    const int64_t wp = oracle_row_width(shp, trimmed);   /* Wr */
-    const int64_t row = wp * FH_;
+    const int64_t wr = oracle_row_width(shp, trimmed);
+    const int64_t total = N_ * C_ * ho * wr * FH_;
     const unsigned char *src = (const unsigned char *)x;
     unsigned char *dst = (unsigned char *)win;
     const size_t eb = (size_t)elem_bytes;
 #pragma omp parallel for
-    for (int64_t i = 0; i < N_; ++i)
-        for (int64_t r = 0; r < C_; ++r)
-            for (int64_t m = 0; m < ho; ++m)
-                for (int64_t k = 0; k < wp; ++k)
-                    for (int64_t u = 0; u < FH_; ++u) {
-                        int64_t yy = m * SH_ + u - PH_; /* row in the unpadded input */
-                        int64_t xx = k - PW_;           /* column in the unpadded input */
-                        size_t o = (size_t)((((i * C_ + r) * ho + m) * row) + k * FH_ + u);
-                        if (yy >= 0 && yy < H_ && xx >= 0 && xx < W_) {
-                            size_t s = (size_t)(((i * C_ + r) * H_ + yy) * W_ + xx);
-                            memcpy(dst + o * eb, src + s * eb, eb);
-                        } else {
-                            memset(dst + o * eb, 0, eb);
-                        }
-                    }
+    for (int64_t e = 0; e < total; ++e) {
+        const int64_t u = e % FH_;
+        const int64_t k = (e / FH_) % wr;
+        const int64_t m = (e / (FH_ * wr)) % ho;
+        const int64_t plane = e / (FH_ * wr * ho);     /* i*C + r */
+        const int64_t yy = m * SH_ + u - PH_;          /* row in the unpadded input */
+        const int64_t xx = k - PW_;                    /* column in the unpadded input */
+        if (yy >= 0 && yy < H_ && xx >= 0 && xx < W_)
+            memcpy(dst + (size_t)e * eb, src + (size_t)((plane * H_ + yy) * W_ + xx) * eb, eb);
+        else
+            memset(dst + (size_t)e * eb, 0, eb);
+    }
 }
 
 /* One output of the convolution, Eq. 1 with padding:
@@ -159,29 +161,32 @@ void oracle_direct_conv_at(const int64_t *shp, const double *x, const double *w,
     }
 }
 
-/* Basic im2win-based convolution (Alg. 2) evaluated on a window tensor `win`
- * (N x C x Ho x Wr*Fh, as produced by the transformation):
+/* The im2win-based convolution (Alg. 2's definition of an output) evaluated
+ * on a window tensor `win` (N x C x Ho x Wr*Fh, as the transformation writes
+ * it), each output computed from its flat NCHW index o = ((i*K + j)*Ho + m)*Wo + n:
  *   O[i][j][m][n] = sum_r sum_u sum_v win[i][r][m][(n*sw + v)*Fh + u] * F[j][r][u][v]
- * The window of output column n begins at input column n*sw, which sits at
- * offset n*sw*Fh of the row. */
+ * summed in fp64 in the order r, u, v.  The window of output column n begins
+ * at input column n*sw, which sits at offset n*sw*Fh of the row. */
 void oracle_window_conv(const int64_t *shp, const double *win, const double *w, double *y,
                         int trimmed) {
     const int64_t ho = oracle_out_extent(H_, FH_, SH_, PH_);
     const int64_t wo = oracle_out_extent(W_, FW_, SW_, PW_);
     const int64_t row = oracle_row_width(shp, trimmed) * FH_;
-#pragma omp parallel for collapse(2) schedule(dynamic)
-    for (int64_t i = 0; i < N_; ++i)
-        for (int64_t j = 0; j < K_; ++j)
-            for (int64_t m = 0; m < ho; ++m)
-                for (int64_t n = 0; n < wo; ++n) {
-                    double acc = 0.0;
-                    for (int64_t r = 0; r < C_; ++r)
-                        for (int64_t u = 0; u < FH_; ++u)
-                            for (int64_t v = 0; v < FW_; ++v)
-                                acc += win[((i * C_ + r) * ho + m) * row + (n * SW_ + v) * FH_ + u]
-                                     * w[((j * C_ + r) * FH_ + u) * FW_ + v];
-                    y[((i * K_ + j) * ho + m) * wo + n] = acc;
-                }
+    const int64_t total = N_ * K_ * ho * wo;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t o = 0; o < total; ++o) {
+        const int64_t n = o % wo;
+        const int64_t m = (o / wo) % ho;
+        const int64_t j = (o / (wo * ho)) % K_;
+        const int64_t i = o / (wo * ho * K_);
+        double acc = 0.0;
+        for (int64_t r = 0; r < C_; ++r)
+            for (int64_t u = 0; u < FH_; ++u)
+                for (int64_t v = 0; v < FW_; ++v)
+                    acc += win[((i * C_ + r) * ho + m) * row + (n * SW_ + v) * FH_ + u]
+                         * w[((j * C_ + r) * FH_ + u) * FW_ + v];
+        y[o] = acc;
+    }
 }
 
 /* Brute-force im2col (Sec. II-B): for each image a (Ho*Wo) x (C*Fh*Fw) matrix
