@@ -123,16 +123,19 @@ def run_workload(wl, steps, warmup, with_cpu):
     x = workloads.make_input(wl).to(dev)
     w = workloads.make_filter(wl).to(dev)
     ws = torch.empty(P.workspace_shape(d), dtype=x.dtype, device=dev)
+    scratch_bytes = P.im2win_filter_scratch_bytes(d)
+    scratch = torch.empty(max(scratch_bytes, 16), dtype=torch.uint8, device=dev)
     y = torch.empty((wl.n, wl.k, ho, wo), dtype=torch.float32, device=dev)
     y2 = torch.empty_like(y)
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     xp, wp, wsp, yp, y2p = x.data_ptr(), w.data_ptr(), ws.data_ptr(), y.data_ptr(), y2.data_ptr()
+    scp = scratch.data_ptr()
 
     launch = {
         "transform": lambda: P.im2win_transform(d, xp, wsp, ws_bytes, sp),
-        "conv2d": lambda: P.im2win_conv2d(d, wsp, ws_bytes, wp, yp, sp),
-        "conv2d_fused": lambda: P.im2win_conv2d_fused(d, xp, wp, y2p, sp),
+        "conv2d": lambda: P.im2win_conv2d(d, wsp, ws_bytes, wp, scp, scratch_bytes, yp, sp),
+        "conv2d_fused": lambda: P.im2win_conv2d_fused(d, xp, wp, scp, scratch_bytes, y2p, sp),
     }
 
     def step():
@@ -298,11 +301,15 @@ def profile_call(wl, call, steps, warmup):
     x = workloads.make_input(wl).to(dev)
     w = workloads.make_filter(wl).to(dev)
     ws = torch.empty(P.workspace_shape(d), dtype=x.dtype, device=dev)
+    sb = P.im2win_filter_scratch_bytes(d)
+    scratch = torch.empty(max(sb, 16), dtype=torch.uint8, device=dev)
     y = torch.empty((wl.n, wl.k, ho, wo), dtype=torch.float32, device=dev)
     sp = torch.cuda.current_stream().cuda_stream
     fn = {"transform": lambda: P.im2win_transform(d, x.data_ptr(), ws.data_ptr(), ws_bytes, sp),
-          "conv2d": lambda: P.im2win_conv2d(d, ws.data_ptr(), ws_bytes, w.data_ptr(), y.data_ptr(), sp),
-          "conv2d_fused": lambda: P.im2win_conv2d_fused(d, x.data_ptr(), w.data_ptr(), y.data_ptr(), sp)}[call]
+          "conv2d": lambda: P.im2win_conv2d(d, ws.data_ptr(), ws_bytes, w.data_ptr(), scratch.data_ptr(), sb,
+                                            y.data_ptr(), sp),
+          "conv2d_fused": lambda: P.im2win_conv2d_fused(d, x.data_ptr(), w.data_ptr(), scratch.data_ptr(), sb,
+                                                        y.data_ptr(), sp)}[call]
     if call == "conv2d":
         P.im2win_transform(d, x.data_ptr(), ws.data_ptr(), ws_bytes, sp)
     torch.cuda.synchronize()

@@ -21,24 +21,15 @@
  *  - Padding is symmetric zero padding (not in the paper; the convolution is
  *    the one of PyTorch's conv2d with these strides and paddings, no bias, no
  *    dilation, no groups).
- *  - Device pointers (x, w, ws, y) are owned by the caller.  Each must be
- *    16-byte aligned and the buffers must not overlap.  The only device
- *    memory the library holds itself: some convolutions first rewrite w into
- *    the order their kernels copy to on-chip memory -- bf16 ones that run on
- *    the fast kernels (C a multiple of 16, K a multiple of 64, filter 3x3, 3x5
- *    or 1x1, among other shape conditions; K*C*Fh*Fw*2 bytes), and fp32 ones
- *    whose per-chunk filter rows are not whole 16-byte vectors (C*Fh*Fw
- *    floats per output channel rounded up to the kernel's tile and row
- *    stride, about K*C*Fh*Fw*4 bytes) -- in a buffer that
- *    the library keeps per stream (the default stream once per device),
- *    taken from the device's stream-ordered memory pool (hipMallocAsync on
- *    that stream) and replaced, stream-ordered, only when a larger filter
- *    needs more; it is held until the process ends.  A failed allocation is
- *    EHIP.
+ *  - Device pointers (x, w, ws, scratch, y) are owned by the caller; the
+ *    library never allocates, frees or keeps device memory.  Each pointer
+ *    must be 16-byte aligned and the buffers must not overlap.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Calls only
- *    enqueue work: they never synchronise and may be made from several host
- *    threads at once; apart from the per-stream filter buffer above they hold
- *    no state between calls.
+ *    enqueue work: they never synchronise and hold no state between calls,
+ *    so they may be made from several host threads at once.  Buffers a call
+ *    writes (ws, scratch, y) must not be in use by other work that may run
+ *    concurrently with it (another stream, another thread's call): calls on
+ *    one stream may share them, since the stream orders them.
  *  - Return value: IM2WIN_OK or a negative IM2WIN_E* code.  Arguments are
  *    validated on the host before any HIP call, so an invalid call enqueues
  *    nothing.  im2win_last_error() then describes the failure.
@@ -93,7 +84,7 @@ enum {
     IM2WIN_OK = 0,
     IM2WIN_EINVAL = -1,      /* bad shape, stride, padding, dtype, layout, or Ho/Wo < 1 */
     IM2WIN_ENULL = -2,       /* a required pointer is NULL */
-    IM2WIN_EWORKSPACE = -3,  /* ws_bytes is smaller than im2win_workspace_bytes() */
+    IM2WIN_EWORKSPACE = -3,  /* ws_bytes or scratch_bytes is smaller than the call needs */
     IM2WIN_EHIP = -4,        /* the HIP runtime reported an error at launch */
     IM2WIN_EOVERFLOW = -5,   /* a size exceeds what the kernels index */
     IM2WIN_EALIGN = -6       /* a device pointer is not 16-byte aligned */
@@ -123,6 +114,32 @@ int im2win_im2col_bytes(const im2win_desc* d, size_t* bytes);
 int im2win_output_shape(const im2win_desc* d, int64_t* ho, int64_t* wo);
 
 /*
+ * Shape of the window tensor (Sec. III-A: N x C x Ho x (Wi*Hf), with the row
+ * width Wr of d->layout in place of Wi): dims[0..3] = N, C, Ho, Wr*Fh, in
+ * elements of d->dtype.  Host only; `dims` points to 4 int64_t.
+ * Errors: EINVAL, ENULL, EOVERFLOW.
+ */
+int im2win_workspace_shape(const im2win_desc* d, int64_t* dims);
+
+/*
+ * Size in bytes of the filter scratch that im2win_conv2d and
+ * im2win_conv2d_fused take for this descriptor (0 when neither needs one).
+ * Alg. 3 reads the filter transposed, F[j][r][v][u], so that a filter row
+ * follows the window order (v*Fh + u) of the window tensor; the matrix-core
+ * kernels go further and copy the filter to on-chip memory in the order of
+ * their reduction.  For the shapes where the filter rows are not whole
+ * 16-byte vectors in that order (fp32: C*Fh*Fw per tile chunk not a multiple
+ * of 4 floats), and for the bf16 kernels that stage 8-channel pieces
+ * (C a multiple of 16, K a multiple of the tile, 3x3, 3x5 or 1x1 filters),
+ * each convolution call first rewrites w into the scratch in that order and
+ * the kernels read it from there.  The size is at most about
+ * K*C*Fh*Fw*sizeof(dtype), padded to the kernels' tile.  The same buffer may
+ * serve both entry points and every call with this descriptor.
+ * Host only.  Errors: EINVAL, ENULL, EOVERFLOW.
+ */
+int im2win_filter_scratch_bytes(const im2win_desc* d, size_t* bytes);
+
+/*
  * The im2win transformation (Alg. 1, Eq. 2) with zero padding:
  *   ws[i][r][m][k*Fh + u] = x[i][r][m*stride_h + u - pad_h][k - pad_w]
  * for k < Wr, u < Fh, and +0 where the source lies in the padding.  Each row
@@ -146,25 +163,31 @@ int im2win_transform(const im2win_desc* d, const void* x, void* ws, size_t ws_by
  * starts at input column n*stride_w, i.e. at n*stride_w*Fh in the row, which
  * is the same for the square filters the paper evaluates.)
  * y is overwritten (not accumulated into).  Products and sums are fp32 on
- * the matrix cores, for both dtypes.
- *   ws  device, the window tensor of x for this descriptor (read only)
- *   w   device, K x C x Fh x Fw, dtype d->dtype (read only)
- *   y   device, N x K x Ho x Wo fp32 (written)
- * Errors: EINVAL, ENULL, EALIGN, EWORKSPACE, EOVERFLOW, EHIP.
+ * the matrix cores, for both dtypes.  Shapes whose window strips no on-chip
+ * tile holds (rows of very many columns with few output columns) run on a
+ * kernel with one thread per output instead, with the same definition.
+ *   ws       device, the window tensor of x for this descriptor (read only)
+ *   w        device, K x C x Fh x Fw, dtype d->dtype (read only)
+ *   scratch  device, scratch_bytes >= im2win_filter_scratch_bytes() (written:
+ *            the repacked filter); may be NULL when that size is 0
+ *   y        device, N x K x Ho x Wo fp32 (written)
+ * Errors: EINVAL, ENULL, EALIGN, EWORKSPACE (ws or scratch too small),
+ * EOVERFLOW, EHIP.
  */
 int im2win_conv2d(const im2win_desc* d, const void* ws, size_t ws_bytes, const void* w,
-                  float* y, void* stream);
+                  void* scratch, size_t scratch_bytes, float* y, void* stream);
 
 /*
  * The same convolution computed straight from x: each workgroup builds the
  * window-tensor rows it needs in on-chip memory (LDS) and never writes the
  * window tensor to device memory, so no workspace is needed.  Same result
  * definition, accumulation and output as im2win_conv2d.
- *   x   device, N x C x H x W (read only); w as above; y as above (written)
- * Errors: EINVAL, ENULL, EALIGN, EOVERFLOW, EHIP.
+ *   x        device, N x C x H x W (read only); w, scratch, y as above
+ * Errors: EINVAL, ENULL, EALIGN, EWORKSPACE (scratch too small), EOVERFLOW,
+ * EHIP.
  */
-int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, float* y,
-                        void* stream);
+int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, void* scratch,
+                        size_t scratch_bytes, float* y, void* stream);
 
 /*
  * Message for the last failed call on this host thread ("" if none).  The

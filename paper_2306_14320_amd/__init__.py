@@ -4,8 +4,9 @@ Python binding of ``libim2win.so`` (C ABI in ``include/im2win.h``).  The
 functions named ``im2win_*`` mirror the C entry points one to one and only
 marshal arguments; every step of the computation runs in the HIP kernels.
 The tensor helpers below them (``desc_for``, ``transform``, ``conv2d``,
-``conv2d_fused``) use PyTorch only to allocate device memory and to pick the
-current HIP stream.
+``conv2d_fused``) check that the tensors match the descriptor and use PyTorch
+only to allocate device memory (window tensor, filter scratch, output) on the
+call's HIP stream.
 
 There is no fallback: if the library is missing or was built for another
 target, loading fails with an error.  Build it with
@@ -67,14 +68,19 @@ def load_library():
         raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                            "`python -m paper_2306_14320_amd.build` (hipcc, gfx950)")
     lib = ctypes.CDLL(LIB_PATH)
+    runtimes = hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise RuntimeError("libim2win bound a second HIP runtime next to torch's: " + ", ".join(runtimes))
     P, D, SZ, I64P = ctypes.c_void_p, ctypes.POINTER(im2win_desc), ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64)
     sigs = {
         "im2win_workspace_bytes": [D, ctypes.POINTER(SZ)],
         "im2win_im2col_bytes": [D, ctypes.POINTER(SZ)],
         "im2win_output_shape": [D, I64P, I64P],
+        "im2win_workspace_shape": [D, I64P],
+        "im2win_filter_scratch_bytes": [D, ctypes.POINTER(SZ)],
         "im2win_transform": [D, P, P, SZ, P],
-        "im2win_conv2d": [D, P, SZ, P, P, P],
-        "im2win_conv2d_fused": [D, P, P, P, P],
+        "im2win_conv2d": [D, P, SZ, P, P, SZ, P, P],
+        "im2win_conv2d_fused": [D, P, P, P, SZ, P, P],
         "im2win_direct_conv2d": [D, P, P, P, P],
         "im2win_selftest": [],
         "im2win_check_plan": [D],
@@ -87,6 +93,17 @@ def load_library():
     lib.im2win_last_error.restype = ctypes.c_char_p
     _lib = lib
     return lib
+
+
+def hip_runtimes_mapped():
+    """Distinct HIP runtime libraries (libamdhip64) mapped into this process.
+    libim2win must bind to the one torch loaded (it is imported first), never
+    to a second copy with its own device state."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({l.split()[-1] for l in f if "libamdhip64" in l})
+    except OSError:
+        return []
 
 
 def _check(rc):
@@ -116,16 +133,32 @@ def im2win_output_shape(desc: im2win_desc):
     return ho.value, wo.value
 
 
+def im2win_workspace_shape(desc: im2win_desc):
+    dims = (ctypes.c_int64 * 4)()
+    _check(load_library().im2win_workspace_shape(ctypes.byref(desc), dims))
+    return tuple(dims)
+
+
+def im2win_filter_scratch_bytes(desc: im2win_desc) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().im2win_filter_scratch_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
 def im2win_transform(desc: im2win_desc, x: int, ws: int, ws_bytes: int, stream: int) -> None:
     _check(load_library().im2win_transform(ctypes.byref(desc), x, ws, ws_bytes, stream))
 
 
-def im2win_conv2d(desc: im2win_desc, ws: int, ws_bytes: int, w: int, y: int, stream: int) -> None:
-    _check(load_library().im2win_conv2d(ctypes.byref(desc), ws, ws_bytes, w, y, stream))
+def im2win_conv2d(desc: im2win_desc, ws: int, ws_bytes: int, w: int, scratch: int,
+                  scratch_bytes: int, y: int, stream: int) -> None:
+    _check(load_library().im2win_conv2d(ctypes.byref(desc), ws, ws_bytes, w, scratch, scratch_bytes,
+                                        y, stream))
 
 
-def im2win_conv2d_fused(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
-    _check(load_library().im2win_conv2d_fused(ctypes.byref(desc), x, w, y, stream))
+def im2win_conv2d_fused(desc: im2win_desc, x: int, w: int, scratch: int, scratch_bytes: int,
+                        y: int, stream: int) -> None:
+    _check(load_library().im2win_conv2d_fused(ctypes.byref(desc), x, w, scratch, scratch_bytes, y,
+                                              stream))
 
 
 def im2win_direct_conv2d(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
@@ -174,65 +207,120 @@ def desc_for(x_shape, w_shape, stride=1, padding=0, dtype=torch.float32,
                        IM2WIN_ROWS_PADDED if layout is None else layout)
 
 
+def _torch_stream(stream):
+    """The torch stream a call runs on (the current one when None)."""
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
 def _stream(stream):
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _dev(t, name):
-    if not t.is_cuda or not t.is_contiguous():
+def _dev(t, name, shape=None, dtype=None):
+    """Device pointer of t, after checking that it is a contiguous device
+    tensor of the given shape and dtype (the C ABI receives no tensor sizes,
+    so a mismatch here would make the kernels read or write out of bounds)."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous device tensor")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, the descriptor needs {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, the descriptor needs {dtype}")
     return t.data_ptr()
 
 
-def row_width(desc: im2win_desc) -> int:
-    """Columns per window-tensor row: Wp, or (Wo-1)*stride_w + Fw when trimmed."""
-    _, wo = im2win_output_shape(desc)
-    if desc.layout == IM2WIN_ROWS_TRIMMED:
-        return (wo - 1) * desc.stride_w + desc.fw
-    return desc.w + 2 * desc.pad_w
+def _dtype_of(desc):
+    return torch.float32 if desc.dtype == IM2WIN_F32 else torch.bfloat16
+
+
+def x_shape(desc: im2win_desc):
+    return (desc.n, desc.c, desc.h, desc.w)
+
+
+def w_shape(desc: im2win_desc):
+    return (desc.k, desc.c, desc.fh, desc.fw)
+
+
+def y_shape(desc: im2win_desc):
+    ho, wo = im2win_output_shape(desc)
+    return (desc.n, desc.k, ho, wo)
 
 
 def workspace_shape(desc: im2win_desc):
-    ho, _ = im2win_output_shape(desc)
-    return (desc.n, desc.c, ho, row_width(desc) * desc.fh)
+    """N x C x Ho x Wr*Fh (im2win_workspace_shape)."""
+    return im2win_workspace_shape(desc)
+
+
+def filter_scratch(desc: im2win_desc, device, stream=None) -> torch.Tensor:
+    """A device buffer of im2win_filter_scratch_bytes() bytes (may be empty),
+    allocated on the call's stream."""
+    nbytes = im2win_filter_scratch_bytes(desc)
+    with torch.cuda.stream(_torch_stream(stream)):
+        return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+
+
+def _scratch_args(desc, scratch, device, stream):
+    need = im2win_filter_scratch_bytes(desc)
+    if need == 0 and scratch is None:
+        return None, 0, 0
+    if scratch is None:
+        scratch = filter_scratch(desc, device, stream)
+    p = _dev(scratch, "scratch")
+    return scratch, p, scratch.numel() * scratch.element_size()
 
 
 def transform(x: torch.Tensor, desc: im2win_desc, ws: torch.Tensor = None, stream=None) -> torch.Tensor:
-    """Window tensor of x (N x C x Ho x Wp*Fh, dtype of x)."""
+    """Window tensor of x (N x C x Ho x Wr*Fh, dtype of x)."""
+    xp = _dev(x, "x", x_shape(desc), _dtype_of(desc))
     if ws is None:
-        ws = torch.empty(workspace_shape(desc), dtype=x.dtype, device=x.device)
-    im2win_transform(desc, _dev(x, "x"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+        with torch.cuda.stream(_torch_stream(stream)):
+            ws = torch.empty(workspace_shape(desc), dtype=x.dtype, device=x.device)
+    im2win_transform(desc, xp, _dev(ws, "ws", dtype=_dtype_of(desc)), ws.numel() * ws.element_size(),
+                     _stream(stream))
     return ws
 
 
-def conv2d(ws: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
-           stream=None) -> torch.Tensor:
-    """Convolution from a window tensor; returns y (N x K x Ho x Wo, fp32)."""
-    ho, wo = im2win_output_shape(desc)
+def _output(y, desc, device, stream):
     if y is None:
-        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=ws.device)
-    im2win_conv2d(desc, _dev(ws, "ws"), ws.numel() * ws.element_size(), _dev(w, "w"),
-                  _dev(y, "y"), _stream(stream))
+        with torch.cuda.stream(_torch_stream(stream)):
+            y = torch.empty(y_shape(desc), dtype=torch.float32, device=device)
+    return y, _dev(y, "y", y_shape(desc), torch.float32)
+
+
+def conv2d(ws: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
+           stream=None, scratch: torch.Tensor = None) -> torch.Tensor:
+    """Convolution from a window tensor; returns y (N x K x Ho x Wo, fp32).
+    `scratch` is the filter scratch (allocated per call when None)."""
+    wsp = _dev(ws, "ws", dtype=_dtype_of(desc))
+    wp = _dev(w, "w", w_shape(desc), _dtype_of(desc))
+    y, yp = _output(y, desc, ws.device, stream)
+    scratch, sp, sbytes = _scratch_args(desc, scratch, ws.device, stream)
+    im2win_conv2d(desc, wsp, ws.numel() * ws.element_size(), wp, sp, sbytes, yp, _stream(stream))
     return y
 
 
 def conv2d_fused(x: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
-                 stream=None) -> torch.Tensor:
+                 stream=None, scratch: torch.Tensor = None) -> torch.Tensor:
     """Convolution straight from x (window strips built on chip); returns y."""
-    ho, wo = im2win_output_shape(desc)
-    if y is None:
-        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=x.device)
-    im2win_conv2d_fused(desc, _dev(x, "x"), _dev(w, "w"), _dev(y, "y"), _stream(stream))
+    xp = _dev(x, "x", x_shape(desc), _dtype_of(desc))
+    wp = _dev(w, "w", w_shape(desc), _dtype_of(desc))
+    y, yp = _output(y, desc, x.device, stream)
+    scratch, sp, sbytes = _scratch_args(desc, scratch, x.device, stream)
+    im2win_conv2d_fused(desc, xp, wp, sp, sbytes, yp, _stream(stream))
     return y
 
 
 def direct_conv2d(x: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
                   stream=None) -> torch.Tensor:
     """Comparison baseline: direct convolution (no data transformation); returns y."""
-    ho, wo = im2win_output_shape(desc)
-    if y is None:
-        y = torch.empty((desc.n, desc.k, ho, wo), dtype=torch.float32, device=x.device)
-    im2win_direct_conv2d(desc, _dev(x, "x"), _dev(w, "w"), _dev(y, "y"), _stream(stream))
+    xp = _dev(x, "x", x_shape(desc), _dtype_of(desc))
+    wp = _dev(w, "w", w_shape(desc), _dtype_of(desc))
+    y, yp = _output(y, desc, x.device, stream)
+    im2win_direct_conv2d(desc, xp, wp, yp, _stream(stream))
     return y

@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libim2win.so")
-SOURCES = ["api.hip", "transform.hip", "conv_f32.hip", "conv_bf16.hip", "check.hip", "direct.hip"]
+SOURCES = ["api.hip", "transform.hip", "conv_f32.hip", "conv_bf16.hip", "conv_plain.hip", "check.hip", "direct.hip"]
 ARCH = "gfx950"
 
 
@@ -23,7 +23,7 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (needs ROCm with gfx950 support)")
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
+def build(verbose: bool = False, jobs: int = 8) -> str:
     """Compile every HIP source for gfx950 and link libim2win.so; returns its path."""
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)

@@ -4,6 +4,7 @@
 #include "im2win.h"
 #include "im2win_baseline.h"
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -163,8 +164,51 @@ int im2win_transform(const im2win_desc* d, const void* x, void* ws, size_t ws_by
     return after_launch(rc, "transform", msg);
 }
 
-int im2win_conv2d(const im2win_desc* d, const void* ws, size_t ws_bytes, const void* w, float* y,
-                  void* stream) {
+int im2win_filter_scratch_bytes(const im2win_desc* d, size_t* bytes) {
+    im2win::Geometry g;
+    int rc = geometry(d, &g);
+    if (rc) return rc;
+    if (!bytes) return fail(IM2WIN_ENULL, "bytes is NULL");
+    const int64_t a = im2win::conv_scratch_bytes(g, false), b = im2win::conv_scratch_bytes(g, true);
+    *bytes = (size_t)std::max<int64_t>(0, std::max(a, b));
+    return ok();
+}
+
+int im2win_workspace_shape(const im2win_desc* d, int64_t* dims) {
+    im2win::Geometry g;
+    int rc = geometry(d, &g);
+    if (rc) return rc;
+    if (!dims) return fail(IM2WIN_ENULL, "dims is NULL");
+    dims[0] = g.n;
+    dims[1] = g.c;
+    dims[2] = g.ho;
+    dims[3] = g.row_len;
+    return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+// The filter scratch a convolution variant needs: checked against the
+// caller's buffer (NULL is accepted when none is needed).
+int check_scratch(const im2win::Geometry& g, bool fused, const void* scratch, size_t scratch_bytes) {
+    const int64_t need = im2win::conv_scratch_bytes(g, fused);
+    if (need <= 0) return IM2WIN_OK;
+    int rc = check_ptr(scratch, "scratch");
+    if (rc) return rc;
+    if (scratch_bytes < (size_t)need)
+        return fail(IM2WIN_EWORKSPACE, "filter scratch holds %zu bytes, this convolution needs %lld",
+                    scratch_bytes, (long long)need);
+    return IM2WIN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int im2win_conv2d(const im2win_desc* d, const void* ws, size_t ws_bytes, const void* w,
+                  void* scratch, size_t scratch_bytes, float* y, void* stream) {
     im2win::Geometry g;
     int rc = geometry(d, &g);
     if (rc) return rc;
@@ -175,24 +219,26 @@ int im2win_conv2d(const im2win_desc* d, const void* ws, size_t ws_bytes, const v
     if (ws_bytes < need)
         return fail(IM2WIN_EWORKSPACE, "workspace holds %zu bytes, the window tensor needs %zu",
                     ws_bytes, need);
+    if ((rc = check_scratch(g, false, scratch, scratch_bytes))) return rc;
     char msg[256] = "";
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = g.elem == 4 ? im2win::launch_conv_f32(g, false, ws, w, y, s, msg, sizeof msg)
-                     : im2win::launch_conv_bf16(g, false, ws, w, y, s, msg, sizeof msg);
+    rc = g.elem == 4 ? im2win::launch_conv_f32(g, false, ws, w, scratch, y, s, msg, sizeof msg)
+                     : im2win::launch_conv_bf16(g, false, ws, w, scratch, y, s, msg, sizeof msg);
     return after_launch(rc, "conv2d", msg);
 }
 
-int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, float* y,
-                        void* stream) {
+int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, void* scratch,
+                        size_t scratch_bytes, float* y, void* stream) {
     im2win::Geometry g;
     int rc = geometry(d, &g);
     if (rc) return rc;
     if ((rc = check_ptr(x, "x")) || (rc = check_ptr(w, "w")) || (rc = check_ptr(y, "y")))
         return rc;
+    if ((rc = check_scratch(g, true, scratch, scratch_bytes))) return rc;
     char msg[256] = "";
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = g.elem == 4 ? im2win::launch_conv_f32(g, true, x, w, y, s, msg, sizeof msg)
-                     : im2win::launch_conv_bf16(g, true, x, w, y, s, msg, sizeof msg);
+    rc = g.elem == 4 ? im2win::launch_conv_f32(g, true, x, w, scratch, y, s, msg, sizeof msg)
+                     : im2win::launch_conv_bf16(g, true, x, w, scratch, y, s, msg, sizeof msg);
     return after_launch(rc, "conv2d_fused", msg);
 }
 

@@ -414,6 +414,12 @@ void check_packed_filter(const Geometry& g, const ConvPlan& p, Report& r) {
         return;
     }
     const int64_t npieces = g.k * g.c * T / 8;
+    if (npieces * 16 > conv_scratch_bytes(g, false) && npieces * 16 > conv_scratch_bytes(g, true)) {
+        r.fail("conv: filter scratch of %lld bytes, the packed filter needs %lld",
+               (long long)std::max(conv_scratch_bytes(g, false), conv_scratch_bytes(g, true)),
+               (long long)(npieces * 16));
+        return;
+    }
     if (npieces != (g.k / bm) * (int64_t)nchunks * pieces) {
         r.fail("conv: %lld packed pieces, blocks hold %lld", (long long)npieces,
                (long long)((g.k / bm) * nchunks * pieces));
@@ -448,10 +454,9 @@ void check_packed_filter(const Geometry& g, const ConvPlan& p, Report& r) {
 
 void check_conv(const Geometry& g, bool fused_plan, Report& r) {
     const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused_plan) : plan_conv_f32(g);
-    if (p.kind == ConvPlan::kNone) {
-        r.fail("conv: no tile configuration fits in LDS (the launch would be refused)");
-        return;
-    }
+    // no tile fits in LDS: the per-output kernel runs instead, which indexes
+    // every operand directly (no LDS, no plan)
+    if (p.kind == ConvPlan::kNone) return;
     const bool bf16 = p.kind == ConvPlan::kBf16Lds;
     if (p.lds_bytes > kConvLdsMaxBytes)
         r.fail("conv: plan uses %lld bytes of LDS", (long long)p.lds_bytes);
@@ -480,6 +485,11 @@ void check_conv(const Geometry& g, bool fused_plan, Report& r) {
                 (int64_t)p.bm * p.fp > p.stage - p.rc * p.sc)
                 r.fail("conv: repacked filter blocks of %lld floats do not fit the stage (fp %lld)",
                        (long long)(p.bm * p.fp), (long long)p.fp);
+            // the caller's scratch (conv_scratch_bytes) holds every block
+            const int64_t need = (blk_last + 1) * p.bm * p.fp * 4;
+            if (conv_scratch_bytes(g, false) < need || conv_scratch_bytes(g, true) < need)
+                r.fail("conv: filter scratch of %lld bytes, the repacked filter needs %lld",
+                       (long long)conv_scratch_bytes(g, false), (long long)need);
         }
         if (conv_args_f32(g, p, nullptr, nullptr, nullptr, false).ilv &&
             (!p.fvec || p.bm * (p.fp / 4) > (int64_t)kConvThreads * kIlvSlots))

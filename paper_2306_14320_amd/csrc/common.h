@@ -134,10 +134,23 @@ int launch_transform(const Geometry& g, const void* x, void* ws, hipStream_t str
 // Convolution kernels.  `fused` selects where the window strips come from:
 // false -> the window tensor `src`; true -> the input tensor `src`.
 // ---------------------------------------------------------------------------
-int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, float* y,
-                    hipStream_t stream, char* err, size_t errlen);
-int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, float* y,
-                     hipStream_t stream, char* err, size_t errlen);
+// `scratch` (device, caller-owned) receives the repacked filter when the
+// plan reads one; it holds at least conv_scratch_bytes(g, fused) bytes.
+int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
+                    float* y, hipStream_t stream, char* err, size_t errlen);
+int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
+                     float* y, hipStream_t stream, char* err, size_t errlen);
+
+// Bytes of device scratch (the repacked filter) the tiled convolution of
+// this geometry needs, 0 when its kernels read w as given; -1 when no tile
+// fits in LDS, in which case launch_conv_plain computes the convolution.
+int64_t conv_scratch_bytes(const Geometry& g, bool fused);
+
+// One thread per output, reading the window tensor (or x, fused) and the
+// filter straight from device memory: the convolution of any shape whose
+// window strips do not fit the tiled kernels' LDS.
+int launch_conv_plain(const Geometry& g, bool fused, const void* src, const void* w, float* y,
+                      hipStream_t stream, char* err, size_t errlen);
 
 // Host-side bounds check of the launch plans (see im2win_check_plan).
 // Returns the number of violations; the first is described in `msg`.

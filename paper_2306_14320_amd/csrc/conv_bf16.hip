@@ -33,8 +33,6 @@
 #include "conv_common.h"
 
 #include <cstdio>
-#include <map>
-#include <mutex>
 #include <utility>
 
 namespace im2win {
@@ -1162,52 +1160,19 @@ int bf16_strip_mode(const ConvPlan& p, bool fused) {
 // The fast kernels read the filter packed (packed_piece).
 bool bf16_packed(const ConvPlan& p, bool fused) { return fused ? p.fused_fast != 0 : p.fast != 0; }
 
-// One packed-filter buffer per stream (the legacy default stream counted once
-// per device), from the stream-ordered memory pool.  A call reuses its
-// stream's buffer, so steady-state calls enqueue no pool operations; a larger
-// filter replaces it by a stream-ordered free and allocation, after the work
-// already enqueued on the stream.  Calls on one stream are ordered, so they
-// never overwrite a buffer another call is still reading.
-struct PackBuffers {
-    std::mutex mu;
-    std::map<std::pair<int, hipStream_t>, std::pair<void*, size_t>> bufs;
-};
-
-hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out) {
-    static PackBuffers pb;
-    int dev = -1;
-    if (stream == nullptr) {
-        const hipError_t e = hipGetDevice(&dev);
-        if (e != hipSuccess) return e;
-    }
-    std::lock_guard<std::mutex> lock(pb.mu);
-    auto& slot = pb.bufs[{dev, stream}];
-    if (slot.second < bytes) {
-        if (slot.first) {
-            const hipError_t e = hipFreeAsync(slot.first, stream);
-            slot = {nullptr, 0};
-            if (e != hipSuccess) return e;
-        }
-        void* p = nullptr;
-        const hipError_t e = hipMallocAsync(&p, bytes, stream);
-        if (e != hipSuccess) return e;
-        slot = {p, bytes};
-    }
-    *out = slot.first;
-    return hipSuccess;
+int64_t conv_scratch_bytes(const Geometry& g, bool fused) {
+    const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused) : plan_conv_f32(g);
+    if (p.kind == ConvPlan::kNone) return -1;
+    if (p.kind == ConvPlan::kF32Lds) return filter_scratch_f32(g, p);
+    return bf16_packed(p, fused) ? g.k * g.c * g.taps * 2 : 0;
 }
 
-int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, float* y,
-                     hipStream_t stream, char* err, size_t errlen) {
+int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
+                     float* y, hipStream_t stream, char* err, size_t errlen) {
     const ConvPlan p = plan_conv_bf16(g, fused);
-    if (p.kind == ConvPlan::kNone) {
-        snprintf(err, errlen,
-                 "conv: the window strips of one tile (row length %lld) do not fit in LDS; "
-                 "this shape is not supported", (long long)g.row_len);
-        return -5;
-    }
+    if (p.kind == ConvPlan::kNone) return launch_conv_plain(g, fused, src, w, y, stream, err, errlen);
     if (p.kind == ConvPlan::kF32Lds)
-        return launch_conv_f32_plan(g, p, fused, src, w, y, stream, err, errlen);
+        return launch_conv_f32_plan(g, p, fused, src, w, scratch, y, stream, err, errlen);
     ConvArgs a = conv_args_bf16(g, p, src, w, y, fused);
     const int64_t blocks = ((g.npix + p.bn - 1) / p.bn) * a.num_jtiles;
     if (blocks > 0x7fffffff) {
@@ -1215,21 +1180,14 @@ int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void*
         return -5;
     }
     const int smode = bf16_strip_mode(p, fused);
-    void* wpack = nullptr;
     if (bf16_packed(p, fused)) {
-        // the filter, repacked for 16-byte DMA, in the stream's buffer
-        const int64_t npieces = g.k * g.c * g.taps / 8;
-        const hipError_t e = packed_filter_buffer(stream, (size_t)npieces * 16, &wpack);
-        if (e != hipSuccess) {
-            snprintf(err, errlen, "conv: packed-filter buffer of %lld bytes: %s", (long long)npieces * 16,
-                     hipGetErrorString(e));
-            return -4;
-        }
+        // the filter, repacked for 16-byte copies, into the caller's scratch
+        // (K*C*Fh*Fw*2 bytes)
         const int64_t nchunks = g.c / kRC;
         hipLaunchKernelGGL(pack_filter_bf16_kernel, dim3((unsigned)(g.k / kPackRows * nchunks)), dim3(256),
                            (size_t)kPackRows * kRC * g.taps * 2, stream, static_cast<const uint16_t*>(w),
-                           static_cast<uint16_t*>(wpack), (int)g.c, (int)g.fh, (int)g.fw, p.bm, (int)nchunks);
-        a.w = wpack;
+                           static_cast<uint16_t*>(scratch), (int)g.c, (int)g.fh, (int)g.fw, p.bm, (int)nchunks);
+        a.w = scratch;
     }
     if (p.fvec && g.fh == 3 && g.fw == 3) launch_tile<3, 3, true>(p, a, blocks, smode, stream);
     else if (p.fvec && g.fh == 3 && g.fw == 5) launch_tile<3, 5, true>(p, a, blocks, smode, stream);

@@ -58,11 +58,6 @@ struct ConvArgs {
     int fpack;             // fp32: w is the filter repacked into chunk blocks (pack_filter_f32_kernel)
 };
 
-// Device buffer of at least `bytes` for a repacked filter, one per stream (the
-// legacy default stream once per device), taken from the stream-ordered pool
-// and replaced, stream-ordered, only when a larger one is needed; held until
-// the process ends.  Calls on one stream reuse it in stream order.
-hipError_t packed_filter_buffer(hipStream_t stream, size_t bytes, void** out);
 
 // Geometry of the window-tensor runs that one pixel tile reads (per channel).
 struct TileRuns {
@@ -331,7 +326,10 @@ constexpr int kBf16Spare = 64;        // spare positions at the end of every str
 constexpr int kBf16FusedItems = 2;    // fused kernel: at most this many raw items per thread (2 elements x 8 channels)
 constexpr int kIlvSlots = 8;          // fp32 copies issued inside the MFMA loop: per lane and channel / chunk
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
-                         const void* w, float* y, hipStream_t stream, char* err, size_t errlen);
+                         const void* w, void* scratch, float* y, hipStream_t stream, char* err,
+                         size_t errlen);
+// Bytes of the repacked filter an fp32-strip plan reads (0: w as given).
+int64_t filter_scratch_f32(const Geometry& g, const ConvPlan& p);
 
 struct TileCfg {
     int bm, bn;

@@ -1158,8 +1158,16 @@ ConvArgs conv_args_f32(const Geometry& g, const ConvPlan& p, const void* src, co
     return a;
 }
 
+int64_t filter_scratch_f32(const Geometry& g, const ConvPlan& p) {
+    if (g.elem != 4 || p.fvec) return 0;
+    const int64_t nchunks = (g.c + p.rc - 1) / p.rc;
+    const int64_t jtiles = (g.k + p.bm - 1) / p.bm;
+    return jtiles * nchunks * p.bm * p.fp * 4;
+}
+
 int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const void* src,
-                         const void* w, float* y, hipStream_t stream, char* err, size_t errlen) {
+                         const void* w, void* scratch, float* y, hipStream_t stream, char* err,
+                         size_t errlen) {
     ConvArgs a = conv_args_f32(g, p, src, w, y, fused);
     const int64_t blocks = ((g.npix + p.bn - 1) / p.bn) * a.num_jtiles;
     if (blocks > 0x7fffffff) {
@@ -1167,20 +1175,14 @@ int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const
         return -5;
     }
     if (a.fpack) {
+        // the filter, repacked into the caller's scratch (filter_scratch_f32 bytes)
         const int64_t nchunks = (g.c + p.rc - 1) / p.rc;
         const int64_t total = (int64_t)a.num_jtiles * nchunks * p.bm * p.fp;
-        void* wpack = nullptr;
-        const hipError_t e = packed_filter_buffer(stream, (size_t)total * 4, &wpack);
-        if (e != hipSuccess) {
-            snprintf(err, errlen, "conv: packed-filter buffer of %lld bytes: %s", (long long)total * 4,
-                     hipGetErrorString(e));
-            return -4;
-        }
         const int64_t pblocks = std::min<int64_t>((total + 255) / 256, 65536);
         hipLaunchKernelGGL(pack_filter_f32_kernel, dim3((unsigned)pblocks), dim3(256), 0, stream,
-                           static_cast<const float*>(w), static_cast<float*>(wpack), (int)g.k, (int)g.c,
+                           static_cast<const float*>(w), static_cast<float*>(scratch), (int)g.k, (int)g.c,
                            (int)g.taps, p.bm, p.rc, (int)p.fp, (int)nchunks, total);
-        a.w = wpack;
+        a.w = scratch;
     }
     if (g.elem == 2) launch_tile<uint16_t, 0, 0>(p, a, blocks, fused, stream);
     else if (g.fh == 3 && g.fw == 3) launch_tile<float, 3, 3>(p, a, blocks, fused, stream);
@@ -1193,16 +1195,11 @@ int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const
     return 0;
 }
 
-int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, float* y,
-                    hipStream_t stream, char* err, size_t errlen) {
+int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
+                    float* y, hipStream_t stream, char* err, size_t errlen) {
     const ConvPlan p = plan_conv_f32(g);
-    if (p.kind == ConvPlan::kNone) {
-        snprintf(err, errlen,
-                 "conv: the window strips of one tile (row length %lld) do not fit in LDS; "
-                 "this shape is not supported", (long long)g.row_len);
-        return -5;
-    }
-    return launch_conv_f32_plan(g, p, fused, src, w, y, stream, err, errlen);
+    if (p.kind == ConvPlan::kNone) return launch_conv_plain(g, fused, src, w, y, stream, err, errlen);
+    return launch_conv_f32_plan(g, p, fused, src, w, scratch, y, stream, err, errlen);
 }
 
 }  // namespace im2win

@@ -88,9 +88,11 @@ def test_invalid_descriptor_rejected(field, value):
     setattr(d, field, value)
     assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EINVAL
     assert _code(P.im2win_transform, d, FAKE, FAKE, 1 << 30, 0) == P.IM2WIN_EINVAL
-    assert _code(P.im2win_conv2d, d, FAKE, 1 << 30, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
-    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d, d, FAKE, 1 << 30, FAKE, FAKE, 1 << 30, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 1 << 30, FAKE, 0) == P.IM2WIN_EINVAL
     assert _code(P.im2win_direct_conv2d, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_filter_scratch_bytes, d) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_workspace_shape, d) == P.IM2WIN_EINVAL
     assert P.im2win_last_error() != ""
 
 
@@ -101,11 +103,12 @@ def test_null_misaligned_and_short_workspace_rejected():
     assert _code(P.im2win_transform, d, FAKE, 0, need, 0) == P.IM2WIN_ENULL
     assert _code(P.im2win_transform, d, FAKE + 4, FAKE, need, 0) == P.IM2WIN_EALIGN
     assert _code(P.im2win_transform, d, FAKE, FAKE, need - 1, 0) == P.IM2WIN_EWORKSPACE
-    assert _code(P.im2win_conv2d, d, FAKE, need - 4, FAKE, FAKE, 0) == P.IM2WIN_EWORKSPACE
-    assert _code(P.im2win_conv2d, d, FAKE, need, 0, FAKE, 0) == P.IM2WIN_ENULL
-    assert _code(P.im2win_conv2d, d, FAKE, need, FAKE, FAKE + 8, 0) == P.IM2WIN_EALIGN
-    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, 0, 0) == P.IM2WIN_ENULL
-    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE + 2, FAKE, 0) == P.IM2WIN_EALIGN
+    sb = 1 << 20
+    assert _code(P.im2win_conv2d, d, FAKE, need - 4, FAKE, FAKE, sb, FAKE, 0) == P.IM2WIN_EWORKSPACE
+    assert _code(P.im2win_conv2d, d, FAKE, need, 0, FAKE, sb, FAKE, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_conv2d, d, FAKE, need, FAKE, FAKE, sb, FAKE + 8, 0) == P.IM2WIN_EALIGN
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, sb, 0, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE + 2, FAKE, sb, FAKE, 0) == P.IM2WIN_EALIGN
     for i in range(3):   # the direct baseline checks nulls (its pointers need no 16-byte alignment)
         args = [FAKE, FAKE, FAKE]
         args[i] = 0
@@ -118,7 +121,7 @@ def test_null_misaligned_and_short_workspace_rejected():
 def test_oversized_problem_rejected():
     d = _desc(Shape(1 << 20, 4, 1024, 1024, 4, 3, 3, 1, 1, 1, 1))   # N*Ho*Wo >= 2^31
     assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EOVERFLOW
-    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 1 << 30, FAKE, 0) == P.IM2WIN_EOVERFLOW
     assert _code(P.im2win_direct_conv2d, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EOVERFLOW
 
 
@@ -145,7 +148,7 @@ def test_unknown_layout_rejected():
     d = _desc(GOOD)
     d.layout = 2
     assert _code(P.im2win_workspace_bytes, d) == P.IM2WIN_EINVAL
-    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, 1 << 30, FAKE, 0) == P.IM2WIN_EINVAL
     assert "layout" in P.im2win_last_error()
 
 
@@ -178,3 +181,77 @@ def test_launch_plans_in_bounds_on_paper_layers():
             for layout in (P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED):
                 d = P.im2win_desc(2, ci, hi, wi, co, hf, wf, st, st, 0, 0, dt, layout)
                 assert P.im2win_check_plan(d) == 0, (layer["name"], P.im2win_last_error())
+
+
+# ---------------------------------------------------------------------------
+# Filter scratch (the repacked filter lives in a caller-owned buffer)
+# ---------------------------------------------------------------------------
+
+def test_filter_scratch_sizes_on_workloads():
+    """Which workloads repack the filter, and how large the scratch is: bf16
+    fast kernels take K*C*Fh*Fw*2 bytes exactly; fp32 filters whose chunk rows
+    are not whole 16-byte vectors (C*Fh*Fw odd: the single-image and stem
+    layers) take padded blocks of about K*C*Fh*Fw*4 bytes; the others none."""
+    got = {}
+    for wl in workloads.WORKLOADS:
+        d = _desc(_wl_shape(wl), _wl_dtype(wl))
+        got[wl.name] = P.im2win_filter_scratch_bytes(d)
+    kcft = {wl.name: wl.k * wl.c * wl.fh * wl.fw for wl in workloads.WORKLOADS}
+    assert got["deep_3x3_bf16"] == kcft["deep_3x3_bf16"] * 2
+    assert got["resnet_3x3_f32"] == 0 and got["rect_3x5_s2_f32"] == 0
+    for name in ("single_3x3_f32", "stem_7x7_s2_f32"):
+        assert kcft[name] * 4 <= got[name] <= 2 * kcft[name] * 4 + (1 << 16), (name, got[name])
+
+
+def test_short_or_missing_scratch_rejected():
+    wl = workloads.BY_NAME["deep_3x3_bf16"]
+    d = _desc(_wl_shape(wl), _wl_dtype(wl))
+    need_ws = P.im2win_workspace_bytes(d)
+    need = P.im2win_filter_scratch_bytes(d)
+    assert need > 0
+    assert _code(P.im2win_conv2d, d, FAKE, need_ws, FAKE, FAKE, need - 16, FAKE, 0) == P.IM2WIN_EWORKSPACE
+    assert "scratch" in P.im2win_last_error()
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE, need - 16, FAKE, 0) == P.IM2WIN_EWORKSPACE
+    assert _code(P.im2win_conv2d, d, FAKE, need_ws, FAKE, 0, need, FAKE, 0) == P.IM2WIN_ENULL
+    assert _code(P.im2win_conv2d_fused, d, FAKE, FAKE, FAKE + 4, need, FAKE, 0) == P.IM2WIN_EALIGN
+
+
+@pytest.mark.parametrize("s", SHAPES, ids=str)
+@pytest.mark.parametrize("dtype", [P.IM2WIN_F32, P.IM2WIN_BF16])
+def test_workspace_shape_query(s, dtype):
+    d = _desc(s, dtype)
+    n, c, ho, row = P.im2win_workspace_shape(d)
+    e = 4 if dtype == P.IM2WIN_F32 else 2
+    assert (n, c, ho) == (s.n, s.c, s.ho)
+    assert n * c * ho * row * e == P.im2win_workspace_bytes(d)
+    assert (n, c, ho, row) == s.win_shape
+
+
+# Shapes whose window strips fit no LDS tile (long rows, few output columns):
+# they run on the per-output kernel, which needs no plan and no scratch.
+NO_TILE = [Shape(1, 2, 3, 4096, 3, 3, 4096, 1, 1, 0, 0), Shape(2, 1, 5, 20000, 2, 5, 19000, 1, 7, 0, 0)]
+
+
+@pytest.mark.parametrize("s", NO_TILE, ids=str)
+@pytest.mark.parametrize("dtype", [P.IM2WIN_F32, P.IM2WIN_BF16])
+def test_shapes_without_a_tile_take_the_plain_kernel(s, dtype):
+    d = _desc(s, dtype)
+    assert P.im2win_filter_scratch_bytes(d) == 0
+    assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+
+
+def test_binding_rejects_mismatched_tensors():
+    """The tensor helpers check shapes and dtypes before any C call (the C
+    ABI takes no tensor sizes)."""
+    import torch
+    d = P.desc_for((2, 3, 8, 8), (4, 3, 3, 3), 1, 1)
+    x = torch.zeros(2, 3, 8, 8)           # a host tensor: refused as not on the device
+    with pytest.raises(ValueError):
+        P.conv2d_fused(x, torch.zeros(4, 3, 3, 3), d)
+
+
+def test_one_hip_runtime_mapped():
+    """libim2win binds to the HIP runtime torch loaded, not to a second copy."""
+    P.load_library()
+    maps = P.hip_runtimes_mapped()
+    assert len(maps) == 1, maps

@@ -6,8 +6,8 @@
 - convolution and fused convolution: element by element within the fp32
   rounding bound (n + 2) * 2^-24 * sum|x*w| (n = C*Fh*Fw terms), and relative
   L2 error <= 1e-5 (fp32) / 1e-2 (bf16), against the fp64 direct convolution
-  of the same (bf16-rounded) data: on the whole output at reduced batch and on
-  sampled outputs at full size;
+  of the same (bf16-rounded) data, on the whole output, at reduced batch and
+  at full size;
 - fused and unfused stage identical window strips and run the same matrix-core
   sequence, so their outputs must be bitwise identical.
 """
@@ -141,34 +141,19 @@ def test_conv_whole_output_reduced_batch(wl, fused):
     print(f"[parity] rel-L2 {rel:.3e}", flush=True)
 
 
-def _sample_indices(n, k, ho, wo, count, seed):
-    rng = np.random.default_rng(seed)
-    total = n * k * ho * wo
-    idx = [rng.integers(0, total, size=count)]
-    # borders of the first and last image for the first and last channel
-    for i in (0, n - 1):
-        for j in (0, k - 1):
-            base = (i * k + j) * ho * wo
-            rows = np.arange(ho)
-            cols = np.arange(wo)
-            idx += [base + cols, base + (ho - 1) * wo + cols, base + rows * wo, base + rows * wo + wo - 1]
-    idx.append(np.array([0, total - 1]))
-    return np.unique(np.concatenate(idx))
-
-
 @pytest.mark.parametrize("wl", workloads.WORKLOADS, ids=lambda wl: wl.name)
-def test_conv_full_size_sampled_and_fused_identical(wl):
+def test_conv_full_size_whole_output_and_fused_identical(wl):
+    """Every output of both convolutions at full size, in the launch
+    configuration bench.py times, against the fp64 oracle (Eq. 1)."""
     _label("conv-full", wl)
     x_cpu, w_cpu = workloads.make_input(wl), workloads.make_filter(wl)
     y_unf = _run_conv(wl, x_cpu, w_cpu, wl.n, False)
     y_fus = _run_conv(wl, x_cpu, w_cpu, wl.n, True)
     assert np.array_equal(y_unf, y_fus), "fused and unfused outputs differ"
-    s = _shape(wl)
-    idx = _sample_indices(wl.n, wl.k, s.ho, s.wo, 4000, 7)
-    ref, ref_abs = oracle.direct_conv_at(s, _f64(x_cpu), _f64(w_cpu), idx)
-    rel = _assert_close(y_unf.reshape(-1)[idx], ref, ref_abs, wl.c * wl.fh * wl.fw, wl.dtype,
-                        wl.name + " (sampled)")
-    print(f"[parity] sampled rel-L2 {rel:.3e} over {idx.size} outputs", flush=True)
+    del y_fus
+    ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
+    rel = _assert_close(y_unf, ref, ref_abs, wl.c * wl.fh * wl.fw, wl.dtype, wl.name + " (full size)")
+    print(f"[parity] full-size rel-L2 {rel:.3e} over {y_unf.size} outputs", flush=True)
 
 
 # --------------------------------------------------------------------------
@@ -190,6 +175,10 @@ EDGE = [
     (1, 33, 30, 70, 65, 7, 7, 2, 2, 3, 3),    # stem-like with ragged pixel and channel tiles
     (2, 40, 7, 7, 300, 3, 3, 1, 1, 1, 1),     # deep-narrow, 3 channel tiles
     (1, 3, 227, 227, 96, 11, 11, 4, 4, 0, 0), # Table 1 Conv1 at batch 1
+    (2, 32, 9, 11, 64, 3, 5, 2, 2, 1, 2),     # bf16 3x5 with 16-byte filter pieces (strips gathered)
+    (2, 32, 10, 12, 64, 3, 5, 1, 2, 1, 2),    # bf16 3x5 fast and fused-fast kernels (rows of 48, W even)
+    (2, 32, 14, 14, 128, 1, 1, 1, 1, 0, 0),   # 1x1 with 16-byte filter pieces
+    (2, 32, 16, 16, 128, 1, 1, 1, 1, 0, 0),   # 1x1 fast and fused-fast kernels
 ]
 
 
@@ -244,34 +233,16 @@ def test_bf16_error_against_unrounded_data():
     assert rel < 1e-2
 
 
-def test_repacked_filters_share_the_stream_buffer():
-    """fp32 filters whose chunk rows are not whole 16-byte vectors (7x7, 5x5,
-    11x11) are repacked per call into the same per-stream buffer as the bf16
-    fast kernels' filters: fp32 and bf16 convolutions interleaved on two
-    streams, with a larger filter replacing a stream's buffer in the middle,
-    each result against the oracle."""
-    cases = [
-        (1, "f32", (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3)),
-        (2, "bf16", (2, 32, 14, 14, 64, 3, 3, 1, 1, 1, 1)),
-        (1, "f32", (1, 6, 24, 24, 96, 5, 5, 1, 1, 0, 0)),
-        (2, "f32", (1, 3, 47, 47, 96, 11, 11, 4, 4, 0, 0)),
-        (1, "bf16", (1, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)),
-        (2, "f32", (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3)),
-    ]
-    streams = {1: torch.cuda.Stream(device=DEV), 2: torch.cuda.Stream(device=DEV)}
-    runs = []
-    for i, (sid, dtype, shape) in enumerate(cases):
-        wl, x_cpu, w_cpu = workloads.random_case(800 + i, *shape, dtype=dtype)
-        _label("repacked-filter stream", wl)
-        d = _desc(wl)
-        assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
-        stream = streams[sid]
-        with torch.cuda.stream(stream):
-            x, w = x_cpu.to(DEV), w_cpu.to(DEV)
-            y_fused = P.conv2d_fused(x, w, d, stream=stream)
-            y = P.conv2d(P.transform(x, d, stream=stream), w, d, stream=stream)
-        runs.append((wl, x_cpu, w_cpu, y, y_fused))
-    torch.cuda.synchronize()
+REPACK_CASES = [
+    ("f32", (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3)),    # fp32 rows not whole vectors: repacked
+    ("bf16", (2, 32, 14, 14, 64, 3, 3, 1, 1, 1, 1)),  # bf16 fast kernels: 8-channel pieces
+    ("f32", (1, 6, 24, 24, 96, 5, 5, 1, 1, 0, 0)),
+    ("f32", (1, 3, 47, 47, 96, 11, 11, 4, 4, 0, 0)),
+    ("bf16", (1, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)),
+]
+
+
+def _check_runs(runs):
     for wl, x_cpu, w_cpu, y, y_fused in runs:
         ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
         for what, out in (("unfused", y), ("fused", y_fused)):
@@ -279,28 +250,106 @@ def test_repacked_filters_share_the_stream_buffer():
                           f"{wl.name} {what}")
 
 
-def test_bf16_packed_filter_per_stream():
-    """The bf16 fast kernels read a repacked filter that the library keeps per
-    stream: two streams with different filters in flight at once, then a
-    larger filter on the first stream (its buffer is replaced in stream
-    order), each result against the oracle."""
-    small = (2, 32, 14, 14, 64, 3, 3, 1, 1, 1, 1)
-    large = (1, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)
-    s1, s2 = torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)
+def test_repacked_filters_in_caller_scratch_on_two_streams():
+    """Filters that the kernels read repacked go to the scratch each call is
+    given: fp32 and bf16 convolutions with different filters interleaved on
+    two streams, each call with its own scratch, each result against the
+    oracle."""
+    streams = [torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)]
     runs = []
-    for seed, shape, stream in ((1, small, s1), (2, small, s2), (3, large, s1), (4, small, s2)):
-        wl, x_cpu, w_cpu = workloads.random_case(700 + seed, *shape, dtype="bf16")
-        _label("packed-filter stream", wl)
+    for i, (dtype, shape) in enumerate(REPACK_CASES + REPACK_CASES[:1]):
+        wl, x_cpu, w_cpu = workloads.random_case(800 + i, *shape, dtype=dtype)
+        _label("repacked-filter stream", wl)
         d = _desc(wl)
         assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+        stream = streams[i % 2]
         with torch.cuda.stream(stream):
             x, w = x_cpu.to(DEV), w_cpu.to(DEV)
             y_fused = P.conv2d_fused(x, w, d, stream=stream)
             y = P.conv2d(P.transform(x, d, stream=stream), w, d, stream=stream)
         runs.append((wl, x_cpu, w_cpu, y, y_fused))
     torch.cuda.synchronize()
-    for wl, x_cpu, w_cpu, y, y_fused in runs:
-        ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
-        for what, out in (("unfused", y), ("fused", y_fused)):
-            _assert_close(out.cpu().numpy().astype(np.float64), ref, ref_abs, wl.c * wl.fh * wl.fw, "bf16",
-                          f"{wl.name} {what}")
+    _check_runs(runs)
+
+
+def test_two_host_threads_on_the_default_stream():
+    """Two host threads call the library at once on the same (default) stream,
+    each with its own filters -- fp32 ones that are repacked and bf16 ones for
+    the fast kernels -- and its own scratch: the library keeps no state
+    between calls, so every result matches the oracle."""
+    import threading
+    cases = [[REPACK_CASES[0], REPACK_CASES[1], REPACK_CASES[3]],
+             [REPACK_CASES[4], REPACK_CASES[2], REPACK_CASES[1]]]
+    inputs = [[workloads.random_case(900 + 10 * t + i, *shape, dtype=dtype) for i, (dtype, shape) in enumerate(cs)]
+              for t, cs in enumerate(cases)]
+    for per in inputs:
+        for wl, _, _ in per:
+            assert P.im2win_check_plan(_desc(wl)) == 0, P.im2win_last_error()
+    results = [[], []]
+    errors = []
+    barrier = threading.Barrier(2)
+
+    def worker(t):
+        try:
+            torch.cuda.set_device(0)
+            barrier.wait()
+            for _ in range(3):
+                for wl, x_cpu, w_cpu in inputs[t]:
+                    d = _desc(wl)
+                    x, w = x_cpu.to(DEV), w_cpu.to(DEV)
+                    y_fused = P.conv2d_fused(x, w, d)
+                    y = P.conv2d(P.transform(x, d), w, d)
+                    results[t].append((wl, x_cpu, w_cpu, y, y_fused))
+        except Exception as e:   # reported by the main thread
+            errors.append(e)
+
+    print("[parity] two host threads on the default stream", flush=True)
+    threads = [threading.Thread(target=worker, args=(t,)) for t in (0, 1)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    _check_runs(results[0] + results[1])
+
+
+def test_transform_rows_beyond_lds():
+    """Window-tensor rows too long to build in on-chip memory (a 2000-wide
+    input with a 9x9 filter: Wp*Fh*4 = 72 KB per row) take the transform's
+    direct kernel, one workgroup per row: bit-exact, with a guard band."""
+    for dtype in ("f32", "bf16"):
+        wl, x_cpu, w_cpu = workloads.random_case(950, 1, 2, 12, 2000, 3, 9, 9, 1, 1, 0, 0, dtype)
+        _label("transform-direct", wl)
+        assert P.im2win_check_plan(_desc(wl)) == 0, P.im2win_last_error()
+        _check_transform(wl, x_cpu, wl.n)
+
+
+NO_TILE = [
+    (1, 2, 3, 4096, 3, 3, 4096, 1, 1, 0, 0),       # filter as wide as the input: Wo = 1
+    (2, 1, 5, 20000, 2, 5, 19000, 1, 7, 0, 0),     # 64 windows of one row span 97k elements
+    (1, 3, 4, 3000, 2, 3, 2990, 2, 3, 1, 0),       # stride, padding, Wo = 4
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", NO_TILE, ids=lambda c: "x".join(map(str, c)))
+def test_shapes_without_an_lds_tile(case, dtype):
+    """Window strips no LDS tile holds: both convolutions run on the
+    per-output kernel, against the oracle; no filter scratch is needed."""
+    wl, x_cpu, w_cpu = workloads.random_case(sum(case), *case, dtype=dtype)
+    _label("no-tile", wl)
+    d = _desc(wl)
+    assert P.im2win_filter_scratch_bytes(d) == 0
+    assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+    _check_transform(wl, x_cpu, wl.n)
+    ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
+    y_unf = _run_conv(wl, x_cpu, w_cpu, wl.n, False)
+    y_fus = _run_conv(wl, x_cpu, w_cpu, wl.n, True)
+    nterms = wl.c * wl.fh * wl.fw
+    _assert_close(y_unf, ref, ref_abs, nterms, dtype, "unfused")
+    _assert_close(y_fus, ref, ref_abs, nterms, dtype, "fused")
+
+
+def test_one_hip_runtime_after_gpu_use():
+    assert len(P.hip_runtimes_mapped()) == 1, P.hip_runtimes_mapped()
