@@ -190,6 +190,27 @@ int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, void
                         size_t scratch_bytes, float* y, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * convolution as im2win_conv2d_fused with no scratch argument.  The repacked
+ * filter goes to a static device array of IM2WIN_NOALLOC_SCRATCH_BYTES inside
+ * the library, one per device, held until the process ends; the call
+ * allocates and frees nothing.  The device current on the calling thread
+ * must be the device of x, w, y and the stream.
+ * Every call on a device shares that device's array: calls that may overlap
+ * on one device (other streams, other host threads) race on it and must be
+ * serialised by the caller; calls on one stream are ordered and safe.  Each
+ * call rewrites the part of the array it reads before reading it.
+ *   x, w, y  as for im2win_conv2d_fused
+ * Errors: EINVAL, ENULL, EALIGN, EOVERFLOW, EHIP, and EWORKSPACE when
+ * im2win_filter_scratch_bytes() exceeds IM2WIN_NOALLOC_SCRATCH_BYTES (use
+ * im2win_conv2d_fused with a caller buffer then).
+ */
+#define IM2WIN_NOALLOC_SCRATCH_BYTES (8u << 20)
+int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void* w, float* y,
+                                void* stream);
+
+/*
  * Message for the last failed call on this host thread ("" if none).  The
  * string is owned by the library and valid until the next call on the thread.
  */

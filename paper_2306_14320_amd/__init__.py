@@ -31,6 +31,7 @@ IM2WIN_EWORKSPACE = -3
 IM2WIN_EHIP = -4
 IM2WIN_EOVERFLOW = -5
 IM2WIN_EALIGN = -6
+IM2WIN_NOALLOC_SCRATCH_BYTES = 8 << 20
 
 
 class im2win_desc(ctypes.Structure):
@@ -82,6 +83,7 @@ def load_library():
         "im2win_conv2d": [D, P, SZ, P, P, SZ, P, P],
         "im2win_conv2d_fused": [D, P, P, P, SZ, P, P],
         "im2win_direct_conv2d": [D, P, P, P, P],
+        "im2win_conv2d_fused_noalloc": [D, P, P, P, P],
         "im2win_selftest": [],
         "im2win_check_plan": [D],
     }
@@ -159,6 +161,10 @@ def im2win_conv2d_fused(desc: im2win_desc, x: int, w: int, scratch: int, scratch
                         y: int, stream: int) -> None:
     _check(load_library().im2win_conv2d_fused(ctypes.byref(desc), x, w, scratch, scratch_bytes, y,
                                               stream))
+
+
+def im2win_conv2d_fused_noalloc(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:
+    _check(load_library().im2win_conv2d_fused_noalloc(ctypes.byref(desc), x, w, y, stream))
 
 
 def im2win_direct_conv2d(desc: im2win_desc, x: int, w: int, y: int, stream: int) -> None:

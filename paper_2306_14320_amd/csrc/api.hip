@@ -8,9 +8,16 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "common.h"
 #include "direct.h"
+
+// Filter scratch of im2win_conv2d_fused_noalloc: a static device array, so
+// that the call allocates nothing.  Each device holds its own copy; its
+// device address is looked up once per device (with that device current)
+// and kept.  Host code uses only that address, never the array's name.
+static __device__ __align__(256) unsigned char scratch[IM2WIN_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -203,6 +210,30 @@ int check_scratch(const im2win::Geometry& g, bool fused, const void* scratch, si
     return IM2WIN_OK;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_scratch(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(IM2WIN_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(IM2WIN_EINVAL, "device %d is beyond the %d devices the static scratch serves", dev,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(IM2WIN_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return IM2WIN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -240,6 +271,28 @@ int im2win_conv2d_fused(const im2win_desc* d, const void* x, const void* w, void
     rc = g.elem == 4 ? im2win::launch_conv_f32(g, true, x, w, scratch, y, s, msg, sizeof msg)
                      : im2win::launch_conv_bf16(g, true, x, w, scratch, y, s, msg, sizeof msg);
     return after_launch(rc, "conv2d_fused", msg);
+}
+
+int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void* w, float* y,
+                                void* stream) {
+    im2win::Geometry g;
+    int rc = geometry(d, &g);
+    if (rc) return rc;
+    if ((rc = check_ptr(x, "x")) || (rc = check_ptr(w, "w")) || (rc = check_ptr(y, "y")))
+        return rc;
+    const int64_t need = im2win::conv_scratch_bytes(g, true);
+    if (need > (int64_t)IM2WIN_NOALLOC_SCRATCH_BYTES)
+        return fail(IM2WIN_EWORKSPACE,
+                    "this convolution needs %lld bytes of filter scratch; the library's static "
+                    "scratch holds %lld (use im2win_conv2d_fused with a scratch buffer)",
+                    (long long)need, (long long)IM2WIN_NOALLOC_SCRATCH_BYTES);
+    void* sp = nullptr;
+    if (need > 0 && (rc = static_scratch(&sp))) return rc;
+    char msg[256] = "";
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = g.elem == 4 ? im2win::launch_conv_f32(g, true, x, w, sp, y, s, msg, sizeof msg)
+                     : im2win::launch_conv_bf16(g, true, x, w, sp, y, s, msg, sizeof msg);
+    return after_launch(rc, "conv2d_fused_noalloc", msg);
 }
 
 int im2win_direct_conv2d(const im2win_desc* d, const void* x, const void* w, float* y,

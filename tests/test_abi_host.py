@@ -255,3 +255,17 @@ def test_one_hip_runtime_mapped():
     P.load_library()
     maps = P.hip_runtimes_mapped()
     assert len(maps) == 1, maps
+
+
+def test_noalloc_entry_point_rejects_scratch_beyond_its_array():
+    """im2win_conv2d_fused_noalloc keeps the repacked filter in a static
+    device array of IM2WIN_NOALLOC_SCRATCH_BYTES; a filter that needs more is
+    refused on the host (EWORKSPACE) before any HIP call."""
+    d = P.im2win_desc(2, 1024, 14, 14, 1024, 3, 3, 1, 1, 1, 1, P.IM2WIN_BF16)
+    assert P.im2win_filter_scratch_bytes(d) > P.IM2WIN_NOALLOC_SCRATCH_BYTES
+    assert _code(P.im2win_conv2d_fused_noalloc, d, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EWORKSPACE
+    assert "static" in P.im2win_last_error()
+    bad = _desc(GOOD)
+    bad.k = 0
+    assert _code(P.im2win_conv2d_fused_noalloc, bad, FAKE, FAKE, FAKE, 0) == P.IM2WIN_EINVAL
+    assert _code(P.im2win_conv2d_fused_noalloc, _desc(GOOD), FAKE, FAKE, FAKE + 4, 0) == P.IM2WIN_EALIGN
