@@ -452,7 +452,144 @@ void check_packed_filter(const Geometry& g, const ConvPlan& p, Report& r) {
             }
 }
 
+// One-image-per-workgroup bf16 kernel: replays the kernel's own index
+// arithmetic for every lane of every wave (window reads of each tap, staging
+// loads and LDS writes, filter-fragment loads, output stores) and checks
+// that every index stays inside its buffer, that the LDS positions the
+// windows read hold exactly the window-tensor elements Alg. 2 sums (written
+// once per chunk, or padding that is never written), and that every output
+// is stored exactly once.
+void check_conv_image(const Geometry& g, bool fused, const ImgPlan& p, Report& r) {
+    const ImgArgs a = image_args(g, p, nullptr, nullptr, nullptr);
+    const int T = (int)g.taps, FH = (int)g.fh;
+    if (p.lds_bytes != 2 * p.stage_pos * 16 || p.lds_bytes > kConvLdsMaxBytes || p.stage_pos != 4 * p.plane_pos ||
+        p.pitch < g.row_len || (p.pitch - g.sw * g.fh * g.wo) % 16 != 0)
+        r.fail("image conv: LDS layout (pitch %lld, plane %lld, %lld bytes)", (long long)p.pitch,
+               (long long)p.plane_pos, (long long)p.lds_bytes);
+    // workgroup -> (image, K tile) is a bijection
+    std::vector<uint8_t> seen_wg(a.grid, 0);
+    for (int b = 0; b < a.grid; ++b) {
+        const int bid = a.xcd_remap ? (b & 7) * (a.grid >> 3) + (b >> 3) : b;
+        if (bid < 0 || bid >= a.grid || seen_wg[bid]++) {
+            r.fail("image conv: workgroup %d maps to %d (repeated or out of range)", b, bid);
+            return;
+        }
+    }
+    // What each LDS position of one stage holds after the staging of a
+    // chunk: -1 never written, else (channel group, window-tensor element
+    // m*row_len + k*Fh + u) encoded as g*2^28 + element.
+    const int64_t plane_elems = (int64_t)g.ho * g.row_len;
+    std::vector<int64_t> holds(p.stage_pos, -1);
+    const int SI = fused ? kImgFusedItems : kImgStripItems;
+    const int64_t src_chan = (int64_t)g.c * p.plane_src;   // elements per image
+    for (int tid = 0; tid < kImgThreads; ++tid)
+        for (int k = 0; k < SI; ++k) {
+            const int item = tid + k * kImgThreads;
+            if (item >= 4 * a.ngroups) continue;
+            const int gg = item / a.ngroups, e = item - gg * a.ngroups;
+            if (!fused) {
+                const int64_t off = (int64_t)gg * 8 * a.plane_src + 4 * e;
+                // loads: 4 elements of channels 8gg .. 8gg+7 of the last chunk's planes
+                const int64_t last = (int64_t)(a.nchunks - 1) * kImgChunk * a.plane_src + off + 7 * (int64_t)a.plane_src + 3;
+                if (last >= src_chan || off % 4) r.fail("image conv: strip load of item %d reads %lld of %lld", item,
+                                                        (long long)last, (long long)src_chan);
+                const int m = (4 * e) / a.row_len, q = 4 * e - m * a.row_len;
+                for (int pq = 0; pq < 4; ++pq) {
+                    const int64_t pos = (int64_t)gg * a.plane_pos + (int64_t)m * a.pitch + q + pq;
+                    if (q + pq >= a.row_len || pos < 0 || pos >= (gg + 1) * (int64_t)a.plane_pos || holds[pos] != -1) {
+                        r.fail("image conv: item %d writes LDS position %lld twice or out of its plane", item, (long long)pos);
+                        return;
+                    }
+                    holds[pos] = ((int64_t)gg << 28) + (int64_t)m * g.row_len + q + pq;
+                }
+            } else {
+                const int64_t off = (int64_t)gg * 8 * a.plane_src + 2 * e;
+                const int64_t last = (int64_t)(a.nchunks - 1) * kImgChunk * a.plane_src + off + 7 * (int64_t)a.plane_src + 1;
+                if (last >= src_chan || off % 2) r.fail("image conv: x load of item %d reads %lld of %lld", item,
+                                                        (long long)last, (long long)src_chan);
+                const int yy = (2 * e) / a.w, xx = 2 * e - yy * a.w;
+                for (int u = 0; u < FH; ++u) {
+                    const int t = yy + a.ph - u;
+                    const int m = t >= 0 ? t / a.sh : -1;
+                    if (!(t >= 0 && m * a.sh == t && m < a.ho && xx + a.pw < a.wr)) continue;
+                    for (int d = 0; d < 2; ++d) {
+                        if (d == 1 && !(xx + 1 + a.pw < a.wr)) continue;
+                        const int kk = xx + d + a.pw;
+                        const int64_t pos = (int64_t)gg * a.plane_pos + (int64_t)m * a.pitch + (int64_t)kk * FH + u;
+                        if (pos < 0 || pos >= (gg + 1) * (int64_t)a.plane_pos || holds[pos] != -1) {
+                            r.fail("image conv: x item %d writes LDS position %lld twice or out of its plane", item,
+                                   (long long)pos);
+                            return;
+                        }
+                        holds[pos] = ((int64_t)gg << 28) + (int64_t)m * g.row_len + (int64_t)kk * FH + u;
+                    }
+                }
+            }
+        }
+    // window reads: every tap of every lane's window is the element Alg. 2
+    // sums (or, fused, padding that reads zero)
+    const int64_t frags = g.k * g.c * T * 2 / 16;   // scratch in 16-byte units
+    for (int wv = 0; wv < kImgThreads / 64 && r.violations < 16; ++wv) {
+        const int kp = wv & 3, half = wv >> 2;
+        for (int lane = 0; lane < 64; ++lane) {
+            const int gl = lane >> 4;
+            for (int q = 0; q < kImgNPB; ++q) {
+                int pix = (half * kImgNPB + q) * 16 + (lane & 15);
+                if (pix > a.npix - 1) pix = a.npix - 1;
+                const int m = pix / a.wo, n = pix - m * a.wo;
+                const int64_t base = (int64_t)gl * a.plane_pos + (int64_t)m * a.pitch + (int64_t)n * a.sw * FH;
+                for (int t = 0; t < T; ++t) {
+                    const int64_t pos = base + t;
+                    const int v = t / FH, u = t - v * FH;
+                    const int64_t want = ((int64_t)gl << 28) + (int64_t)m * g.row_len + ((int64_t)n * a.sw + v) * FH + u;
+                    const bool pad_ok = fused && holds[pos] == -1 &&
+                                        ((int64_t)m * a.sh + u - a.ph < 0 || (int64_t)m * a.sh + u - a.ph >= a.h ||
+                                         (int64_t)n * a.sw + v - a.pw < 0 || (int64_t)n * a.sw + v - a.pw >= a.w);
+                    if (pos < 0 || pos >= p.stage_pos || (holds[pos] != want && !pad_ok)) {
+                        r.fail("image conv: wave %d lane %d block %d tap %d reads LDS %lld holding %lld, wants %lld", wv,
+                               lane, q, t, (long long)pos, (long long)(pos >= 0 && pos < p.stage_pos ? holds[pos] : -2),
+                               (long long)want);
+                        break;
+                    }
+                }
+            }
+            // filter fragments (16-byte units) of the last chunk of the last K tile
+            const int64_t idx = ((((int64_t)(a.nkt - 1) * 4 + kp) * a.nchunks + a.nchunks - 1) * T + T - 1) * 2 * 64 +
+                                64 + lane;
+            if (idx >= frags) r.fail("image conv: filter fragment %lld of %lld", (long long)idx, (long long)frags);
+        }
+    }
+    // outputs: each (image, channel, pixel) stored once
+    std::vector<uint8_t> out((size_t)g.k * a.npix, 0);
+    for (int kt = 0; kt < a.nkt; ++kt)
+        for (int wv = 0; wv < kImgThreads / 64; ++wv)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int q = 0; q < kImgNPB; ++q) {
+                    const int pix = ((wv >> 2) * kImgNPB + q) * 16 + (lane & 15);
+                    if (pix >= a.npix) continue;
+                    for (int i = 0; i < 2; ++i)
+                        for (int v = 0; v < 4; ++v) {
+                            const int j = kt * 128 + (wv & 3) * 32 + i * 16 + 4 * (lane >> 4) + v;
+                            if (j >= g.k) { r.fail("image conv: output channel %d", j); return; }
+                            ++out[(size_t)j * a.npix + pix];
+                        }
+                }
+    for (size_t i = 0; i < out.size(); ++i)
+        if (out[i] != 1) {
+            r.fail("image conv: output %zu of an image stored %d times", i, (int)out[i]);
+            return;
+        }
+    if (conv_scratch_bytes(g, fused) < g.k * g.c * T * 2)
+        r.fail("image conv: filter scratch of %lld bytes", (long long)conv_scratch_bytes(g, fused));
+    (void)plane_elems;
+}
+
 void check_conv(const Geometry& g, bool fused_plan, Report& r) {
+    const ImgPlan ip = plan_image_bf16(g, fused_plan);
+    if (ip.ok) {
+        check_conv_image(g, fused_plan, ip, r);
+        return;
+    }
     const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused_plan) : plan_conv_f32(g);
     // no tile fits in LDS: the per-output kernel runs instead, which indexes
     // every operand directly (no LDS, no plan)

@@ -1161,6 +1161,7 @@ int bf16_strip_mode(const ConvPlan& p, bool fused) {
 bool bf16_packed(const ConvPlan& p, bool fused) { return fused ? p.fused_fast != 0 : p.fast != 0; }
 
 int64_t conv_scratch_bytes(const Geometry& g, bool fused) {
+    if (plan_image_bf16(g, fused).ok) return g.k * g.c * g.taps * 2;
     const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused) : plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) return -1;
     if (p.kind == ConvPlan::kF32Lds) return filter_scratch_f32(g, p);
@@ -1169,6 +1170,8 @@ int64_t conv_scratch_bytes(const Geometry& g, bool fused) {
 
 int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
                      float* y, hipStream_t stream, char* err, size_t errlen) {
+    const ImgPlan ip = plan_image_bf16(g, fused);
+    if (ip.ok) return launch_conv_bf16_image(g, ip, fused, src, w, scratch, y, stream);
     const ConvPlan p = plan_conv_bf16(g, fused);
     if (p.kind == ConvPlan::kNone) return launch_conv_plain(g, fused, src, w, y, stream, err, errlen);
     if (p.kind == ConvPlan::kF32Lds)

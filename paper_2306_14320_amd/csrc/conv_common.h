@@ -335,6 +335,53 @@ struct TileCfg {
     int bm, bn;
 };
 
+// ---------------------------------------------------------------------------
+// bf16 convolution with one image per workgroup (conv_bf16_image.hip)
+// ---------------------------------------------------------------------------
+constexpr int kImgThreads = 512;     // 8 waves: 4 groups of 32 output channels x 2 halves of the pixels
+constexpr int kImgChunk = 32;        // input channels per chunk (one MFMA per tap)
+constexpr int kImgNPB = 7;           // 16-pixel blocks per wave (193 to 224 output pixels per image)
+constexpr int kImgStripItems = 2;    // unfused staging items per thread (4 positions x 8 channels)
+constexpr int kPackFragLoads = 5;    // filter pack: 16-byte loads per thread (16 rows of 32*9 elements)
+constexpr int kImgBRing = 4;         // B fragments in flight + 1 (LDS reads issued ahead of their MFMAs)
+constexpr int kImgFusedItems = 2;    // fused staging items per thread (2 input elements x 8 channels)
+
+struct ImgArgs {
+    const uint16_t* src;   // window tensor (unfused) or x (fused)
+    const uint16_t* wf;    // filter in fragment order
+    float* y;
+    int c, h, w, k, sh, sw, ph, pw, ho, wo;
+    int wr;                // window-tensor row width in input columns
+    int row_len;           // wr * Fh
+    int npix;              // Ho * Wo
+    int pitch;             // LDS positions per window-tensor row
+    int plane_pos;         // LDS positions per 8-channel plane
+    int stage_pos;         // LDS positions per stage (4 planes)
+    int plane_src;         // elements per channel plane of src (Ho*row_len, or H*W)
+    int ngroups;           // staging groups per channel plane (4 positions, or 2 elements)
+    int nkt;               // K / 128
+    int nchunks;           // C / 32
+    int grid;              // workgroups (N * nkt)
+    int xcd_remap;         // place the workgroups of one image on one XCD
+};
+
+struct ImgPlan {
+    bool ok = false;
+    int64_t pitch = 0, plane_pos = 0, stage_pos = 0, lds_bytes = 0, plane_src = 0, ngroups = 0, grid = 0;
+};
+
+// The plan of the one-image-per-workgroup kernel, or !ok when the shape is
+// not one it takes (bf16, 3x3 filter, C a multiple of 32, K of 128, 193 to
+// 224 output pixels per image, odd sw*Fh, strips of both stages in LDS, the
+// staging items of both variants within the per-thread registers).  Both
+// variants take a shape or neither, so that they stage the same strips and
+// run the same matrix-core sequence.
+ImgPlan plan_image_bf16(const Geometry& g, bool fused);
+ImgArgs image_args(const Geometry& g, const ImgPlan& p, const void* src, const void* wf, float* y);
+// Repacks w into `scratch` (K*C*Fh*Fw*2 bytes) and launches the convolution.
+int launch_conv_bf16_image(const Geometry& g, const ImgPlan& p, bool fused, const void* src,
+                           const void* w, void* scratch, float* y, hipStream_t stream);
+
 // Upper bound of the per-channel strip length over all pixel tiles of `bn`
 // pixels: a tile spanning D row boundaries reads D*L + (n1-n0)*sw*Fh + Fw*Fh
 // elements with n1 - n0 = (pixels - 1) - D*Wo; the bound is linear in D.

@@ -179,6 +179,9 @@ EDGE = [
     (2, 32, 10, 12, 64, 3, 5, 1, 2, 1, 2),    # bf16 3x5 fast and fused-fast kernels (rows of 48, W even)
     (2, 32, 14, 14, 128, 1, 1, 1, 1, 0, 0),   # 1x1 with 16-byte filter pieces
     (2, 32, 16, 16, 128, 1, 1, 1, 1, 0, 0),   # 1x1 fast and fused-fast kernels
+    (3, 64, 16, 14, 128, 3, 3, 1, 1, 0, 1),   # bf16 one-image tiles: 196 pixels, pad (0, 1)
+    (2, 32, 27, 14, 128, 3, 3, 2, 1, 1, 1),   # bf16 one-image tiles with row stride 2
+    (4, 32, 14, 14, 256, 3, 3, 1, 1, 1, 1),   # bf16 one-image tiles, 2 K tiles, XCD placement
 ]
 
 
