@@ -263,20 +263,28 @@ def workspace_shape(desc: im2win_desc):
     return im2win_workspace_shape(desc)
 
 
-def filter_scratch(desc: im2win_desc, device, stream=None) -> torch.Tensor:
-    """A device buffer of im2win_filter_scratch_bytes() bytes (may be empty),
-    allocated on the call's stream."""
-    nbytes = im2win_filter_scratch_bytes(desc)
+def _empty(shape, dtype, device, stream):
+    """torch.empty on the call's stream (the current one when stream is None)."""
+    if stream is None:
+        return torch.empty(shape, dtype=dtype, device=device)
     with torch.cuda.stream(_torch_stream(stream)):
-        return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+        return torch.empty(shape, dtype=dtype, device=device)
+
+
+def filter_scratch(desc: im2win_desc, device, stream=None, nbytes=None) -> torch.Tensor:
+    """A device buffer of im2win_filter_scratch_bytes() bytes (at least 16),
+    allocated on the call's stream."""
+    if nbytes is None:
+        nbytes = im2win_filter_scratch_bytes(desc)
+    return _empty(max(nbytes, 16), torch.uint8, device, stream)
 
 
 def _scratch_args(desc, scratch, device, stream):
-    need = im2win_filter_scratch_bytes(desc)
-    if need == 0 and scratch is None:
-        return None, 0, 0
     if scratch is None:
-        scratch = filter_scratch(desc, device, stream)
+        need = im2win_filter_scratch_bytes(desc)
+        if need == 0:
+            return None, 0, 0
+        scratch = filter_scratch(desc, device, stream, need)
     p = _dev(scratch, "scratch")
     return scratch, p, scratch.numel() * scratch.element_size()
 
@@ -285,18 +293,17 @@ def transform(x: torch.Tensor, desc: im2win_desc, ws: torch.Tensor = None, strea
     """Window tensor of x (N x C x Ho x Wr*Fh, dtype of x)."""
     xp = _dev(x, "x", x_shape(desc), _dtype_of(desc))
     if ws is None:
-        with torch.cuda.stream(_torch_stream(stream)):
-            ws = torch.empty(workspace_shape(desc), dtype=x.dtype, device=x.device)
+        ws = _empty(workspace_shape(desc), x.dtype, x.device, stream)
     im2win_transform(desc, xp, _dev(ws, "ws", dtype=_dtype_of(desc)), ws.numel() * ws.element_size(),
                      _stream(stream))
     return ws
 
 
 def _output(y, desc, device, stream):
+    shape = y_shape(desc)
     if y is None:
-        with torch.cuda.stream(_torch_stream(stream)):
-            y = torch.empty(y_shape(desc), dtype=torch.float32, device=device)
-    return y, _dev(y, "y", y_shape(desc), torch.float32)
+        y = _empty(shape, torch.float32, device, stream)
+    return y, _dev(y, "y", shape, torch.float32)
 
 
 def conv2d(ws: torch.Tensor, w: torch.Tensor, desc: im2win_desc, y: torch.Tensor = None,
