@@ -211,6 +211,21 @@ int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void*
                                 void* stream);
 
 /*
+ * Name of the convolution kernel that im2win_conv2d (fused == 0) or
+ * im2win_conv2d_fused (fused != 0) launches for *d, for logs, profiles and
+ * tests.  *name receives a string owned by the library (valid for the life of
+ * the process), one of:
+ *   "f32_one_image"      fp32, one image x 32 output channels per workgroup
+ *   "f32_tiles"          fp32, tiles of output channels x pixels
+ *   "bf16_one_image"     bf16, one image x 128 output channels per workgroup
+ *   "bf16_tiles"         bf16, tiles of output channels x pixels
+ *   "bf16_widened_tiles" bf16 inputs widened to fp32 in the fp32 tile kernel
+ *   "per_output"         one thread per output (no tile fits on chip)
+ * Host only.  Errors: EINVAL, ENULL, EOVERFLOW.
+ */
+int im2win_conv_kernel(const im2win_desc* d, int fused, const char** name);
+
+/*
  * Message for the last failed call on this host thread ("" if none).  The
  * string is owned by the library and valid until the next call on the thread.
  */

@@ -79,6 +79,7 @@ def load_library():
         "im2win_output_shape": [D, I64P, I64P],
         "im2win_workspace_shape": [D, I64P],
         "im2win_filter_scratch_bytes": [D, ctypes.POINTER(SZ)],
+        "im2win_conv_kernel": [D, ctypes.c_int, ctypes.POINTER(ctypes.c_char_p)],
         "im2win_transform": [D, P, P, SZ, P],
         "im2win_conv2d": [D, P, SZ, P, P, SZ, P, P],
         "im2win_conv2d_fused": [D, P, P, P, SZ, P, P],
@@ -145,6 +146,14 @@ def im2win_filter_scratch_bytes(desc: im2win_desc) -> int:
     out = ctypes.c_size_t()
     _check(load_library().im2win_filter_scratch_bytes(ctypes.byref(desc), ctypes.byref(out)))
     return out.value
+
+
+def im2win_conv_kernel(desc: im2win_desc, fused: bool) -> str:
+    """Name of the kernel im2win_conv2d (fused False) or im2win_conv2d_fused
+    (fused True) launches for desc."""
+    out = ctypes.c_char_p()
+    _check(load_library().im2win_conv_kernel(ctypes.byref(desc), int(bool(fused)), ctypes.byref(out)))
+    return out.value.decode()
 
 
 def im2win_transform(desc: im2win_desc, x: int, ws: int, ws_bytes: int, stream: int) -> None:

@@ -181,6 +181,15 @@ int im2win_filter_scratch_bytes(const im2win_desc* d, size_t* bytes) {
     return ok();
 }
 
+int im2win_conv_kernel(const im2win_desc* d, int fused, const char** name) {
+    im2win::Geometry g;
+    int rc = geometry(d, &g);
+    if (rc) return rc;
+    if (!name) return fail(IM2WIN_ENULL, "name is NULL");
+    *name = im2win::conv_kernel_name(g, fused != 0);
+    return ok();
+}
+
 int im2win_workspace_shape(const im2win_desc* d, int64_t* dims) {
     im2win::Geometry g;
     int rc = geometry(d, &g);

@@ -145,6 +145,8 @@ int launch_conv_bf16(const Geometry& g, bool fused, const void* src, const void*
 // this geometry needs, 0 when its kernels read w as given; -1 when no tile
 // fits in LDS, in which case launch_conv_plain computes the convolution.
 int64_t conv_scratch_bytes(const Geometry& g, bool fused);
+// Name of the kernel family the convolution launches (static string).
+const char* conv_kernel_name(const Geometry& g, bool fused);
 
 // One thread per output, reading the window tensor (or x, fused) and the
 // filter straight from device memory: the convolution of any shape whose

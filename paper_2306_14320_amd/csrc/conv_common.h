@@ -382,6 +382,102 @@ ImgArgs image_args(const Geometry& g, const ImgPlan& p, const void* src, const v
 int launch_conv_bf16_image(const Geometry& g, const ImgPlan& p, bool fused, const void* src,
                            const void* w, void* scratch, float* y, hipStream_t stream);
 
+// ---------------------------------------------------------------------------
+// fp32 convolution with one image per workgroup (conv_f32_image.hip)
+// ---------------------------------------------------------------------------
+constexpr int kF32ImgThreads = 256;   // 4 waves, each a quarter of every channel chunk
+constexpr int kF32ImgChunk = 8;       // input channels per chunk (2 per wave, one per k-slot)
+constexpr int kF32ImgMinNB = 4;       // 32-pixel blocks per image: 97 ..
+constexpr int kF32ImgMaxNB = 7;       // .. 224 output pixels
+constexpr int kF32ImgMaxSeg = 24;     // 64-element segments per channel strip (1536 elements)
+// LDS floats per channel slot: the longest strip plus 32 banks, so that the
+// two k-slots of a wave (adjacent slots) read different banks
+constexpr int kF32ImgSlot = 64 * kF32ImgMaxSeg + 32;
+
+struct F32ImgArgs {
+    const float* src;      // window tensor (unfused) or x (fused)
+    const float* wt;       // filter, K x C x Fh x Fw
+    float* y;
+    int c, h, w, k, sh, sw, ph, pw, ho, wo;
+    int row_len;           // window-tensor row length L
+    int npix;              // Ho * Wo
+    int plane_strip;       // Ho * L, strip elements per channel
+    int plane_src;         // elements per channel plane of src (Ho*L, or H*W)
+    int nkt;               // K / 32
+    int nchunks;           // C / 8
+    int grid;              // workgroups (N * nkt)
+    int xcd_remap;         // place the workgroups of one image on one XCD
+    int mode;              // kF32ImgWide, kF32ImgNarrow or kF32ImgGather
+    FastDiv div_row, div_wo;   // by L, by Wo
+};
+
+struct F32ImgPlan {
+    bool ok = false;
+    int nb = 0;            // 32-pixel blocks per image
+    int64_t lds_bytes = 0, grid = 0;
+};
+
+// Offset that no staging buffer of the fp32 one-image kernel reaches (image
+// slabs are below 2^30 bytes): a buffer load from it reads zero.
+constexpr uint32_t kF32ImgOutside = 0x40000000u;
+
+// LDS byte address, in stage 0, of the window start of the pixel of `lane`
+// in pixel block b (k-slot lane / 32 reads channel slot 2*wv + lane / 32);
+// pixels past the image are clamped to its last pixel.
+__host__ __device__ inline uint32_t f32img_window(const F32ImgArgs& a, int fh, int wv, int lane, int b) {
+    int p = b * 32 + (lane & 31);
+    if (p > a.npix - 1) p = a.npix - 1;
+    const int m = (int)fast_div((uint32_t)p, a.div_wo), n = p - m * a.wo;
+    return (uint32_t)((2 * wv + (lane >> 5)) * kF32ImgSlot + m * a.row_len + n * a.sw * fh) * 4u;
+}
+
+// How a workgroup of the fp32 one-image kernel copies strips into LDS.
+constexpr int kF32ImgWide = 0;     // window-tensor planes, 16-byte copies (Ho*L a multiple of 4)
+constexpr int kF32ImgNarrow = 1;   // window-tensor planes, 4-byte copies
+constexpr int kF32ImgGather = 2;   // fused: each strip position gathered from x
+
+// Source byte offset, within one channel plane of the staging source, of
+// part s of a slot copy for `lane`, or kF32ImgOutside (reads zero).
+// Wide: strip elements s*256 + 4*lane .. + 3 of the window-tensor plane.
+// Narrow: strip element s*64 + lane.  Gather: strip position s*64 + lane,
+// i.e. window-tensor element (m, k, u) of the plane, read from
+// x[m*sh + u - ph][k - pw] (zero in the padding).
+__host__ __device__ inline uint32_t f32img_source(const F32ImgArgs& a, int mode, int fh, int s, int lane) {
+    if (mode == kF32ImgWide) {
+        const int e = s * 256 + lane * 4;
+        return e < a.plane_strip ? (uint32_t)e * 4u : kF32ImgOutside;
+    }
+    const int pos = s * 64 + lane;
+    if (mode == kF32ImgNarrow) return pos < a.plane_strip ? (uint32_t)pos * 4u : kF32ImgOutside;
+    const int m = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - m * a.row_len;
+    const int k = rem / fh, u = rem - k * fh;
+    const int yy = m * a.sh + u - a.ph, xx = k - a.pw;
+    const bool inside = pos < a.plane_strip && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w;
+    return inside ? (uint32_t)(yy * a.w + xx) * 4u : kF32ImgOutside;
+}
+
+// LDS byte offset, within a stage, of copy j of wave wv: channel slot
+// 2*wv + (j & 1), part j / 2 (256 elements wide, 64 otherwise).
+__host__ __device__ inline uint32_t f32img_dest(int mode, int wv, int j) {
+    return (uint32_t)(((2 * wv + (j & 1)) * kF32ImgSlot) * 4 + (j >> 1) * (mode == kF32ImgWide ? 1024 : 256));
+}
+
+// Copies per wave and chunk (two channel slots).
+__host__ __device__ constexpr int f32img_copies(int mode) {
+    return mode == kF32ImgWide ? 2 * (kF32ImgMaxSeg / 4) : 2 * kF32ImgMaxSeg;
+}
+
+// The plan of the fp32 one-image-per-workgroup kernel, or !ok when the shape
+// is not one it takes (fp32, 3x3 or 3x5 filter, C a multiple of 16, K of 32,
+// 97 to 224 output pixels per image, at most 1536 strip elements per
+// channel, at least 256 workgroups).  The plan does not depend on fusion, so both
+// variants take a shape or neither.
+F32ImgPlan plan_image_f32(const Geometry& g);
+F32ImgArgs image_args_f32(const Geometry& g, const F32ImgPlan& p, bool fused, const void* src, const void* w,
+                          float* y);
+int launch_conv_f32_image(const Geometry& g, const F32ImgPlan& p, bool fused, const void* src, const void* w,
+                          float* y, hipStream_t stream);
+
 // Upper bound of the per-channel strip length over all pixel tiles of `bn`
 // pixels: a tile spanning D row boundaries reads D*L + (n1-n0)*sw*Fh + Fw*Fh
 // elements with n1 - n0 = (pixels - 1) - D*Wo; the bound is linear in D.

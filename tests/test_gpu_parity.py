@@ -201,6 +201,50 @@ def test_edge_shapes(case, dtype):
     assert np.array_equal(y_unf, y_fus), "fused and unfused outputs differ"
 
 
+# Shapes that the fp32 one-image kernel takes (at least 256 workgroups of one
+# image x 32 output channels, 97 to 224 output pixels), each in both row
+# layouts; the copy granularity (16-byte or 4-byte pieces of the strips)
+# follows from Ho*L.
+F32_ONE_IMAGE = [
+    (2, 16, 28, 28, 4096, 3, 5, 2, 2, 1, 2),   # 3x5 stride 2, 196 pixels in 7 blocks
+    (8, 32, 14, 14, 1024, 3, 3, 1, 1, 1, 1),   # 196 pixels, two chunk pairs, XCD placement
+    (16, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),   # 100 pixels in 4 blocks
+    (4, 16, 13, 23, 2048, 3, 5, 1, 2, 0, 1),   # 121 pixels, rows of 75 (4-byte copies)
+    (3, 32, 29, 15, 3200, 3, 3, 2, 1, 1, 0),   # 195 pixels, row stride 2, grid not a multiple of 8
+]
+
+
+@pytest.mark.parametrize("layout", [P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED], ids=["padded", "trimmed"])
+@pytest.mark.parametrize("case", F32_ONE_IMAGE, ids=lambda c: "x".join(map(str, c)))
+def test_fp32_one_image_kernel(case, layout):
+    """Whole output of both convolutions against the fp64 oracle (Eq. 1),
+    fused and unfused bitwise identical, nothing written past the output."""
+    n, c, h, w, k, fh, fw, sh, sw, ph, pw = case
+    wl, x_cpu, w_cpu = workloads.random_case(sum(case) + layout, n, c, h, w, k, fh, fw, sh, sw, ph, pw, "f32")
+    _label(f"f32-one-image layout={layout}", wl)
+    d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, P.IM2WIN_F32, layout)
+    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == "f32_one_image"
+    assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+    x, wt = x_cpu.to(DEV), w_cpu.to(DEV)
+    ho, wo = P.im2win_output_shape(d)
+    numel = n * k * ho * wo
+    outs = []
+    for fused in (False, True):
+        ybuf = torch.full((numel + 4096,), float("nan"), dtype=torch.float32, device=DEV)
+        y = ybuf[:numel].view(n, k, ho, wo)
+        if fused:
+            P.conv2d_fused(x, wt, d, y=y)
+        else:
+            P.conv2d(P.transform(x, d), wt, d, y=y)
+        torch.cuda.synchronize()
+        assert torch.isnan(ybuf[numel:]).all(), "convolution wrote past the output"
+        outs.append(y.cpu().numpy().astype(np.float64))
+    assert np.array_equal(outs[0], outs[1]), "fused and unfused outputs differ"
+    ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
+    rel = _assert_close(outs[0], ref, ref_abs, c * fh * fw, "f32", "one-image kernel")
+    print(f"[parity] rel-L2 {rel:.3e}", flush=True)
+
+
 def test_non_default_stream_and_reuse():
     """Calls are ordered on the caller's stream; a second, smaller problem on
     the same buffers gives its own correct result."""
