@@ -35,7 +35,8 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = {
     "transform": ["paper_2306_14320_amd/csrc/transform.hip", "paper_2306_14320_amd/csrc/common.h"],
     "conv": ["paper_2306_14320_amd/csrc/conv_f32.hip", "paper_2306_14320_amd/csrc/conv_bf16.hip",
-             "paper_2306_14320_amd/csrc/conv_bf16_image.hip", "paper_2306_14320_amd/csrc/conv_plain.hip",
+             "paper_2306_14320_amd/csrc/conv_bf16_image.hip", "paper_2306_14320_amd/csrc/conv_f32_band.hip",
+             "paper_2306_14320_amd/csrc/conv_plain.hip",
              "paper_2306_14320_amd/csrc/conv_common.h", "paper_2306_14320_amd/csrc/common.h"],
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")

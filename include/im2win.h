@@ -215,7 +215,8 @@ int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void*
  * im2win_conv2d_fused (fused != 0) launches for *d, for logs, profiles and
  * tests.  *name receives a string owned by the library (valid for the life of
  * the process), one of:
- *   "f32_one_image"      fp32, one image x 32 output channels per workgroup
+ *   "f32_bands"          fp32, a band of output rows of one image x 32 or 64
+ *                        output channels per workgroup
  *   "f32_tiles"          fp32, tiles of output channels x pixels
  *   "bf16_one_image"     bf16, one image x 128 output channels per workgroup
  *   "bf16_tiles"         bf16, tiles of output channels x pixels

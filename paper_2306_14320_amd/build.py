@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libim2win.so")
-SOURCES = ["api.hip", "transform.hip", "conv_f32.hip", "conv_bf16.hip", "conv_bf16_image.hip", "conv_f32_image.hip", "conv_plain.hip", "check.hip", "direct.hip"]
+SOURCES = ["api.hip", "transform.hip", "conv_f32.hip", "conv_bf16.hip", "conv_bf16_image.hip", "conv_f32_band.hip", "conv_plain.hip", "check.hip", "direct.hip"]
 ARCH = "gfx950"
 
 

@@ -584,141 +584,175 @@ void check_conv_image(const Geometry& g, bool fused, const ImgPlan& p, Report& r
     (void)plane_elems;
 }
 
-// fp32 one-image kernel: replays the workgroup map, every staging copy of
-// every wave (source inside the image slab or the zero-reading offset, LDS
-// destination inside the copy's channel slot, each strip position written
-// once with the window-tensor element it must hold), every window read of
-// every lane, tap and pixel block, the filter loads, the partial-sum area and
-// the output stores (each output exactly once).
-void check_conv_image_f32(const Geometry& g, bool fused, const F32ImgPlan& p, Report& r) {
-    const F32ImgArgs a = image_args_f32(g, p, fused, nullptr, nullptr, nullptr);
+// fp32 band kernel: replays the workgroup map (each (image, band, channel
+// group) once), and for every band: every staging copy of every wave (source
+// inside the image slab or the zero-reading offset, LDS destination inside the
+// copy's channel slot, each strip position written once with the
+// window-tensor element it must hold), every window read of every wave, lane,
+// pair, tap and pixel block, the filter rows, the partial-sum area and the
+// output stores (each output of the layer exactly once).
+void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Report& r) {
+    const F32BandArgs a = band_args_f32(g, p, fused, nullptr, nullptr, nullptr);
     const int T = (int)g.taps, FH = (int)g.fh, FW = (int)g.fw;
-    const int64_t stage_b = (int64_t)kF32ImgChunk * kF32ImgSlot * 4;
-    const int nb = p.nb;
-    if (2 * stage_b > p.lds_bytes || (int64_t)4 * 32 * nb * 32 * 4 > p.lds_bytes || p.lds_bytes > kConvLdsMaxBytes ||
-        nb * 32 < a.npix || (nb - 1) * 32 >= a.npix || a.plane_strip > 64 * kF32ImgMaxSeg ||
-        g.c % (2 * kF32ImgChunk) || g.k % 32) {
-        r.fail("fp32 image conv: plan (nb %d, %lld bytes of LDS, strip %d)", nb, (long long)p.lds_bytes,
-               a.plane_strip);
+    const int KS = p.ks, PP = 4 / KS, CB = 4 / KS, nb = p.nb;
+    const int64_t stage_f = kBandStageBytes / 4;
+    if (2 * (int64_t)kBandStageBytes > p.lds_bytes ||
+        (int64_t)CB * (KS - 1) * 32 * nb * 32 * 4 > p.lds_bytes || p.lds_bytes > kConvLdsMaxBytes ||
+        (KS != 4 && KS != 2) || a.rows < 1 || nb * 32 < a.rows * a.wo || (nb - 1) * 32 >= a.rows * a.wo ||
+        (int64_t)a.rows * g.row_len + 3 > 64 * kBandMaxSeg || g.c % (2 * kBandChunk) || g.k % (32 * CB) ||
+        (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho ||
+        (int64_t)g.n * a.nbands * a.nkt != a.grid) {
+        r.fail("fp32 band conv: plan (ks %d, %d rows, nb %d, %lld bytes of LDS)", KS, a.rows, nb,
+               (long long)p.lds_bytes);
         return;
     }
+    if (a.mode != (fused ? kBandGather : (g.ho * g.row_len) % 4 == 0 ? kBandWide : kBandNarrow))
+        r.fail("fp32 band conv: copy mode %d", a.mode);
     std::vector<uint8_t> seen_wg(a.grid, 0);
     for (int b = 0; b < a.grid; ++b) {
         const int bid = a.xcd_remap ? (b & 7) * (a.grid >> 3) + (b >> 3) : b;
         if (bid < 0 || bid >= a.grid || seen_wg[bid]++) {
-            r.fail("fp32 image conv: workgroup %d maps to %d (repeated or out of range)", b, bid);
+            r.fail("fp32 band conv: workgroup %d maps to %d (repeated or out of range)", b, bid);
             return;
         }
     }
-    // staging: holds[float of a stage] = slot << 24 | strip element, or
-    // kZero (a copy wrote zero), or -1 (never written)
-    const int64_t kZero = -2;
-    std::vector<int64_t> holds(stage_b / 4, -1);
-    const int nj = f32img_copies(a.mode);
-    const int per = a.mode == kF32ImgWide ? 4 : 1;      // floats per lane and copy
-    if (a.mode != (fused ? kF32ImgGather : a.plane_strip % 4 == 0 ? kF32ImgWide : kF32ImgNarrow))
-        r.fail("fp32 image conv: copy mode %d", a.mode);
+    const int nj = band_copies(a.mode);
+    const int per = a.mode == kBandWide ? 4 : 1;      // floats per lane and copy
     const uint64_t slab = (uint64_t)g.c * a.plane_src * 4;
     const uint64_t plane_bytes = (uint64_t)a.plane_src * 4;
-    if (slab >= kF32ImgOutside) r.fail("fp32 image conv: image slab of %llu bytes", (unsigned long long)slab);
-    for (int wv = 0; wv < kF32ImgThreads / 64; ++wv)
-        for (int j = 0; j < nj; ++j)
-            for (int lane = 0; lane < 64; ++lane) {
-                const int cc = 2 * wv + (j & 1);
-                const uint32_t off = f32img_source(a, a.mode, FH, j >> 1, lane);
-                const int64_t dst = f32img_dest(a.mode, wv, j) + (int64_t)lane * per * 4;
-                if (dst < (int64_t)cc * kF32ImgSlot * 4 || dst + per * 4 > (int64_t)(cc + 1) * kF32ImgSlot * 4) {
-                    r.fail("fp32 image conv: copy %d of wave %d lane %d writes LDS byte %lld outside slot %d", j, wv, lane,
-                           (long long)dst, cc);
-                    return;
-                }
-                // the last real chunk reads inside the slab; the one past it
-                // (issued, never used) reads only zeros; no offset wraps
-                const uint64_t last = ((uint64_t)(a.nchunks - 1) * kF32ImgChunk + cc) * plane_bytes + off;
-                const uint64_t past = ((uint64_t)a.nchunks * kF32ImgChunk + cc) * plane_bytes + off;
-                if (past >= (uint64_t(1) << 32) || past < slab ||
-                    (off != kF32ImgOutside && (off >= plane_bytes || last + per * 4 > slab))) {
-                    r.fail("fp32 image conv: copy %d of wave %d lane %d reads byte %llu of a %llu-byte slab", j, wv,
-                           lane, (unsigned long long)last, (unsigned long long)slab);
-                    return;
-                }
-                for (int e = 0; e < per; ++e) {
-                    const int64_t f = dst / 4 + e;
-                    const int64_t pos = per == 1 ? (int64_t)(j >> 1) * 64 + lane : (int64_t)(j >> 1) * 256 + lane * 4 + e;
-                    int64_t v = kZero;
-                    if (off != kF32ImgOutside) {
-                        if (!fused && (int64_t)off / 4 + e != pos) {
-                            r.fail("fp32 image conv: strip element %lld copied from %u", (long long)pos, off / 4 + e);
+    if (slab >= kBandOutside) r.fail("fp32 band conv: image slab of %llu bytes", (unsigned long long)slab);
+    const int64_t kZero = -2;
+    std::vector<int64_t> holds(stage_f);
+    std::vector<uint8_t> out((size_t)g.k * g.ho * g.wo, 0);
+    for (int band = 0; band < a.nbands && r.violations == 0; ++band) {
+        // (image 0, channel group 0 of the band: the staging and the reads
+        // do not depend on either)
+        const BandTile t = band_tile(a, band * a.nkt);
+        if (t.band != band || t.img != 0 || t.kt != 0 || t.m0 != band * a.rows || t.nrows < 1 ||
+            t.npix > nb * 32 || (a.mode == kBandWide && t.shift + (int64_t)t.nrows * g.row_len > 64 * kBandMaxSeg)) {
+            r.fail("fp32 band conv: band %d (rows %d + %d, shift %d)", band, t.m0, t.nrows, t.shift);
+            return;
+        }
+        // staging: holds[float of a stage] = slot << 24 | window-tensor
+        // element of the plane, or kZero (a copy wrote zero), or -1
+        std::fill(holds.begin(), holds.end(), -1);
+        for (int wv = 0; wv < kBandThreads / 64; ++wv)
+            for (int j = 0; j < nj; ++j)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int cc = 2 * wv + (j & 1);
+                    const uint32_t off = band_source(a, t, a.mode, FH, j >> 1, lane);
+                    const int64_t dst = band_dest(a.mode, wv, j) + (int64_t)lane * per * 4;
+                    if (dst < (int64_t)cc * kBandSlot * 4 || dst + per * 4 > (int64_t)(cc + 1) * kBandSlot * 4) {
+                        r.fail("fp32 band conv: copy %d of wave %d lane %d writes LDS byte %lld outside slot %d", j,
+                               wv, lane, (long long)dst, cc);
+                        return;
+                    }
+                    // the last real chunk reads inside the slab; the one past
+                    // it (issued, never used) reads only zeros; no offset wraps
+                    const uint64_t last = ((uint64_t)(a.nchunks - 1) * kBandChunk + cc) * plane_bytes + off;
+                    const uint64_t past = ((uint64_t)a.nchunks * kBandChunk + cc) * plane_bytes + off;
+                    if (past >= (uint64_t(1) << 32) || past < slab ||
+                        (off != kBandOutside && (off + per * 4 > plane_bytes || last + per * 4 > slab))) {
+                        r.fail("fp32 band conv: copy %d of wave %d lane %d reads byte %llu of a %llu-byte slab", j,
+                               wv, lane, (unsigned long long)last, (unsigned long long)slab);
+                        return;
+                    }
+                    for (int e = 0; e < per; ++e) {
+                        const int64_t f = dst / 4 + e;
+                        // strip position of this float: band-run element pos
+                        const int64_t pos = per == 1 ? (int64_t)(j >> 1) * 64 + lane
+                                                     : (int64_t)(j >> 1) * 256 + lane * 4 + e - t.shift;
+                        int64_t v = kZero;
+                        if (off != kBandOutside) {
+                            const int64_t elem = (int64_t)t.m0 * g.row_len + pos;   // element of the plane
+                            if (!fused && (int64_t)off / 4 + e != elem) {
+                                r.fail("fp32 band conv: strip position %lld copied from element %u", (long long)pos,
+                                       off / 4 + e);
+                                return;
+                            }
+                            if (fused) {   // the x element of window-tensor element elem (transform's definition)
+                                const int64_t m = elem / g.row_len, k = (elem % g.row_len) / FH, u = elem % FH;
+                                const int64_t yy = m * g.sh + u - g.ph, xx = k - g.pw;
+                                if (pos < 0 || pos >= (int64_t)t.nrows * g.row_len || yy < 0 || yy >= g.h ||
+                                    xx < 0 || xx >= g.w || (int64_t)off / 4 != yy * g.w + xx) {
+                                    r.fail("fp32 band conv: strip position %lld gathered from x element %u",
+                                           (long long)pos, off / 4);
+                                    return;
+                                }
+                            }
+                            v = ((int64_t)cc << 24) + elem;
+                        }
+                        if (holds[f] != -1) {
+                            r.fail("fp32 band conv: LDS float %lld written twice", (long long)f);
                             return;
                         }
-                        if (fused) {   // the x element of window-tensor element pos, from the transform's definition
-                            const int64_t m = pos / g.row_len, k = (pos % g.row_len) / FH, u = pos % FH;
-                            const int64_t yy = m * g.sh + u - g.ph, xx = k - g.pw;
-                            if (yy < 0 || yy >= g.h || xx < 0 || xx >= g.w || (int64_t)off / 4 != yy * g.w + xx) {
-                                r.fail("fp32 image conv: strip position %lld gathered from x element %u", (long long)pos,
-                                       off / 4);
+                        holds[f] = v;
+                    }
+                }
+        // window reads: every tap of every lane's window is the element
+        // Alg. 2 sums (the padding of the fused variant reads a zero copy)
+        for (int wv = 0; wv < kBandThreads / 64 && r.violations == 0; ++wv) {
+            const int ks = wv % KS;
+            for (int lane = 0; lane < 64; ++lane)
+                for (int b = 0; b < nb; ++b) {
+                    int pix = b * 32 + (lane & 31);
+                    if (pix > t.npix - 1) pix = t.npix - 1;
+                    const int64_t m = t.m0 + pix / g.wo, n = pix % g.wo;
+                    for (int pp = 0; pp < PP; ++pp) {
+                        const int cc = 2 * (ks * PP + pp) + (lane >> 5);
+                        for (int tap = 0; tap < T; ++tap) {
+                            const int u = tap / FW, v = tap % FW;
+                            const int64_t f = band_window(a, t, FH, 2 * ks * PP + (lane >> 5), lane, b) / 4 +
+                                              (int64_t)pp * 2 * kBandSlot + (int64_t)v * FH + u;
+                            const int64_t elem = m * g.row_len + (n * g.sw + v) * FH + u;
+                            const int64_t yy = m * g.sh + u - g.ph, xx = n * g.sw + v - g.pw;
+                            const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
+                            const bool ok = f >= 0 && f < stage_f &&
+                                            (holds[f] == ((int64_t)cc << 24) + elem || (fused && pad && holds[f] == kZero));
+                            if (!ok) {
+                                r.fail("fp32 band conv: band %d wave %d lane %d block %d pair %d tap %d reads LDS float "
+                                       "%lld holding %lld, wants element %lld of slot %d", band, wv, lane, b, pp, tap,
+                                       (long long)f, (long long)(f >= 0 && f < stage_f ? holds[f] : -3),
+                                       (long long)elem, cc);
                                 return;
                             }
                         }
-                        v = ((int64_t)cc << 24) + pos;
-                    }
-                    if (holds[f] != -1) {
-                        r.fail("fp32 image conv: LDS float %lld written twice", (long long)f);
-                        return;
-                    }
-                    holds[f] = v;
-                }
-            }
-    // window reads: every tap of every lane's window is the element Alg. 2
-    // sums (the padding of the fused variant reads a zero copy)
-    for (int wv = 0; wv < kF32ImgThreads / 64 && r.violations == 0; ++wv)
-        for (int lane = 0; lane < 64; ++lane)
-            for (int b = 0; b < nb; ++b) {
-                int pix = b * 32 + (lane & 31);
-                if (pix > a.npix - 1) pix = a.npix - 1;
-                const int64_t m = pix / g.wo, n = pix % g.wo;
-                const int cc = 2 * wv + (lane >> 5);
-                for (int t = 0; t < T; ++t) {
-                    const int u = t / FW, v = t % FW;
-                    const int64_t f = f32img_window(a, FH, wv, lane, b) / 4 + (int64_t)v * FH + u;
-                    const int64_t elem = m * g.row_len + (n * g.sw + v) * FH + u;
-                    const int64_t yy = m * g.sh + u - g.ph, xx = n * g.sw + v - g.pw;
-                    const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
-                    const bool ok = f >= 0 && f < stage_b / 4 &&
-                                    (holds[f] == ((int64_t)cc << 24) + elem || (fused && pad && holds[f] == kZero));
-                    if (!ok) {
-                        r.fail("fp32 image conv: wave %d lane %d block %d tap %d reads LDS float %lld holding %lld, wants "
-                               "element %lld of slot %d", wv, lane, b, t, (long long)f,
-                               (long long)(f >= 0 && f < stage_b / 4 ? holds[f] : -3), (long long)elem, cc);
-                        break;
                     }
                 }
-            }
-    // filter loads: the lane's row of the last chunk of the last K tile
-    const int64_t wmax = (((int64_t)(a.nkt - 1) * 32 + 31) * g.c + (a.nchunks - 1) * kF32ImgChunk + 7) * T + T - 1;
-    if (wmax >= g.k * g.c * T) r.fail("fp32 image conv: filter element %lld of %lld", (long long)wmax,
-                                      (long long)(g.k * g.c * T));
-    // partial sums R[wave][channel][pixel] inside the LDS allocation
-    if ((int64_t)((3 * 32 + 31) * nb * 32 + nb * 32) * 4 > p.lds_bytes)
-        r.fail("fp32 image conv: partial sums exceed LDS");
-    // outputs: each (channel, pixel) of an image stored once
-    std::vector<uint8_t> out((size_t)g.k * a.npix, 0);
-    for (int kt = 0; kt < a.nkt; ++kt)
-        for (int tid = 0; tid < std::min(a.npix, kF32ImgThreads); ++tid)
-            for (int ch = 0; ch < 32; ++ch) ++out[(size_t)(kt * 32 + ch) * a.npix + tid];
+        }
+        // outputs of this band (image 0): every channel group, block, pixel
+        for (int kt = 0; kt < a.nkt; ++kt)
+            for (int cb = 0; cb < CB; ++cb)
+                for (int p2 = 0; p2 < nb * 32; ++p2) {
+                    if (p2 >= t.npix) continue;
+                    for (int ch = 0; ch < 32; ++ch) {
+                        const int64_t j = (int64_t)(kt * CB + cb) * 32 + ch;
+                        if (j >= g.k) { r.fail("fp32 band conv: output channel %lld", (long long)j); return; }
+                        ++out[(size_t)j * g.ho * g.wo + (size_t)t.m0 * g.wo + p2];
+                    }
+                }
+    }
+    if (r.violations) return;
     for (size_t i = 0; i < out.size(); ++i)
         if (out[i] != 1) {
-            r.fail("fp32 image conv: output %zu of an image stored %d times", i, (int)out[i]);
+            r.fail("fp32 band conv: output %zu of an image stored %d times", i, (int)out[i]);
             return;
         }
+    // filter rows: the last chunk's pair of the last channel group
+    const int64_t wmax = (((int64_t)(a.nkt - 1) * CB * 32 + CB * 32 - 1) * g.c + (a.nchunks - 1) * kBandChunk + 7) * T + T - 1;
+    if (wmax >= g.k * g.c * T)
+        r.fail("fp32 band conv: filter element %lld of %lld", (long long)wmax, (long long)(g.k * g.c * T));
+    // stage 1, the farthest pair and tap stay inside one LDS read's reach
+    if (kBandStageBytes + (PP - 1) * 2 * kBandSlot * 4 + T * 4 >= 65536)
+        r.fail("fp32 band conv: LDS read offsets exceed 16 bits");
     if (conv_scratch_bytes(g, fused) != 0)
-        r.fail("fp32 image conv: scratch of %lld bytes requested", (long long)conv_scratch_bytes(g, fused));
+        r.fail("fp32 band conv: scratch of %lld bytes requested", (long long)conv_scratch_bytes(g, fused));
 }
 
 void check_conv(const Geometry& g, bool fused_plan, Report& r) {
-    const F32ImgPlan fp = plan_image_f32(g);
+    const F32BandPlan fp = plan_band_f32(g);
     if (fp.ok) {
-        check_conv_image_f32(g, fused_plan, fp, r);
+        check_conv_band_f32(g, fused_plan, fp, r);
         return;
     }
     const ImgPlan ip = plan_image_bf16(g, fused_plan);

@@ -383,100 +383,130 @@ int launch_conv_bf16_image(const Geometry& g, const ImgPlan& p, bool fused, cons
                            const void* w, void* scratch, float* y, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
-// fp32 convolution with one image per workgroup (conv_f32_image.hip)
+// fp32 convolution by bands of output rows (conv_f32_band.hip)
 // ---------------------------------------------------------------------------
-constexpr int kF32ImgThreads = 256;   // 4 waves, each a quarter of every channel chunk
-constexpr int kF32ImgChunk = 8;       // input channels per chunk (2 per wave, one per k-slot)
-constexpr int kF32ImgMinNB = 4;       // 32-pixel blocks per image: 97 ..
-constexpr int kF32ImgMaxNB = 7;       // .. 224 output pixels
-constexpr int kF32ImgMaxSeg = 24;     // 64-element segments per channel strip (1536 elements)
+constexpr int kBandThreads = 256;      // 4 waves
+constexpr int kBandChunk = 8;          // input channels per chunk: 4 pairs, one channel per k-slot
+constexpr int kBandMaxSeg = 24;        // 64-element parts per channel slot (1536 strip elements)
 // LDS floats per channel slot: the longest strip plus 32 banks, so that the
-// two k-slots of a wave (adjacent slots) read different banks
-constexpr int kF32ImgSlot = 64 * kF32ImgMaxSeg + 32;
+// two k-slots of a pair (adjacent slots) start in different banks
+constexpr int kBandSlot = 64 * kBandMaxSeg + 32;
+constexpr int kBandStageBytes = kBandChunk * kBandSlot * 4;   // one chunk of strips
 
-struct F32ImgArgs {
+// How a workgroup copies strips into LDS.
+constexpr int kBandWide = 0;     // window-tensor rows, 16-byte copies (16-byte aligned planes)
+constexpr int kBandNarrow = 1;   // window-tensor rows, 4-byte copies
+constexpr int kBandGather = 2;   // fused: each strip position gathered from x
+
+// Offset that no staging buffer reaches (image slabs are below 2^30 bytes):
+// a buffer load from it reads zero.
+constexpr uint32_t kBandOutside = 0x40000000u;
+
+struct F32BandArgs {
     const float* src;      // window tensor (unfused) or x (fused)
     const float* wt;       // filter, K x C x Fh x Fw
     float* y;
     int c, h, w, k, sh, sw, ph, pw, ho, wo;
     int row_len;           // window-tensor row length L
-    int npix;              // Ho * Wo
-    int plane_strip;       // Ho * L, strip elements per channel
     int plane_src;         // elements per channel plane of src (Ho*L, or H*W)
-    int nkt;               // K / 32
+    int rows;              // output rows per band
+    int nbands;            // bands per image, ceil(Ho / rows)
+    int ks;                // waves that split the reduction of one output (4 or 2)
+    int nkt;               // groups of (4 / ks) * 32 output channels
     int nchunks;           // C / 8
-    int grid;              // workgroups (N * nkt)
-    int xcd_remap;         // place the workgroups of one image on one XCD
-    int mode;              // kF32ImgWide, kF32ImgNarrow or kF32ImgGather
+    int grid;              // workgroups (N * nbands * nkt)
+    int xcd_remap;         // place consecutive workgroups on one XCD
+    int mode;              // kBandWide, kBandNarrow or kBandGather
     FastDiv div_row, div_wo;   // by L, by Wo
 };
 
-struct F32ImgPlan {
-    bool ok = false;
-    int nb = 0;            // 32-pixel blocks per image
-    int64_t lds_bytes = 0, grid = 0;
+// The band of output rows, image and output-channel group of one workgroup.
+struct BandTile {
+    int img, band, kt;
+    int m0, nrows, npix;   // output rows [m0, m0 + nrows), npix = nrows * Wo
+    int shift;             // wide copies: strip element 0 sits at slot position shift
 };
 
-// Offset that no staging buffer of the fp32 one-image kernel reaches (image
-// slabs are below 2^30 bytes): a buffer load from it reads zero.
-constexpr uint32_t kF32ImgOutside = 0x40000000u;
-
-// LDS byte address, in stage 0, of the window start of the pixel of `lane`
-// in pixel block b (k-slot lane / 32 reads channel slot 2*wv + lane / 32);
-// pixels past the image are clamped to its last pixel.
-__host__ __device__ inline uint32_t f32img_window(const F32ImgArgs& a, int fh, int wv, int lane, int b) {
-    int p = b * 32 + (lane & 31);
-    if (p > a.npix - 1) p = a.npix - 1;
-    const int m = (int)fast_div((uint32_t)p, a.div_wo), n = p - m * a.wo;
-    return (uint32_t)((2 * wv + (lane >> 5)) * kF32ImgSlot + m * a.row_len + n * a.sw * fh) * 4u;
+__host__ __device__ inline BandTile band_tile(const F32BandArgs& a, int bid) {
+    BandTile t;
+    t.kt = bid % a.nkt;
+    const int ib = bid / a.nkt;
+    t.band = ib % a.nbands;
+    t.img = ib / a.nbands;
+    t.m0 = t.band * a.rows;
+    t.nrows = a.ho - t.m0 < a.rows ? a.ho - t.m0 : a.rows;
+    t.npix = t.nrows * a.wo;
+    t.shift = a.mode == kBandWide ? (t.m0 * a.row_len) & 3 : 0;
+    return t;
 }
 
-// How a workgroup of the fp32 one-image kernel copies strips into LDS.
-constexpr int kF32ImgWide = 0;     // window-tensor planes, 16-byte copies (Ho*L a multiple of 4)
-constexpr int kF32ImgNarrow = 1;   // window-tensor planes, 4-byte copies
-constexpr int kF32ImgGather = 2;   // fused: each strip position gathered from x
+// LDS byte address, in stage 0, of the window start of the pixel of `lane`
+// in pixel block b, in channel slot `slot`; pixels past the band are
+// clamped to its last pixel (computed, never stored).
+__host__ __device__ inline uint32_t band_window(const F32BandArgs& a, const BandTile& t, int fh, int slot, int lane,
+                                                int b) {
+    int p = b * 32 + (lane & 31);
+    if (p > t.npix - 1) p = t.npix - 1;
+    const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
+    return (uint32_t)(slot * kBandSlot + t.shift + ml * a.row_len + n * a.sw * fh) * 4u;
+}
 
 // Source byte offset, within one channel plane of the staging source, of
-// part s of a slot copy for `lane`, or kF32ImgOutside (reads zero).
-// Wide: strip elements s*256 + 4*lane .. + 3 of the window-tensor plane.
-// Narrow: strip element s*64 + lane.  Gather: strip position s*64 + lane,
-// i.e. window-tensor element (m, k, u) of the plane, read from
-// x[m*sh + u - ph][k - pw] (zero in the padding).
-__host__ __device__ inline uint32_t f32img_source(const F32ImgArgs& a, int mode, int fh, int s, int lane) {
-    if (mode == kF32ImgWide) {
+// part s of a slot copy for `lane`, or kBandOutside (reads zero).  The band's
+// strip is the run of window-tensor rows [m0, m0 + nrows) of the plane.
+// Wide: elements s*256 + 4*lane .. + 3 of the run, counted from `shift`
+// elements before its start (a 16-byte boundary).  Narrow: element
+// s*64 + lane of the run.  Gather: run position s*64 + lane, i.e.
+// window-tensor element (m, k, u), read from x[m*sh + u - ph][k - pw]
+// (zero in the padding).
+__host__ __device__ inline uint32_t band_source(const F32BandArgs& a, const BandTile& t, int mode, int fh, int s,
+                                                int lane) {
+    const int len = t.nrows * a.row_len;
+    if (mode == kBandWide) {
         const int e = s * 256 + lane * 4;
-        return e < a.plane_strip ? (uint32_t)e * 4u : kF32ImgOutside;
+        return e < t.shift + len ? (uint32_t)(t.m0 * a.row_len - t.shift + e) * 4u : kBandOutside;
     }
     const int pos = s * 64 + lane;
-    if (mode == kF32ImgNarrow) return pos < a.plane_strip ? (uint32_t)pos * 4u : kF32ImgOutside;
-    const int m = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - m * a.row_len;
+    if (mode == kBandNarrow) return pos < len ? (uint32_t)(t.m0 * a.row_len + pos) * 4u : kBandOutside;
+    const int ml = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - ml * a.row_len;
     const int k = rem / fh, u = rem - k * fh;
-    const int yy = m * a.sh + u - a.ph, xx = k - a.pw;
-    const bool inside = pos < a.plane_strip && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w;
-    return inside ? (uint32_t)(yy * a.w + xx) * 4u : kF32ImgOutside;
+    const int yy = (t.m0 + ml) * a.sh + u - a.ph, xx = k - a.pw;
+    const bool inside = pos < len && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w;
+    return inside ? (uint32_t)(yy * a.w + xx) * 4u : kBandOutside;
 }
 
 // LDS byte offset, within a stage, of copy j of wave wv: channel slot
 // 2*wv + (j & 1), part j / 2 (256 elements wide, 64 otherwise).
-__host__ __device__ inline uint32_t f32img_dest(int mode, int wv, int j) {
-    return (uint32_t)(((2 * wv + (j & 1)) * kF32ImgSlot) * 4 + (j >> 1) * (mode == kF32ImgWide ? 1024 : 256));
+__host__ __device__ inline uint32_t band_dest(int mode, int wv, int j) {
+    return (uint32_t)(((2 * wv + (j & 1)) * kBandSlot) * 4 + (j >> 1) * (mode == kBandWide ? 1024 : 256));
 }
 
 // Copies per wave and chunk (two channel slots).
-__host__ __device__ constexpr int f32img_copies(int mode) {
-    return mode == kF32ImgWide ? 2 * (kF32ImgMaxSeg / 4) : 2 * kF32ImgMaxSeg;
+__host__ __device__ constexpr int band_copies(int mode) {
+    return mode == kBandWide ? 2 * (kBandMaxSeg / 4) : 2 * kBandMaxSeg;
 }
 
-// The plan of the fp32 one-image-per-workgroup kernel, or !ok when the shape
-// is not one it takes (fp32, 3x3 or 3x5 filter, C a multiple of 16, K of 32,
-// 97 to 224 output pixels per image, at most 1536 strip elements per
-// channel, at least 256 workgroups).  The plan does not depend on fusion, so both
+struct F32BandPlan {
+    bool ok = false;
+    int ks = 0;            // reduction split (4: 32 output channels per workgroup; 2: 64)
+    int rows = 0;          // output rows per band
+    int nb = 0;            // 32-pixel blocks per band
+    int64_t lds_bytes = 0, grid = 0;
+    double eff = 0;        // useful share of the matrix-core work the launch occupies
+};
+
+// The plan of the band kernel, or !ok when the shape is not one it takes
+// (fp32; 3x3 or 3x5 filter; C a multiple of 16, K of 32 (of 64 with the
+// two-way split, 3x3 only); a band of rows whose strips fit a slot and whose
+// pixels fill 4-7 blocks of 32 (12-13 with the two-way split); at most 4
+// rounds of 256 workgroups, and at least 85% of the occupied matrix-core
+// work useful after rounding the grid to whole rounds).  The plan does not depend on fusion, so both
 // variants take a shape or neither.
-F32ImgPlan plan_image_f32(const Geometry& g);
-F32ImgArgs image_args_f32(const Geometry& g, const F32ImgPlan& p, bool fused, const void* src, const void* w,
+F32BandPlan plan_band_f32(const Geometry& g);
+F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
                           float* y);
-int launch_conv_f32_image(const Geometry& g, const F32ImgPlan& p, bool fused, const void* src, const void* w,
-                          float* y, hipStream_t stream);
+int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
+                         float* y, hipStream_t stream);
 
 // Upper bound of the per-channel strip length over all pixel tiles of `bn`
 // pixels: a tile spanning D row boundaries reads D*L + (n1-n0)*sw*Fh + Fw*Fh

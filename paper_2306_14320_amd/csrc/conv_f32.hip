@@ -1197,8 +1197,8 @@ int launch_conv_f32_plan(const Geometry& g, const ConvPlan& p, bool fused, const
 
 int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* w, void* scratch,
                     float* y, hipStream_t stream, char* err, size_t errlen) {
-    const F32ImgPlan ip = plan_image_f32(g);
-    if (ip.ok) return launch_conv_f32_image(g, ip, fused, src, w, y, stream);
+    const F32BandPlan bp = plan_band_f32(g);
+    if (bp.ok) return launch_conv_f32_band(g, bp, fused, src, w, y, stream);
     const ConvPlan p = plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) return launch_conv_plain(g, fused, src, w, y, stream, err, errlen);
     return launch_conv_f32_plan(g, p, fused, src, w, scratch, y, stream, err, errlen);

@@ -183,18 +183,25 @@ def test_launch_plans_in_bounds_on_paper_layers():
                 assert P.im2win_check_plan(d) == 0, (layer["name"], P.im2win_last_error())
 
 
-# Shapes that the fp32 one-image kernel takes (n, c, h, w, k, fh, fw, sh, sw,
-# ph, pw): 97 to 224 output pixels, C a multiple of 16, K of 32, at least 256
-# workgroups of one image x 32 output channels.
-F32_ONE_IMAGE = [
-    (64, 128, 28, 28, 128, 3, 5, 2, 2, 1, 2),   # the rectangular-window layer
-    (128, 256, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # Table 1 Conv11 (144 pixels)
-    (128, 256, 12, 12, 512, 3, 3, 1, 1, 0, 0),  # Table 1 Conv6 (100 pixels)
+# Shapes that the fp32 band kernel takes (n, c, h, w, k, fh, fw, sh, sw, ph,
+# pw): C a multiple of 16, K of 32 (64 with the two-way reduction split), a
+# band of output rows of 97-224 pixels (four-way split) or 353-416 (two-way),
+# at most 4 rounds of 256 workgroups with at least 85% of them useful.
+F32_BANDS = [
+    (64, 128, 28, 28, 128, 3, 5, 2, 2, 1, 2),   # the rectangular-window layer: whole images
+    (32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1),     # the ResNet-style layer: 7-row bands, two-way split
+    (128, 64, 56, 56, 64, 3, 3, 1, 1, 0, 0),    # Table 1 Conv9: ragged last band
+    (128, 128, 28, 28, 128, 3, 3, 1, 1, 0, 0),  # Table 1 Conv10
+    (128, 256, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # Table 1 Conv11
     (2, 16, 28, 28, 4096, 3, 5, 2, 2, 1, 2),
     (8, 32, 14, 14, 1024, 3, 3, 1, 1, 1, 1),
-    (16, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),
+    (16, 16, 13, 13, 512, 3, 3, 1, 1, 0, 0),
     (4, 16, 13, 23, 2048, 3, 5, 1, 2, 0, 1),
-    (3, 32, 29, 15, 3200, 3, 3, 2, 1, 1, 0),
+    (3, 32, 29, 15, 2720, 3, 3, 2, 1, 1, 0),
+    (16, 16, 28, 28, 512, 3, 3, 1, 1, 1, 1),
+    (2, 16, 56, 56, 1024, 3, 3, 1, 1, 1, 1),
+    (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),
+    (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),
 ]
 
 
@@ -203,41 +210,41 @@ def test_conv_kernel_names_on_workloads():
     for wl in workloads.WORKLOADS:
         d = _desc(_wl_shape(wl), _wl_dtype(wl))
         got[wl.name] = (P.im2win_conv_kernel(d, False), P.im2win_conv_kernel(d, True))
-    assert got["rect_3x5_s2_f32"] == ("f32_one_image",) * 2
+    assert got["rect_3x5_s2_f32"] == ("f32_bands",) * 2
+    assert got["resnet_3x3_f32"] == ("f32_bands",) * 2
     assert got["deep_3x3_bf16"] == ("bf16_one_image",) * 2
-    assert got["resnet_3x3_f32"] == ("f32_tiles",) * 2
     assert got["stem_7x7_s2_f32"] == ("f32_tiles",) * 2
     d = P.im2win_desc(1, 3, 4000, 4000, 4, 60, 60, 1, 1, 0, 0, P.IM2WIN_F32)
     assert P.im2win_conv_kernel(d, False) == "per_output"
 
 
 @pytest.mark.parametrize("layout", [0, 1], ids=["padded", "trimmed"])
-@pytest.mark.parametrize("case", F32_ONE_IMAGE, ids=lambda c: "x".join(map(str, c)))
-def test_launch_plans_in_bounds_fp32_one_image(case, layout):
-    """The one-image kernel takes these shapes in both row layouts (and only
-    for fp32), and its replayed staging copies, window reads and stores are in
+@pytest.mark.parametrize("case", F32_BANDS, ids=lambda c: "x".join(map(str, c)))
+def test_launch_plans_in_bounds_fp32_bands(case, layout):
+    """The band kernel takes these shapes in both row layouts (and only for
+    fp32), and its replayed staging copies, window reads and stores are in
     bounds and hold what Alg. 2 sums."""
     d = P.im2win_desc(*case, P.IM2WIN_F32, layout)
-    assert P.im2win_conv_kernel(d, False) == "f32_one_image"
-    assert P.im2win_conv_kernel(d, True) == "f32_one_image"
+    assert P.im2win_conv_kernel(d, False) == "f32_bands"
+    assert P.im2win_conv_kernel(d, True) == "f32_bands"
     assert P.im2win_filter_scratch_bytes(d) == 0
     assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
-    assert P.im2win_conv_kernel(P.im2win_desc(*case, P.IM2WIN_BF16, layout), False) != "f32_one_image"
+    assert P.im2win_conv_kernel(P.im2win_desc(*case, P.IM2WIN_BF16, layout), False) != "f32_bands"
 
 
-def test_fp32_one_image_declines_unsupported_shapes():
-    base = list(F32_ONE_IMAGE[0])
+def test_fp32_bands_decline_unsupported_shapes():
+    base = list(F32_BANDS[0])
     def name(**kw):
         c = dict(zip("n c h w k fh fw sh sw ph pw".split(), base))
         c.update(kw)
         return P.im2win_conv_kernel(P.im2win_desc(*c.values(), P.IM2WIN_F32), False)
-    assert name() == "f32_one_image"
-    assert name(n=63) != "f32_one_image"            # 252 workgroups
-    assert name(c=120) != "f32_one_image"           # C not a multiple of 16
-    assert name(k=112) != "f32_one_image"           # K not a multiple of 32
-    assert name(fh=5, ph=2) != "f32_one_image"      # 5x5 filter
-    assert name(h=12, w=12, ph=0, pw=0) != "f32_one_image"   # 5x4 = 20 pixels
-    assert name(h=34, w=34) != "f32_one_image"      # 17x17 = 289 pixels
+    assert name() == "f32_bands"
+    assert name(n=56) != "f32_bands"            # 224 workgroups: 77% of one round
+    assert name(n=1100) != "f32_bands"          # more than 4 rounds
+    assert name(c=120) != "f32_bands"           # C not a multiple of 16
+    assert name(k=112) != "f32_bands"           # K not a multiple of 32
+    assert name(fh=5, ph=2) != "f32_bands"      # 5x5 filter
+    assert name(h=12, w=12, ph=0, pw=0) != "f32_bands"   # 5x4 = 20 pixels
 
 
 # ---------------------------------------------------------------------------

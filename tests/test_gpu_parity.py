@@ -201,29 +201,31 @@ def test_edge_shapes(case, dtype):
     assert np.array_equal(y_unf, y_fus), "fused and unfused outputs differ"
 
 
-# Shapes that the fp32 one-image kernel takes (at least 256 workgroups of one
-# image x 32 output channels, 97 to 224 output pixels), each in both row
-# layouts; the copy granularity (16-byte or 4-byte pieces of the strips)
-# follows from Ho*L.
-F32_ONE_IMAGE = [
-    (2, 16, 28, 28, 4096, 3, 5, 2, 2, 1, 2),   # 3x5 stride 2, 196 pixels in 7 blocks
+# Shapes that the fp32 band kernel takes (at least 85% of whole rounds of 256
+# workgroups useful), each in both row layouts; the copy granularity (16-byte
+# or 4-byte pieces of the strips) follows from the plane alignment.
+F32_BANDS = [
+    (2, 16, 28, 28, 4096, 3, 5, 2, 2, 1, 2),   # 3x5 stride 2, whole 14x14 images in 7 blocks
     (8, 32, 14, 14, 1024, 3, 3, 1, 1, 1, 1),   # 196 pixels, two chunk pairs, XCD placement
-    (16, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),   # 100 pixels in 4 blocks
+    (16, 16, 13, 13, 512, 3, 3, 1, 1, 0, 0),   # 121 pixels in 4 blocks
     (4, 16, 13, 23, 2048, 3, 5, 1, 2, 0, 1),   # 121 pixels, rows of 75 (4-byte copies)
-    (3, 32, 29, 15, 3200, 3, 3, 2, 1, 1, 0),   # 195 pixels, row stride 2, grid not a multiple of 8
+    (3, 32, 29, 15, 2720, 3, 3, 2, 1, 1, 0),   # 195 pixels, row stride 2, grid not a multiple of 8
+    (2, 16, 56, 56, 1024, 3, 3, 1, 1, 1, 1),   # two-way split: 7-row bands of 56 columns
+    (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),   # two-way split: bands of 14 and 12 rows
+    (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2
 ]
 
 
 @pytest.mark.parametrize("layout", [P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED], ids=["padded", "trimmed"])
-@pytest.mark.parametrize("case", F32_ONE_IMAGE, ids=lambda c: "x".join(map(str, c)))
-def test_fp32_one_image_kernel(case, layout):
+@pytest.mark.parametrize("case", F32_BANDS, ids=lambda c: "x".join(map(str, c)))
+def test_fp32_band_kernel(case, layout):
     """Whole output of both convolutions against the fp64 oracle (Eq. 1),
     fused and unfused bitwise identical, nothing written past the output."""
     n, c, h, w, k, fh, fw, sh, sw, ph, pw = case
     wl, x_cpu, w_cpu = workloads.random_case(sum(case) + layout, n, c, h, w, k, fh, fw, sh, sw, ph, pw, "f32")
-    _label(f"f32-one-image layout={layout}", wl)
+    _label(f"f32-bands layout={layout}", wl)
     d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, P.IM2WIN_F32, layout)
-    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == "f32_one_image"
+    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == "f32_bands"
     assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
     x, wt = x_cpu.to(DEV), w_cpu.to(DEV)
     ho, wo = P.im2win_output_shape(d)
@@ -241,7 +243,7 @@ def test_fp32_one_image_kernel(case, layout):
         outs.append(y.cpu().numpy().astype(np.float64))
     assert np.array_equal(outs[0], outs[1]), "fused and unfused outputs differ"
     ref, ref_abs = oracle.direct_conv(_shape(wl), _f64(x_cpu), _f64(w_cpu), with_abs=True)
-    rel = _assert_close(outs[0], ref, ref_abs, c * fh * fw, "f32", "one-image kernel")
+    rel = _assert_close(outs[0], ref, ref_abs, c * fh * fw, "f32", "band kernel")
     print(f"[parity] rel-L2 {rel:.3e}", flush=True)
 
 
