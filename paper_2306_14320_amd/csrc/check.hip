@@ -597,7 +597,7 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
     const int KS = p.ks, PP = 4 / KS, CB = 4 / KS, nb = p.nb;
     const int64_t stage_f = kBandStageBytes / 4;
     if (2 * (int64_t)kBandStageBytes > p.lds_bytes ||
-        (int64_t)CB * (KS - 1) * 32 * nb * 32 * 4 > p.lds_bytes || p.lds_bytes > kConvLdsMaxBytes ||
+        (int64_t)(KS == 4 ? 4 : 2) * 32 * nb * 32 * 4 > p.lds_bytes || p.lds_bytes > kConvLdsMaxBytes ||
         (KS != 4 && KS != 2) || a.rows < 1 || nb * 32 < a.rows * a.wo || (nb - 1) * 32 >= a.rows * a.wo ||
         (int64_t)a.rows * g.row_len + 3 > 64 * kBandMaxSeg || g.c % (2 * kBandChunk) || g.k % (32 * CB) ||
         (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho ||
@@ -721,9 +721,11 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                 }
         }
         // outputs of this band (image 0): every channel group, block, pixel
+        // (the four-way split stores pixels tid, tid + 256, ... below npix;
+        // the two-way split the pixels of its blocks below npix)
         for (int kt = 0; kt < a.nkt; ++kt)
             for (int cb = 0; cb < CB; ++cb)
-                for (int p2 = 0; p2 < nb * 32; ++p2) {
+                for (int p2 = 0; p2 < (KS == 4 ? t.npix : nb * 32); ++p2) {
                     if (p2 >= t.npix) continue;
                     for (int ch = 0; ch < 32; ++ch) {
                         const int64_t j = (int64_t)(kt * CB + cb) * 32 + ch;

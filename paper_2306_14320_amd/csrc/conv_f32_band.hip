@@ -183,35 +183,57 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
         land();
     }
 
-    // The KS - 1 waves of a block with ks > 0 leave their partial sums in LDS
-    // (R[cb][ks - 1][channel][pixel]); the ks = 0 wave adds them in order,
-    // ((P0 + P1) + P2) + P3, and stores the band's valid pixels.
     constexpr int RP = NB * 32;
     constexpr int RW = 32 * RP;   // floats per partial
-    float* R = S + cb * (KS - 1) * RW;
-    if (ks > 0) {
+    if constexpr (KS == 4) {
+        // All four partial sums go to LDS (R[wave][channel][pixel]); every
+        // thread then adds one pixel's four partials in order,
+        // ((P0 + P1) + P2) + P3, for all 32 channels.
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
-                R[(ks - 1) * RW + ch * RP + b * 32 + col] = acc[b][r];
+                S[wv * RW + ch * RP + b * 32 + col] = acc[b][r];
             }
-    }
-    __syncthreads();
-    if (ks == 0) {
+        __syncthreads();
         const size_t hw = (size_t)a.ho * a.wo;
-        float* yo = a.y + ((size_t)tile.img * a.k + (size_t)(tile.kt * CB + cb) * 32) * hw + (size_t)tile.m0 * a.wo;
+        float* yo = a.y + ((size_t)tile.img * a.k + (size_t)tile.kt * 32) * hw + (size_t)tile.m0 * a.wo;
+        for (int p = tid; p < tile.npix; p += kBandThreads) {
+#pragma unroll 4
+            for (int ch = 0; ch < 32; ++ch) {
+                const int e = ch * RP + p;
+                yo[(size_t)ch * hw + p] = ((S[e] + S[e + RW]) + S[e + 2 * RW]) + S[e + 3 * RW];
+            }
+        }
+    } else {
+        // The ks = 1 wave of each channel block leaves its partial sums in
+        // LDS (R[block][channel][pixel]); the ks = 0 wave adds them, P0 + P1,
+        // and stores the band's valid pixels from its registers.
+        float* R = S + cb * RW;
+        if (ks > 0) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            const int p = b * 32 + col;
+            for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
-                float v = acc[b][r];
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    R[ch * RP + b * 32 + col] = acc[b][r];
+                }
+        }
+        __syncthreads();
+        if (ks == 0) {
+            const size_t hw = (size_t)a.ho * a.wo;
+            float* yo = a.y + ((size_t)tile.img * a.k + (size_t)(tile.kt * CB + cb) * 32) * hw +
+                        (size_t)tile.m0 * a.wo;
 #pragma unroll
-                for (int k = 1; k < KS; ++k) v += R[(k - 1) * RW + ch * RP + p];
-                if (p < tile.npix) yo[(size_t)ch * hw + p] = v;
+            for (int b = 0; b < NB; ++b) {
+                const int p = b * 32 + col;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    const float v = acc[b][r] + R[ch * RP + p];
+                    if (p < tile.npix) yo[(size_t)ch * hw + p] = v;
+                }
             }
         }
     }
@@ -283,7 +305,9 @@ F32BandPlan plan_band_f32(const Geometry& g) {
         }
     }
     if (best.eff < 0.85) return F32BandPlan();
-    const int64_t red = (int64_t)(4 / best.ks) * (best.ks - 1) * 32 * best.nb * 32 * 4;
+    // partial sums: four per block of 32 channels (four-way split), or one
+    // per block of the two
+    const int64_t red = (int64_t)(best.ks == 4 ? 4 : 2) * 32 * best.nb * 32 * 4;
     best.lds_bytes = std::max<int64_t>(2 * kBandStageBytes, red);
     if (best.lds_bytes > kConvLdsMaxBytes) return F32BandPlan();
     best.ok = true;
