@@ -751,7 +751,229 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
         r.fail("fp32 band conv: scratch of %lld bytes requested", (long long)conv_scratch_bytes(g, fused));
 }
 
+// fp32 small-C band kernel: the workgroup map, and for every band every
+// staging copy (source inside the image slab or the zero-reading offset, LDS
+// destination inside its channel slot or raw row, each LDS float written
+// once; fused, the expansion of the raw rows into the strips), every window
+// read of every wave, lane, k-step and pixel block (the element Alg. 2
+// multiplies with the weight that step carries; the zero-weight duplicate
+// row reads an element of the same window), the filter reads and each
+// output stored once.
+void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPlan& p, Report& r) {
+    const F32BandArgs a = band_args_small_c_f32(g, p, fused, nullptr, nullptr, nullptr);
+    const int C = (int)g.c, FH = (int)g.fh, FW = (int)g.fw, T = FH * FW;
+    const int HU = (FH + 1) / 2, S = C * HU * FW, SW = (S + 1) / 2, nb = p.nb;
+    const int64_t slot_bytes = (int64_t)a.slotf * 4;
+    const int64_t rb_f = (int64_t)C * a.rrows * a.rpitch;   // floats of one raw-row buffer (fused)
+    if (C != kSmallCChannels || p.ks != 2 || p.lds_bytes > kConvLdsMaxBytes ||
+        p.lds_bytes != std::max(2 * C * slot_bytes, C * slot_bytes + 2 * rb_f * 4) + (int64_t)2 * 32 * nb * 32 * 4 ||
+        a.rrows != (a.rows - 1) * g.sh + g.fh || a.rpitch < g.w || a.rpitch % 4 || (a.rawwide && g.w % 4) ||
+        a.rparts * 64 * (a.rawwide ? 4 : 1) < g.w || a.rows * g.row_len > 256 * kSmallCExpand || nb * 32 < a.rows * a.wo ||
+        (nb - 1) * 32 >= a.rows * a.wo || g.k % 64 || a.nkt * 64 != g.k || (int64_t)g.n * a.nbands * a.nkt != a.total ||
+        (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho || a.per_wg < 1 ||
+        (int64_t)a.grid * a.per_wg < a.total || (int64_t)(a.grid - 1) * a.per_wg >= a.total) {
+        r.fail("fp32 small-C band conv: plan (%d rows, nb %d, slot %d floats, %lld bytes of LDS, %d x %d bands)", a.rows,
+               nb, a.slotf, (long long)p.lds_bytes, a.grid, a.per_wg);
+        return;
+    }
+    // workgroup w walks bands [w*per_wg, min((w+1)*per_wg, total)): every
+    // band once, alternating between the two strip buffers
+    std::vector<uint8_t> seen_band(a.total, 0);
+    for (int wg = 0; wg < a.grid; ++wg)
+        for (int b = wg * a.per_wg; b < std::min((wg + 1) * a.per_wg, a.total); ++b)
+            if (seen_band[b]++) {
+                r.fail("fp32 small-C band conv: band %d walked twice", b);
+                return;
+            }
+    for (int b = 0; b < a.total; ++b)
+        if (!seen_band[b]) {
+            r.fail("fp32 small-C band conv: band %d never walked", b);
+            return;
+        }
+    const int per = a.mode == kBandWide ? 4 : 1;
+    const int part = a.mode == kBandWide ? 256 : 64;
+    const uint64_t slab = (uint64_t)C * a.plane_src * 4;
+    const int64_t kZero = -2;
+    std::vector<int64_t> holds((size_t)C * a.slotf);
+    std::vector<int64_t> raw((size_t)rb_f);
+    std::vector<uint8_t> out((size_t)g.k * g.ho * g.wo, 0);
+    // Unfused: the strip copies of band t, each strip position written once
+    // with (channel << 24) + its window-tensor element, or zero past the strip.
+    auto stage_strips = [&](const BandTile& t) {
+        const int np = smallc_parts(a, t);
+        if ((int64_t)np * part > a.slotf) {
+            r.fail("fp32 small-C band conv: %d parts of %d floats in a slot of %d", np, part, a.slotf);
+            return false;
+        }
+        for (int j = 0; j < C * np; ++j)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int c = j / np, sp = j % np;
+                const uint32_t off = band_source(a, t, a.mode, FH, sp, lane);
+                const int64_t dst = (int64_t)c * a.slotf + (int64_t)sp * part + (int64_t)lane * per;   // float index
+                if (dst < (int64_t)c * a.slotf || dst + per > (int64_t)(c + 1) * a.slotf) {
+                    r.fail("fp32 small-C band conv: copy %d lane %d writes LDS float %lld outside slot %d", j, lane,
+                           (long long)dst, c);
+                    return false;
+                }
+                if (off != kBandOutside && ((uint64_t)c * a.plane_src * 4 + off + per * 4 > slab ||
+                                            off + per * 4 > (uint64_t)a.plane_src * 4)) {
+                    r.fail("fp32 small-C band conv: copy %d lane %d reads byte %u of a plane", j, lane, off);
+                    return false;
+                }
+                for (int e = 0; e < per; ++e) {
+                    const int64_t pos = per == 1 ? (int64_t)sp * 64 + lane : (int64_t)sp * 256 + lane * 4 + e - t.shift;
+                    int64_t v = kZero;
+                    if (off != kBandOutside) {
+                        const int64_t elem = (int64_t)t.m0 * g.row_len + pos;
+                        if ((int64_t)off / 4 + e != elem) {
+                            r.fail("fp32 small-C band conv: strip position %lld copied from element %u", (long long)pos,
+                                   off / 4 + e);
+                            return false;
+                        }
+                        v = ((int64_t)c << 24) + elem;
+                    }
+                    if (holds[dst + e] != -1) {
+                        r.fail("fp32 small-C band conv: LDS float %lld written twice", (long long)(dst + e));
+                        return false;
+                    }
+                    holds[dst + e] = v;
+                }
+            }
+        return true;
+    };
+    // Fused: the raw-row copies of band t (each raw float written once with
+    // (channel << 24) + its x element, or zero for rows outside the image),
+    // then the expansion of every strip position below the band's length
+    // from them, through the offsets the kernel computes once.
+    auto stage_raw = [&](const BandTile& t) {
+        std::fill(raw.begin(), raw.end(), -1);
+        const int rper = a.rawwide ? 4 : 1;
+        const int64_t y0 = (int64_t)t.m0 * g.sh - g.ph;
+        for (int j = 0; j < C * a.rrows * a.rparts; ++j)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int row = j / a.rparts, pr = j % a.rparts, c = row / a.rrows, rr = row % a.rrows;
+                const int64_t yy = y0 + rr, xx = (int64_t)pr * 64 * rper + lane * rper;
+                if (xx >= g.w) continue;   // lane masked off
+                const int64_t dst = (int64_t)row * a.rpitch + xx;
+                if (xx + rper > g.w || dst + rper > rb_f) {
+                    r.fail("fp32 small-C band conv: raw copy %d lane %d writes float %lld past its row", j, lane,
+                           (long long)dst);
+                    return false;
+                }
+                const bool in = yy >= 0 && yy < g.h;
+                if (in && ((uint64_t)((c * g.h + yy) * g.w + xx) * 4 + rper * 4 > slab)) {
+                    r.fail("fp32 small-C band conv: raw copy %d lane %d reads past the image", j, lane);
+                    return false;
+                }
+                for (int e = 0; e < rper; ++e) {
+                    if (raw[dst + e] != -1) {
+                        r.fail("fp32 small-C band conv: raw float %lld written twice", (long long)(dst + e));
+                        return false;
+                    }
+                    raw[dst + e] = in ? ((int64_t)c << 24) + yy * g.w + xx + e : kZero;
+                }
+            }
+        const int64_t len = (int64_t)t.nrows * g.row_len;
+        for (int64_t pos = 0; pos < len; ++pos) {
+            const int ml = (int)fast_div((uint32_t)pos, a.div_row);
+            if (ml != pos / g.row_len || pos >= 256 * kSmallCExpand) {
+                r.fail("fp32 small-C band conv: strip position %lld expanded as row %d", (long long)pos, ml);
+                return false;
+            }
+            const int64_t rem = pos - (int64_t)ml * g.row_len, k = rem / FH, u = rem % FH, xx = k - g.pw;
+            const int64_t src = xx >= 0 && xx < g.w ? ((int64_t)ml * g.sh + u) * a.rpitch + xx : -1;
+            for (int c = 0; c < C; ++c) {
+                int64_t v = kZero;
+                if (src >= 0) {
+                    v = src < a.rrows * a.rpitch ? raw[(size_t)(c * a.rrows * a.rpitch + src)] : -1;
+                    if (v == -1) {
+                        r.fail("fp32 small-C band conv: strip position %lld expanded from raw float %lld never copied",
+                               (long long)pos, (long long)src);
+                        return false;
+                    }
+                }
+                holds[(size_t)c * a.slotf + pos] = v;
+            }
+        }
+        return true;
+    };
+    for (int band = 0; band < a.nbands && r.violations == 0; ++band) {
+        const BandTile t = smallc_tile(a, band);   // image 0, output-channel group 0
+        if (t.band != band || t.img != 0 || t.kt != 0 || t.nrows < 1 || t.npix > nb * 32) {
+            r.fail("fp32 small-C band conv: band %d", band);
+            return;
+        }
+        std::fill(holds.begin(), holds.end(), -1);
+        if (!fused && !stage_strips(t)) return;
+        if (fused && !stage_raw(t)) return;
+        for (int wv = 0; wv < kBandThreads / 64 && r.violations == 0; ++wv) {
+            const int ks = wv & 1, nq = ks == 0 ? SW : S - SW;
+            for (int lane = 0; lane < 64; ++lane)
+                for (int b = 0; b < nb; ++b) {
+                    int pix = b * 32 + (lane & 31);
+                    if (pix > t.npix - 1) pix = t.npix - 1;
+                    const int64_t m = t.m0 + pix / g.wo, n = pix % g.wo;
+                    const int sl = lane >> 5;
+                    for (int i = 0; i < nq; ++i) {
+                        const int q = ks * SW + i, c = q / (HU * FW), rr = q % (HU * FW), u = rr / FW, v = rr % FW;
+                        const int uu = u + sl * (FH - HU);   // the filter row this slot multiplies
+                        const int64_t f = (int64_t)c * a.slotf + smallc_window(a, t, FH, lane, b) / 4 + (int64_t)v * FH + u;
+                        const int64_t yy = m * g.sh + uu - g.ph, xx = n * g.sw + v - g.pw;
+                        const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
+                        // unfused: the window-tensor element; fused: the x element, zero in the padding
+                        const int64_t elem = fused ? yy * g.w + xx : m * g.row_len + (n * g.sw + v) * FH + uu;
+                        const int64_t want = fused && pad ? kZero : ((int64_t)c << 24) + elem;
+                        const bool ok = f >= 0 && f < (int64_t)C * a.slotf && uu < FH && holds[f] == want;
+                        if (!ok) {
+                            r.fail("fp32 small-C band conv: band %d wave %d lane %d block %d step %d reads LDS float "
+                                   "%lld holding %lld, wants element %lld of channel %d", band, wv, lane, b, q,
+                                   (long long)f, (long long)(f >= 0 && f < (int64_t)C * a.slotf ? holds[f] : -3),
+                                   (long long)elem, c);
+                            return;
+                        }
+                    }
+                }
+        }
+        for (int kt = 0; kt < a.nkt; ++kt)
+            for (int cb = 0; cb < 2; ++cb)
+                for (int p2 = 0; p2 < t.npix; ++p2)
+                    for (int ch = 0; ch < 32; ++ch)
+                        ++out[(size_t)((kt * 2 + cb) * 32 + ch) * g.ho * g.wo + (size_t)t.m0 * g.wo + p2];
+    }
+    if (r.violations) return;
+    for (size_t i = 0; i < out.size(); ++i)
+        if (out[i] != 1) {
+            r.fail("fp32 small-C band conv: output %zu of an image stored %d times", i, (int)out[i]);
+            return;
+        }
+    // outputs go through a buffer resource over y: valid offsets inside it,
+    // the dropped-store offset (plus any channel) past its end, no wrap
+    const uint64_t y_bytes = (uint64_t)g.n * g.k * g.ho * g.wo * 4;
+    if (y_bytes > kBandOutside || (uint64_t)kBandOutside + 31ull * g.ho * g.wo * 4 >= (uint64_t(1) << 32))
+        r.fail("fp32 small-C band conv: y of %llu bytes against the dropped-store offset", (unsigned long long)y_bytes);
+    // every (filter row, column) of every channel is multiplied exactly once
+    // per output: slot 0 rows u < HU, slot 1 rows u + Fh - HU >= HU
+    std::vector<int> used((size_t)C * T, 0);
+    for (int q = 0; q < S; ++q)
+        for (int sl = 0; sl < 2; ++sl) {
+            const int c = q / (HU * FW), rr = q % (HU * FW), u = rr / FW, v = rr % FW, uu = u + sl * (FH - HU);
+            if (sl == 0 || uu >= HU) ++used[(size_t)(c * FH + uu) * FW + v];
+        }
+    for (size_t i = 0; i < used.size(); ++i)
+        if (used[i] != 1) {
+            r.fail("fp32 small-C band conv: filter element %zu multiplied %d times", i, used[i]);
+            return;
+        }
+    if (conv_scratch_bytes(g, fused) != 0)
+        r.fail("fp32 small-C band conv: scratch of %lld bytes requested", (long long)conv_scratch_bytes(g, fused));
+}
+
 void check_conv(const Geometry& g, bool fused_plan, Report& r) {
+    const F32BandPlan sp = plan_band_small_c_f32(g);
+    if (sp.ok && !plan_band_f32(g).ok) {
+        check_conv_band_small_c_f32(g, fused_plan, sp, r);
+        return;
+    }
     const F32BandPlan fp = plan_band_f32(g);
     if (fp.ok) {
         check_conv_band_f32(g, fused_plan, fp, r);

@@ -1162,7 +1162,7 @@ bool bf16_packed(const ConvPlan& p, bool fused) { return fused ? p.fused_fast !=
 
 int64_t conv_scratch_bytes(const Geometry& g, bool fused) {
     if (plan_image_bf16(g, fused).ok) return g.k * g.c * g.taps * 2;
-    if (plan_band_f32(g).ok) return 0;   // reads the filter as given
+    if (plan_band_f32(g).ok || plan_band_small_c_f32(g).ok) return 0;   // read the filter as given
     const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused) : plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) return -1;
     if (p.kind == ConvPlan::kF32Lds) return filter_scratch_f32(g, p);
@@ -1172,6 +1172,7 @@ int64_t conv_scratch_bytes(const Geometry& g, bool fused) {
 const char* conv_kernel_name(const Geometry& g, bool fused) {
     if (plan_image_bf16(g, fused).ok) return "bf16_one_image";
     if (plan_band_f32(g).ok) return "f32_bands";
+    if (plan_band_small_c_f32(g).ok) return "f32_bands_small_c";
     const ConvPlan p = g.elem == 2 ? plan_conv_bf16(g, fused) : plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) return "per_output";
     if (g.elem == 2) return p.kind == ConvPlan::kF32Lds ? "bf16_widened_tiles" : "bf16_tiles";

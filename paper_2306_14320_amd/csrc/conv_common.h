@@ -406,7 +406,7 @@ struct F32BandArgs {
     const float* src;      // window tensor (unfused) or x (fused)
     const float* wt;       // filter, K x C x Fh x Fw
     float* y;
-    int c, h, w, k, sh, sw, ph, pw, ho, wo;
+    int n, c, h, w, k, sh, sw, ph, pw, ho, wo;
     int row_len;           // window-tensor row length L
     int plane_src;         // elements per channel plane of src (Ho*L, or H*W)
     int rows;              // output rows per band
@@ -417,6 +417,11 @@ struct F32BandArgs {
     int grid;              // workgroups (N * nbands * nkt)
     int xcd_remap;         // place consecutive workgroups on one XCD
     int mode;              // kBandWide, kBandNarrow or kBandGather
+    int slotf;             // small-C kernel: LDS floats per channel slot
+    int total;             // small-C kernel: bands (x channel groups) of the layer
+    int per_wg;            // small-C kernel: consecutive bands per workgroup
+    int rrows, rpitch;     // small-C fused: raw input rows per band, LDS floats per raw row
+    int rawwide, rparts;   // small-C fused: raw rows by 16-byte copies; copies per row
     FastDiv div_row, div_wo;   // by L, by Wo
 };
 
@@ -507,6 +512,58 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
                           float* y);
 int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
                          float* y, hipStream_t stream);
+
+// The band kernel for layers with few input channels (conv_f32_band.hip):
+// all C channels' strips of a band in LDS at once (one slot of slotf floats
+// per channel, two buffers), 64 output channels per workgroup, the two
+// k-slots of an MFMA holding the top and the bottom half of the filter rows,
+// two waves per block of 32 output channels splitting the k-steps; one
+// persistent workgroup per CU walks through per_wg consecutive bands.
+constexpr int kSmallCChannels = 3;          // C the kernels are built for
+constexpr int kSmallCExpand = 16;           // fused: strip positions per thread and channel (4096 per strip)
+
+// Band bid of the small-C kernel: output-channel group slowest, so that a
+// workgroup's run of consecutive bands shares one filter.
+__host__ __device__ inline BandTile smallc_tile(const F32BandArgs& a, int bid) {
+    BandTile t;
+    const int per_kt = a.n * a.nbands;
+    t.kt = bid / per_kt;
+    const int ib = bid - t.kt * per_kt;
+    t.img = ib / a.nbands;
+    t.band = ib - t.img * a.nbands;
+    t.m0 = t.band * a.rows;
+    t.nrows = a.ho - t.m0 < a.rows ? a.ho - t.m0 : a.rows;
+    t.npix = t.nrows * a.wo;
+    t.shift = a.mode == kBandWide ? (t.m0 * a.row_len) & 3 : 0;
+    return t;
+}
+
+// LDS byte offset, within a channel slot, of the window start of the pixel of
+// `lane` in pixel block b; k-slot lane / 32 starts Fh - ceil(Fh/2) filter rows
+// (positions) further.  Pixels past the band are clamped to its last pixel.
+__host__ __device__ inline uint32_t smallc_window(const F32BandArgs& a, const BandTile& t, int fh, int lane, int b) {
+    int p = b * 32 + (lane & 31);
+    if (p > t.npix - 1) p = t.npix - 1;
+    const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
+    return (uint32_t)(t.shift + ml * a.row_len + n * a.sw * fh + (lane >> 5) * (fh - (fh + 1) / 2)) * 4u;
+}
+
+// Parts (copies of 256 elements wide, 64 otherwise) of one channel slot.
+__host__ __device__ inline int smallc_parts(const F32BandArgs& a, const BandTile& t) {
+    const int len = t.nrows * a.row_len;
+    return a.mode == kBandWide ? (t.shift + len + 255) / 256 : (len + 63) / 64;
+}
+
+// The plan of the small-C band kernel, or !ok (fp32; C = 3; 7x7 filter; K a
+// multiple of 64; a band of rows whose pixels fill 4-7 blocks of 32 and whose
+// three strips, twice, fit with the partial sums in LDS; at least 75% of the
+// occupied matrix-core work useful, counting ceil(bands / 256) bands per
+// workgroup).  Independent of fusion.
+F32BandPlan plan_band_small_c_f32(const Geometry& g);
+F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
+                                  const void* w, float* y);
+int launch_conv_f32_band_small_c(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
+                                 const void* w, float* y, hipStream_t stream);
 
 // Upper bound of the per-channel strip length over all pixel tiles of `bn`
 // pixels: a tile spanning D row boundaries reads D*L + (n1-n0)*sw*Fh + Fw*Fh

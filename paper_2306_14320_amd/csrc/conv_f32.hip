@@ -1199,6 +1199,8 @@ int launch_conv_f32(const Geometry& g, bool fused, const void* src, const void* 
                     float* y, hipStream_t stream, char* err, size_t errlen) {
     const F32BandPlan bp = plan_band_f32(g);
     if (bp.ok) return launch_conv_f32_band(g, bp, fused, src, w, y, stream);
+    const F32BandPlan sp = plan_band_small_c_f32(g);
+    if (sp.ok) return launch_conv_f32_band_small_c(g, sp, fused, src, w, y, stream);
     const ConvPlan p = plan_conv_f32(g);
     if (p.kind == ConvPlan::kNone) return launch_conv_plain(g, fused, src, w, y, stream, err, errlen);
     return launch_conv_f32_plan(g, p, fused, src, w, scratch, y, stream, err, errlen);

@@ -50,6 +50,10 @@ __device__ inline __amdgpu_buffer_rsrc_t band_rsrc(const void* p, uint32_t bytes
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
+// Element r of a vector, by value (a bit cast of the element expression
+// itself compiles to element 0).
+__device__ inline float elem(const f32x16& v, int r) { return v[r]; }
+
 // Scheduling fence that keeps global/buffer memory accesses where they are
 // issued while LDS reads and MFMAs may still interleave across it.
 #define BAND_PIN_VMEM() __builtin_amdgcn_sched_barrier(0x0001 | 0x0002 | 0x0004 | 0x0008 | 0x0080 | 0x0100 | 0x0200)
@@ -239,6 +243,287 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
     }
 }
 
+// Layers with few input channels (the 7x7 stem layers, C = 3): the whole
+// reduction of a band is C*Fh*Fw elements, so a band's C strips are staged at
+// once.  The kernel is persistent: one workgroup per CU walks through a run
+// of consecutive bands (same output channels and image, neighbouring rows),
+// with the strips of band b + 1 copied into a second LDS buffer while band b
+// is multiplied, and band b - 1's outputs stored from registers between
+// band b's MFMAs, so that no phase of a band waits for memory.  The filter
+// values stay in registers across the run; they are reloaded only where the
+// run crosses into the next group of output channels.  The MFMA's
+// two k-slots take filter rows u and u + Fh - ceil(Fh/2) of one channel and
+// tap column (one LDS read: the second slot is the first plus
+// Fh - ceil(Fh/2) positions), u < ceil(Fh/2); for odd Fh the middle row
+// comes up in both slots and the second slot's copy gets zero weights, so
+// every read stays inside the pixel's window.  Waves (cb, ks): 2 blocks of 32
+// output channels x 2 halves of the C*ceil(Fh/2)*Fw k-steps.
+template <int C, int FH, int FW, int NB, int MODE>
+__global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(F32BandArgs a) {
+    constexpr int HU = (FH + 1) / 2;
+    constexpr int S = C * HU * FW;      // k-steps of the whole reduction
+    constexpr int SW = (S + 1) / 2;     // k-steps of the first half (the second takes S - SW)
+    constexpr int RP = NB * 32;
+    constexpr int RW = 32 * RP;         // floats of one block's partial sums
+    constexpr int NOUT = NB * 16;       // output registers per lane
+    constexpr int SPS = (2 * NOUT + SW - 1) / SW;   // stores issued per k-step (done halfway through)
+    constexpr bool GATHER = MODE == kBandGather;
+    extern __shared__ __align__(16) float L[];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int cb = wv >> 1, ks = wv & 1;
+    const int slot = lane >> 5, col = lane & 31;
+    // LDS: unfused, two strip buffers; fused, one strip buffer and two
+    // buffers of raw input rows; then the partial sums of the two blocks
+    const int buf_f = C * a.slotf;                  // floats per strip buffer
+    const int rb_f = C * a.rrows * a.rpitch;        // floats per raw-row buffer (fused)
+    float* R = L + (GATHER ? buf_f + 2 * rb_f : 2 * buf_f) + cb * RW;
+    const int b0 = (int)blockIdx.x * a.per_wg;
+    const int b1 = b0 + a.per_wg < a.total ? b0 + a.per_wg : a.total;
+    const __amdgpu_buffer_rsrc_t wres = band_rsrc(a.wt, (uint32_t)((size_t)a.k * C * FH * FW * 4));
+    const size_t img_elems = (size_t)C * a.plane_src;
+
+    // Unfused: the C strips of band bid (runs of the window tensor) into
+    // strip buffer buf, parts of 256 (wide) or 64 elements spread over the 4
+    // waves; copies past the strip read zeros.
+    auto issue_strips = [&](int bid, int buf) {
+        const BandTile t = smallc_tile(a, bid);
+        const __amdgpu_buffer_rsrc_t sres = band_rsrc(a.src + (size_t)t.img * img_elems, (uint32_t)(img_elems * 4));
+        const int np = smallc_parts(a, t);
+        for (int j = wv; j < C * np; j += 4) {
+            const int c = j / np, sp = j - c * np;
+            const uint32_t off = band_source(a, t, MODE, FH, sp, lane);
+            char* dst = reinterpret_cast<char*>(L) + (buf * buf_f + c * a.slotf + sp * (MODE == kBandWide ? 256 : 64)) * 4;
+            const uint32_t voff = off == kBandOutside ? off : off + (uint32_t)(c * a.plane_src * 4);
+#if defined(__HIP_DEVICE_COMPILE__)   // (16-byte LDS copies exist on gfx950 only; the host pass checks them too)
+            if constexpr (MODE == kBandWide)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
+#endif
+        }
+    };
+    // Fused: the rrows input rows of band bid (rows m0*sh - ph .. , zero
+    // outside the image) of the C channels into raw buffer buf, one row per
+    // copy (16-byte pieces, or 4-byte ones when rows are not whole vectors).
+    auto issue_raw = [&](int bid, int buf) {
+        const BandTile t = smallc_tile(a, bid);
+        const __amdgpu_buffer_rsrc_t sres = band_rsrc(a.src + (size_t)t.img * img_elems, (uint32_t)(img_elems * 4));
+        const int y0 = t.m0 * a.sh - a.ph;
+        const int per = a.rawwide ? 4 : 1;
+        for (int j = wv; j < C * a.rrows * a.rparts; j += 4) {
+            const int row = j / a.rparts, pr = j - row * a.rparts;
+            const int c = row / a.rrows, r = row - c * a.rrows, yy = y0 + r;
+            const int xx = pr * 64 * per + lane * per;   // first column of this lane
+            if (xx < a.w) {
+                const uint32_t voff = yy >= 0 && yy < a.h ? (uint32_t)(((c * a.h + yy) * a.w + xx) * 4) : kBandOutside;
+                char* dst = reinterpret_cast<char*>(L) + (buf_f + buf * rb_f + row * a.rpitch + pr * 64 * per) * 4;
+#if defined(__HIP_DEVICE_COMPILE__)
+                if (a.rawwide)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
+#endif
+            }
+        }
+    };
+    // Fused: where strip position tid + 256*q of a channel comes from in the
+    // raw rows of its band (raw row ml*sh + u, column k - pw), or -1 for the
+    // zero columns of the padding; the same for every band.
+    int exo[GATHER ? kSmallCExpand : 1];
+    if constexpr (GATHER) {
+#pragma unroll
+        for (int q = 0; q < kSmallCExpand; ++q) {
+            const int pos = tid + 256 * q;
+            const int ml = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - ml * a.row_len;
+            const int k = rem / FH, u = rem - k * FH, xx = k - a.pw;
+            exo[q] = xx >= 0 && xx < a.w ? (ml * a.sh + u) * a.rpitch + xx : -1;
+        }
+    }
+    // Fused: the band's strips from raw buffer buf into the strip buffer
+    // (the window tensor's own positions, as the unfused variant copies them).
+    auto expand = [&](int buf, int len) {
+        const float* raw = L + buf_f + buf * rb_f;
+#pragma unroll
+        for (int q = 0; q < kSmallCExpand; ++q) {
+            const int pos = tid + 256 * q;
+            if (pos < len) {
+#pragma unroll
+                for (int c = 0; c < C; ++c)
+                    L[c * a.slotf + pos] = exo[q] >= 0 ? raw[c * a.rrows * a.rpitch + exo[q]] : 0.0f;
+            }
+        }
+    };
+    // Filter values of this wave's k-steps q = ks*SW + i = (c, u, v) for the
+    // output channels of group kt: slot 0 row u, slot 1 row u + Fh - HU (zero
+    // where that row is also slot 0's, and past the last step).  (q, c, u, v)
+    // are compile-time per half, so each load is a per-lane base plus an
+    // immediate, and the zero-weight duplicate row a select.
+    auto load_filter_half = [&](auto ks_tag, int kt, float (&f)[SW]) {
+        constexpr int KSI = decltype(ks_tag)::value;
+        const int kout = (kt * 2 + cb) * 32 + col;
+        const uint32_t base = (uint32_t)((kout * C * FH + slot * (FH - HU)) * FW * 4);
+#pragma unroll
+        for (int i = 0; i < SW; ++i) {
+            const int q = KSI * SW + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
+            if (q >= S) {
+                f[i] = 0.0f;
+                continue;
+            }
+            uint32_t off = base + (uint32_t)(((c * FH + u) * FW + v) * 4);
+            if (u + (FH - HU) < HU) off = slot ? kBandOutside : off;   // slot 1 would repeat a slot-0 row
+            f[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, off, 0, 0));
+        }
+    };
+    auto load_filter = [&](int kt, float (&f)[SW]) {
+        if (ks == 0)
+            load_filter_half(std::integral_constant<int, 0>(), kt, f);
+        else
+            load_filter_half(std::integral_constant<int, 1>(), kt, f);
+    };
+
+    // y through a buffer resource: a store whose offset lies past the end
+    // (pixels past the band, or no previous band yet) is dropped
+    const size_t hw = (size_t)a.ho * a.wo;
+    const __amdgpu_buffer_rsrc_t yres = band_rsrc(a.y, (uint32_t)((size_t)a.n * a.k * hw * 4));
+    float fa[SW];
+    f32x16 acc[NB], out[NB];
+    // byte offset in y of the previous band's channel 0, pixel (lane, block);
+    // the channel adds ch*hw*4 (scalar)
+    uint32_t ybase[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        ybase[b] = kBandOutside;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) out[b][r] = 0.0f;
+    }
+
+    int kt_loaded = smallc_tile(a, b0).kt;
+    load_filter(kt_loaded, fa);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    if constexpr (GATHER)
+        issue_raw(b0, 0);
+    else
+        issue_strips(b0, 0);
+    for (int bid = b0; bid < b1; ++bid) {
+        const int cur = (bid - b0) & 1;
+        // band bid's strips (raw rows) have landed, and the stores of band
+        // bid - 2; every wave is done with the buffers band bid - 1 read and
+        // with R
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        const BandTile tile = smallc_tile(a, bid);
+        if constexpr (GATHER) {
+            expand(cur, tile.nrows * a.row_len);
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // this wave's LDS writes (the copies stay in flight)
+            asm volatile("s_barrier" ::: "memory");
+        }
+        if (tile.kt != kt_loaded) {   // wave-uniform; waited for here, before the next copies are issued
+            kt_loaded = tile.kt;
+            load_filter(kt_loaded, fa);
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+        }
+        if (bid + 1 < b1) {
+            if constexpr (GATHER)
+                issue_raw(bid + 1, cur ^ 1);
+            else
+                issue_strips(bid + 1, cur ^ 1);
+        }
+        uint32_t bb[C][NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const uint32_t w0 = smallc_window(a, tile, FH, lane, b) + (GATHER ? 0u : (uint32_t)(cur * buf_f) * 4u);
+#pragma unroll
+            for (int c = 0; c < C; ++c) bb[c][b] = w0 + (uint32_t)(c * a.slotf) * 4u;
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
+
+        // The k-steps of half KSI (the immediates of the LDS reads follow the
+        // step, so each half is its own code); the ks = 0 waves store the
+        // previous band's sums, SPS values per step.
+        auto run = [&](auto ks_tag) {
+            constexpr int KSI = decltype(ks_tag)::value;
+            constexpr int Q0 = KSI * SW, NQ = KSI == 0 ? SW : S - SW;
+            float bv[2][NB];
+            auto read_step = [&](int i, float (&dst)[NB]) {
+                const int q = Q0 + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    dst[b] = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(L) + bb[c][b] + (v * FH + u) * 4);
+            };
+            read_step(0, bv[0]);
+#pragma unroll
+            for (int i = 0; i < NQ; ++i) {
+                if (i + 1 < NQ) read_step(i + 1, bv[(i + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i], bv[i & 1][b], acc[b], 0, 0, 0);
+                if constexpr (KSI == 0) {
+#pragma unroll
+                    for (int e = i * SPS; e < (i + 1) * SPS && e < NOUT; ++e) {
+                        const int b = e / 16, r = e % 16;
+                        const int chs = (r >> 2) * 8 + (r & 3);   // + slot*4, in ybase
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(elem(out[b], r)), yres, ybase[b],
+                                                              (int)(chs * hw * 4), 0);
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        if (ks == 0)
+            run(std::integral_constant<int, 0>());
+        else
+            run(std::integral_constant<int, 1>());
+
+        // The ks = 1 wave of each block leaves its partial sums in R; the
+        // ks = 0 wave adds them, P0 + P1, into `out`.  The barrier waits for
+        // the LDS writes only (counter lgkmcnt 0): the next band's copies and
+        // this band's stores stay in flight.
+        if (ks > 0) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    R[ch * RP + b * 32 + col] = acc[b][r];
+                }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        asm volatile("s_barrier" ::: "memory");
+        if (ks == 0) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    out[b][r] = acc[b][r] + R[ch * RP + b * 32 + col];
+                }
+            const uint32_t y0 = (uint32_t)((((size_t)tile.img * a.k + (size_t)(tile.kt * 2 + cb) * 32 + slot * 4) * hw +
+                                            (size_t)tile.m0 * a.wo) * 4);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int p = b * 32 + col;
+                ybase[b] = p < tile.npix ? y0 + (uint32_t)p * 4u : kBandOutside;
+            }
+        }
+    }
+    // the last band's sums
+    if (ks == 0) {
+#pragma unroll
+        for (int e = 0; e < NOUT; ++e) {
+            const int b = e / 16, r = e % 16;
+            const int chs = (r >> 2) * 8 + (r & 3);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(elem(out[b], r)), yres, ybase[b],
+                                                  (int)(chs * hw * 4), 0);
+        }
+    }
+}
+
 template <int FH, int FW, int NB, int MODE, int KS>
 void launch_band_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
     if (lds > 64 * 1024)
@@ -320,7 +605,7 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
     a.src = static_cast<const float*>(src);
     a.wt = static_cast<const float*>(w);
     a.y = y;
-    a.c = (int)g.c; a.h = (int)g.h; a.w = (int)g.w; a.k = (int)g.k;
+    a.n = (int)g.n; a.c = (int)g.c; a.h = (int)g.h; a.w = (int)g.w; a.k = (int)g.k;
     a.sh = (int)g.sh; a.sw = (int)g.sw; a.ph = (int)g.ph; a.pw = (int)g.pw;
     a.ho = (int)g.ho; a.wo = (int)g.wo;
     a.row_len = (int)g.row_len;
@@ -337,6 +622,9 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
     // 16-byte copies need 16-byte aligned planes
     const bool aligned = ((uintptr_t)src & 15) == 0 && (g.ho * g.row_len) % 4 == 0;
     a.mode = fused ? kBandGather : aligned ? kBandWide : kBandNarrow;
+    a.slotf = 0;
+    a.total = a.grid;
+    a.per_wg = 1;
     return a;
 }
 
@@ -362,6 +650,114 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
         BAND_NB4(5)
     }
 #undef BAND_NB4
+    return 0;
+}
+
+namespace {
+
+template <int NB, int MODE>
+void launch_small_c_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
+    constexpr int C = kSmallCChannels;
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)conv_f32_band_small_c_kernel<C, 7, 7, NB, MODE>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL((conv_f32_band_small_c_kernel<C, 7, 7, NB, MODE>), dim3((unsigned)a.grid),
+                       dim3(kBandThreads), (size_t)lds, stream, a);
+}
+
+template <int NB>
+void launch_small_c_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
+    if (a.mode == kBandGather)
+        launch_small_c_v<NB, kBandGather>(a, lds, stream);
+    else if (a.mode == kBandNarrow)
+        launch_small_c_v<NB, kBandNarrow>(a, lds, stream);
+    else
+        launch_small_c_v<NB, kBandWide>(a, lds, stream);
+}
+
+// LDS floats per channel slot of a band of `rows` rows: the strip, its
+// alignment shift and the rounding of the copies to whole 256-element parts.
+int64_t small_c_slot(const Geometry& g, int64_t rows) { return (rows * g.row_len + 3 + 255) / 256 * 256; }
+
+// Raw input rows of a band (fused): (rows - 1)*sh + Fh rows of W floats, the
+// pitch rounded up to whole 16-byte vectors, per channel.
+int64_t small_c_rrows(const Geometry& g, int64_t rows) { return (rows - 1) * g.sh + g.fh; }
+int64_t small_c_rpitch(const Geometry& g) { return (g.w + 3) / 4 * 4; }
+int64_t small_c_raw(const Geometry& g, int64_t rows) {
+    return kSmallCChannels * small_c_rrows(g, rows) * small_c_rpitch(g);
+}
+
+}  // namespace
+
+F32BandPlan plan_band_small_c_f32(const Geometry& g) {
+    F32BandPlan best;
+    if (g.elem != 4 || g.c != kSmallCChannels || g.fh != 7 || g.fw != 7 || g.k % 64) return best;
+    // 32-bit buffer offsets; y (stored through a buffer resource) below the
+    // dropped-store offset
+    if (g.c * g.h * g.w * 4 >= (int64_t(1) << 30) || g.c * g.ho * g.row_len * 4 >= (int64_t(1) << 30) ||
+        g.k * g.c * g.taps * 4 >= (int64_t(1) << 31) || g.n * g.k * g.ho * g.wo * 4 >= (int64_t(1) << 30))
+        return best;
+    constexpr int HU = 4, S = kSmallCChannels * HU * 7, SW = (S + 1) / 2;
+    // useful MFMA k-steps (pairs of reduction elements) over those the launch
+    // occupies: whole workgroups per CU, each 4 waves of NB blocks x SW steps
+    const double useful = (double)g.n * (g.k / 32) * (double)(g.ho * g.wo) / 32.0 * (g.c * g.taps / 2.0);
+    for (int64_t rows = 1; rows <= g.ho; ++rows) {
+        const int64_t nb = (rows * g.wo + 31) / 32;
+        if (nb < 4 || nb > 7) continue;
+        // the fused expansion covers a strip with kSmallCExpand positions per thread
+        if (rows * g.row_len > 256 * kSmallCExpand) continue;
+        // unfused: two strip buffers; fused: one, and two buffers of raw input
+        // rows; both followed by the partial sums of the two channel blocks
+        const int64_t slot = small_c_slot(g, rows), red = 2 * 32 * nb * 32 * 4;
+        const int64_t lds = std::max(2 * kSmallCChannels * slot * 4,
+                                     kSmallCChannels * slot * 4 + 2 * small_c_raw(g, rows) * 4) + red;
+        if (lds > kConvLdsMaxBytes) continue;
+        const int64_t nbands = (g.ho + rows - 1) / rows;
+        const int64_t total = g.n * nbands * (g.k / 64);
+        if (total > 0x7fffffff) continue;
+        const int64_t per_wg = (total + 255) / 256;
+        const double eff = useful / ((double)per_wg * 256.0 * 4.0 * nb * SW);
+        if (eff > best.eff + 1e-9) {
+            best.ks = 2;
+            best.rows = (int)rows;
+            best.nb = (int)nb;
+            best.grid = (total + per_wg - 1) / per_wg;
+            best.eff = eff;
+            best.lds_bytes = lds;
+        }
+    }
+    if (best.eff < 0.75) return F32BandPlan();
+    best.ok = true;
+    return best;
+}
+
+F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
+                                  const void* w, float* y) {
+    F32BandArgs a = band_args_f32(g, p, fused, src, w, y);
+    a.nkt = (int)(g.k / 64);
+    a.nchunks = 1;
+    a.slotf = (int)small_c_slot(g, p.rows);
+    a.total = (int)(g.n * a.nbands * a.nkt);
+    a.per_wg = (a.total + 255) / 256;
+    a.grid = (int)p.grid;
+    a.xcd_remap = 0;   // each workgroup walks its own run of bands
+    a.rrows = (int)small_c_rrows(g, p.rows);
+    a.rpitch = (int)small_c_rpitch(g);
+    // raw rows by 16-byte copies when every row of x starts on a 16-byte boundary
+    a.rawwide = (g.w % 4 == 0 && ((uintptr_t)src & 15) == 0) ? 1 : 0;
+    a.rparts = a.rawwide ? (a.w + 255) / 256 : (a.w + 63) / 64;
+    return a;
+}
+
+int launch_conv_f32_band_small_c(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
+                                 const void* w, float* y, hipStream_t stream) {
+    const F32BandArgs a = band_args_small_c_f32(g, p, fused, src, w, y);
+    switch (p.nb) {
+        case 4: launch_small_c_nb<4>(a, p.lds_bytes, stream); break;
+        case 5: launch_small_c_nb<5>(a, p.lds_bytes, stream); break;
+        case 6: launch_small_c_nb<6>(a, p.lds_bytes, stream); break;
+        default: launch_small_c_nb<7>(a, p.lds_bytes, stream); break;
+    }
     return 0;
 }
 

@@ -205,6 +205,27 @@ F32_BANDS = [
 ]
 
 
+# Shapes that the fp32 small-C band kernel takes: C = 3, 7x7 filters, K a
+# multiple of 64, bands of 97-224 pixels, at least 75% of the occupied
+# matrix-core work useful.
+F32_BANDS_SMALL_C = [
+    (32, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3),    # the stem layer: bands of 2 rows
+    (128, 3, 227, 227, 64, 7, 7, 2, 2, 0, 0),   # Table 1 Conv3
+    (4, 3, 64, 64, 512, 7, 7, 2, 2, 3, 3),
+    (8, 3, 70, 70, 64, 7, 7, 1, 1, 0, 0),
+    (2, 3, 48, 48, 512, 7, 7, 1, 1, 0, 0),      # ragged last band
+]
+
+
+@pytest.mark.parametrize("layout", [0, 1], ids=["padded", "trimmed"])
+@pytest.mark.parametrize("case", F32_BANDS_SMALL_C, ids=lambda c: "x".join(map(str, c)))
+def test_launch_plans_in_bounds_fp32_bands_small_c(case, layout):
+    d = P.im2win_desc(*case, P.IM2WIN_F32, layout)
+    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == "f32_bands_small_c"
+    assert P.im2win_filter_scratch_bytes(d) == 0
+    assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
+
+
 def test_conv_kernel_names_on_workloads():
     got = {}
     for wl in workloads.WORKLOADS:
@@ -213,7 +234,7 @@ def test_conv_kernel_names_on_workloads():
     assert got["rect_3x5_s2_f32"] == ("f32_bands",) * 2
     assert got["resnet_3x3_f32"] == ("f32_bands",) * 2
     assert got["deep_3x3_bf16"] == ("bf16_one_image",) * 2
-    assert got["stem_7x7_s2_f32"] == ("f32_tiles",) * 2
+    assert got["stem_7x7_s2_f32"] == ("f32_bands_small_c",) * 2
     d = P.im2win_desc(1, 3, 4000, 4000, 4, 60, 60, 1, 1, 0, 0, P.IM2WIN_F32)
     assert P.im2win_conv_kernel(d, False) == "per_output"
 
@@ -253,18 +274,23 @@ def test_fp32_bands_decline_unsupported_shapes():
 
 def test_filter_scratch_sizes_on_workloads():
     """Which workloads repack the filter, and how large the scratch is: bf16
-    fast kernels take K*C*Fh*Fw*2 bytes exactly; fp32 filters whose chunk rows
-    are not whole 16-byte vectors (C*Fh*Fw odd: the single-image and stem
-    layers) take padded blocks of about K*C*Fh*Fw*4 bytes; the others none."""
+    fast kernels take K*C*Fh*Fw*2 bytes exactly; fp32 tile kernels whose
+    chunk rows are not whole 16-byte vectors (C*Fh*Fw odd: the single-image
+    layer, and the stem layer at a batch the band kernel does not take) take
+    padded blocks of about K*C*Fh*Fw*4 bytes; the band kernels none."""
     got = {}
     for wl in workloads.WORKLOADS:
         d = _desc(_wl_shape(wl), _wl_dtype(wl))
         got[wl.name] = P.im2win_filter_scratch_bytes(d)
     kcft = {wl.name: wl.k * wl.c * wl.fh * wl.fw for wl in workloads.WORKLOADS}
     assert got["deep_3x3_bf16"] == kcft["deep_3x3_bf16"] * 2
-    assert got["resnet_3x3_f32"] == 0 and got["rect_3x5_s2_f32"] == 0
-    for name in ("single_3x3_f32", "stem_7x7_s2_f32"):
-        assert kcft[name] * 4 <= got[name] <= 2 * kcft[name] * 4 + (1 << 16), (name, got[name])
+    assert got["resnet_3x3_f32"] == 0 and got["rect_3x5_s2_f32"] == 0 and got["stem_7x7_s2_f32"] == 0
+    name = "single_3x3_f32"
+    assert kcft[name] * 4 <= got[name] <= 2 * kcft[name] * 4 + (1 << 16), (name, got[name])
+    st = workloads.BY_NAME["stem_7x7_s2_f32"]
+    stem2 = P.im2win_desc(2, st.c, st.h, st.w, st.k, st.fh, st.fw, st.sh, st.sw, st.ph, st.pw, P.IM2WIN_F32)
+    assert P.im2win_conv_kernel(stem2, False) == "f32_tiles"
+    assert kcft["stem_7x7_s2_f32"] * 4 <= P.im2win_filter_scratch_bytes(stem2) <= 2 * kcft["stem_7x7_s2_f32"] * 4 + (1 << 16)
 
 
 def test_short_or_missing_scratch_rejected():

@@ -216,8 +216,16 @@ F32_BANDS = [
 ]
 
 
+# Shapes that the fp32 small-C band kernel takes (C = 3, 7x7).
+F32_BANDS_SMALL_C = [
+    (4, 3, 64, 64, 512, 7, 7, 2, 2, 3, 3),     # stem-like: stride 2, padding 3, bands of 7 rows
+    (8, 3, 70, 70, 64, 7, 7, 1, 1, 0, 0),      # stride 1, 64 x 64 outputs
+    (2, 3, 48, 48, 512, 7, 7, 1, 1, 0, 0),     # ragged last band
+]
+
+
 @pytest.mark.parametrize("layout", [P.IM2WIN_ROWS_PADDED, P.IM2WIN_ROWS_TRIMMED], ids=["padded", "trimmed"])
-@pytest.mark.parametrize("case", F32_BANDS, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("case", F32_BANDS + F32_BANDS_SMALL_C, ids=lambda c: "x".join(map(str, c)))
 def test_fp32_band_kernel(case, layout):
     """Whole output of both convolutions against the fp64 oracle (Eq. 1),
     fused and unfused bitwise identical, nothing written past the output."""
@@ -225,7 +233,8 @@ def test_fp32_band_kernel(case, layout):
     wl, x_cpu, w_cpu = workloads.random_case(sum(case) + layout, n, c, h, w, k, fh, fw, sh, sw, ph, pw, "f32")
     _label(f"f32-bands layout={layout}", wl)
     d = P.im2win_desc(n, c, h, w, k, fh, fw, sh, sw, ph, pw, P.IM2WIN_F32, layout)
-    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == "f32_bands"
+    want = "f32_bands_small_c" if case in F32_BANDS_SMALL_C else "f32_bands"
+    assert P.im2win_conv_kernel(d, False) == P.im2win_conv_kernel(d, True) == want
     assert P.im2win_check_plan(d) == 0, P.im2win_last_error()
     x, wt = x_cpu.to(DEV), w_cpu.to(DEV)
     ho, wo = P.im2win_output_shape(d)
