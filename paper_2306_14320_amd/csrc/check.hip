@@ -766,9 +766,9 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
     const int64_t slot_bytes = (int64_t)a.slotf * 4;
     const int64_t rb_f = (int64_t)C * a.rrows * a.rpitch;   // floats of one raw-row buffer (fused)
     if (C != kSmallCChannels || p.ks != 2 || p.lds_bytes > kConvLdsMaxBytes ||
-        p.lds_bytes != std::max(2 * C * slot_bytes, C * slot_bytes + 2 * rb_f * 4) + (int64_t)2 * 32 * nb * 32 * 4 ||
-        a.rrows != (a.rows - 1) * g.sh + g.fh || a.rpitch < g.w || a.rpitch % 4 || (a.rawwide && g.w % 4) ||
-        a.rparts * 64 * (a.rawwide ? 4 : 1) < g.w || a.rows * g.row_len > 256 * kSmallCExpand || nb * 32 < a.rows * a.wo ||
+        p.lds_bytes != std::max(2 * C * slot_bytes, 2 * rb_f * 4) + (int64_t)2 * 32 * nb * 32 * 4 ||
+        a.rrows != (a.rows - 1) * g.sh + g.fh || a.rlpad < g.pw || a.rlpad % 4 || a.rpitch < a.rlpad + g.w ||
+        a.rpitch % 4 || (a.rawwide && g.w % 4) || a.rparts * 64 * (a.rawwide ? 4 : 1) < g.w || nb * 32 < a.rows * a.wo ||
         (nb - 1) * 32 >= a.rows * a.wo || g.k % 64 || a.nkt * 64 != g.k || (int64_t)g.n * a.nbands * a.nkt != a.total ||
         (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho || a.per_wg < 1 ||
         (int64_t)a.grid * a.per_wg < a.total || (int64_t)(a.grid - 1) * a.per_wg >= a.total) {
@@ -841,12 +841,29 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
             }
         return true;
     };
-    // Fused: the raw-row copies of band t (each raw float written once with
-    // (channel << 24) + its x element, or zero for rows outside the image),
-    // then the expansion of every strip position below the band's length
-    // from them, through the offsets the kernel computes once.
+    // Fused: the pad columns the kernel zeroes once (both buffers' rows: the
+    // map must reach exactly the columns outside 0..W-1), then the raw-row
+    // copies of band t, each data float written once with (channel << 24) +
+    // its x element, or zero for rows outside the image.
+    std::vector<int64_t> pads((size_t)2 * rb_f, -1);
+    {
+        const int padc = a.rpitch - g.w;
+        for (int i = 0; i < 2 * C * a.rrows * padc; ++i) {
+            const int row = i / padc, k = i % padc;
+            const int64_t col = k < a.rlpad ? k : g.w + k;
+            if (col >= a.rpitch || (col >= a.rlpad && col < a.rlpad + g.w) || pads[(size_t)row * a.rpitch + col] != -1) {
+                r.fail("fp32 small-C band conv: pad zero %d lands on raw column %lld", i, (long long)col);
+                return;
+            }
+            pads[(size_t)row * a.rpitch + col] = kZero;
+        }
+    }
     auto stage_raw = [&](const BandTile& t) {
-        std::fill(raw.begin(), raw.end(), -1);
+        std::copy(pads.begin(), pads.begin() + rb_f, raw.begin());   // buffer 0's pads (buffer 1's are alike)
+        if (!std::equal(pads.begin(), pads.begin() + rb_f, pads.begin() + rb_f)) {
+            r.fail("fp32 small-C band conv: the two raw buffers' pad columns differ");
+            return false;
+        }
         const int rper = a.rawwide ? 4 : 1;
         const int64_t y0 = (int64_t)t.m0 * g.sh - g.ph;
         for (int j = 0; j < C * a.rrows * a.rparts; ++j)
@@ -854,8 +871,8 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
                 const int row = j / a.rparts, pr = j % a.rparts, c = row / a.rrows, rr = row % a.rrows;
                 const int64_t yy = y0 + rr, xx = (int64_t)pr * 64 * rper + lane * rper;
                 if (xx >= g.w) continue;   // lane masked off
-                const int64_t dst = (int64_t)row * a.rpitch + xx;
-                if (xx + rper > g.w || dst + rper > rb_f) {
+                const int64_t dst = (int64_t)row * a.rpitch + a.rlpad + xx;
+                if (xx + rper > g.w || dst + rper > rb_f || (rper == 4 && dst % 4)) {
                     r.fail("fp32 small-C band conv: raw copy %d lane %d writes float %lld past its row", j, lane,
                            (long long)dst);
                     return false;
@@ -873,28 +890,6 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
                     raw[dst + e] = in ? ((int64_t)c << 24) + yy * g.w + xx + e : kZero;
                 }
             }
-        const int64_t len = (int64_t)t.nrows * g.row_len;
-        for (int64_t pos = 0; pos < len; ++pos) {
-            const int ml = (int)fast_div((uint32_t)pos, a.div_row);
-            if (ml != pos / g.row_len || pos >= 256 * kSmallCExpand) {
-                r.fail("fp32 small-C band conv: strip position %lld expanded as row %d", (long long)pos, ml);
-                return false;
-            }
-            const int64_t rem = pos - (int64_t)ml * g.row_len, k = rem / FH, u = rem % FH, xx = k - g.pw;
-            const int64_t src = xx >= 0 && xx < g.w ? ((int64_t)ml * g.sh + u) * a.rpitch + xx : -1;
-            for (int c = 0; c < C; ++c) {
-                int64_t v = kZero;
-                if (src >= 0) {
-                    v = src < a.rrows * a.rpitch ? raw[(size_t)(c * a.rrows * a.rpitch + src)] : -1;
-                    if (v == -1) {
-                        r.fail("fp32 small-C band conv: strip position %lld expanded from raw float %lld never copied",
-                               (long long)pos, (long long)src);
-                        return false;
-                    }
-                }
-                holds[(size_t)c * a.slotf + pos] = v;
-            }
-        }
         return true;
     };
     for (int band = 0; band < a.nbands && r.violations == 0; ++band) {
@@ -917,18 +912,21 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
                     for (int i = 0; i < nq; ++i) {
                         const int q = ks * SW + i, c = q / (HU * FW), rr = q % (HU * FW), u = rr / FW, v = rr % FW;
                         const int uu = u + sl * (FH - HU);   // the filter row this slot multiplies
-                        const int64_t f = (int64_t)c * a.slotf + smallc_window(a, t, FH, lane, b) / 4 + (int64_t)v * FH + u;
+                        const int64_t f =
+                            fused ? smallc_raw_window(a, t, FH, lane, b) / 4 + ((int64_t)c * a.rrows + u) * a.rpitch + v
+                                  : (int64_t)c * a.slotf + smallc_window(a, t, FH, lane, b) / 4 + (int64_t)v * FH + u;
+                        const std::vector<int64_t>& src = fused ? raw : holds;
                         const int64_t yy = m * g.sh + uu - g.ph, xx = n * g.sw + v - g.pw;
                         const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
                         // unfused: the window-tensor element; fused: the x element, zero in the padding
                         const int64_t elem = fused ? yy * g.w + xx : m * g.row_len + (n * g.sw + v) * FH + uu;
                         const int64_t want = fused && pad ? kZero : ((int64_t)c << 24) + elem;
-                        const bool ok = f >= 0 && f < (int64_t)C * a.slotf && uu < FH && holds[f] == want;
+                        const bool in = f >= 0 && f < (int64_t)src.size();
+                        const bool ok = in && uu < FH && src[f] == want;
                         if (!ok) {
                             r.fail("fp32 small-C band conv: band %d wave %d lane %d block %d step %d reads LDS float "
                                    "%lld holding %lld, wants element %lld of channel %d", band, wv, lane, b, q,
-                                   (long long)f, (long long)(f >= 0 && f < (int64_t)C * a.slotf ? holds[f] : -3),
-                                   (long long)elem, c);
+                                   (long long)f, (long long)(in ? src[f] : -3), (long long)elem, c);
                             return;
                         }
                     }

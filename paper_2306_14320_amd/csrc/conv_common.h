@@ -421,6 +421,7 @@ struct F32BandArgs {
     int total;             // small-C kernel: bands (x channel groups) of the layer
     int per_wg;            // small-C kernel: consecutive bands per workgroup
     int rrows, rpitch;     // small-C fused: raw input rows per band, LDS floats per raw row
+    int rlpad;             // small-C fused: LDS floats before column 0 of a raw row (zero, >= pw)
     int rawwide, rparts;   // small-C fused: raw rows by 16-byte copies; copies per row
     FastDiv div_row, div_wo;   // by L, by Wo
 };
@@ -520,7 +521,6 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
 // two waves per block of 32 output channels splitting the k-steps; one
 // persistent workgroup per CU walks through per_wg consecutive bands.
 constexpr int kSmallCChannels = 3;          // C the kernels are built for
-constexpr int kSmallCExpand = 16;           // fused: strip positions per thread and channel (4096 per strip)
 
 // Band bid of the small-C kernel: output-channel group slowest, so that a
 // workgroup's run of consecutive bands shares one filter.
@@ -546,6 +546,17 @@ __host__ __device__ inline uint32_t smallc_window(const F32BandArgs& a, const Ba
     if (p > t.npix - 1) p = t.npix - 1;
     const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
     return (uint32_t)(t.shift + ml * a.row_len + n * a.sw * fh + (lane >> 5) * (fh - (fh + 1) / 2)) * 4u;
+}
+
+// Fused: byte offset, in a raw-row buffer, of the window that lane `lane`
+// of pixel block b reads (the zero-padded input row ml*sh + its slot's first
+// filter row, column n*sw - pw); filter tap (c, u, v) adds
+// ((c*rrows + u)*rpitch + v) floats.  Pixels past the band repeat the last.
+__host__ __device__ inline uint32_t smallc_raw_window(const F32BandArgs& a, const BandTile& t, int fh, int lane, int b) {
+    int p = b * 32 + (lane & 31);
+    if (p > t.npix - 1) p = t.npix - 1;
+    const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
+    return (uint32_t)((ml * a.sh + (lane >> 5) * (fh - (fh + 1) / 2)) * a.rpitch + a.rlpad - a.pw + n * a.sw) * 4u;
 }
 
 // Parts (copies of 256 elements wide, 64 otherwise) of one channel slot.

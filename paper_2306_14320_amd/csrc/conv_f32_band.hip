@@ -274,11 +274,10 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int cb = wv >> 1, ks = wv & 1;
     const int slot = lane >> 5, col = lane & 31;
-    // LDS: unfused, two strip buffers; fused, one strip buffer and two
-    // buffers of raw input rows; then the partial sums of the two blocks
-    const int buf_f = C * a.slotf;                  // floats per strip buffer
-    const int rb_f = C * a.rrows * a.rpitch;        // floats per raw-row buffer (fused)
-    float* R = L + (GATHER ? buf_f + 2 * rb_f : 2 * buf_f) + cb * RW;
+    // LDS: two strip buffers (unfused) or two buffers of zero-padded raw
+    // input rows (fused), then the partial sums of the two blocks
+    const int buf_f = GATHER ? C * a.rrows * a.rpitch : C * a.slotf;   // floats per buffer
+    float* R = L + 2 * buf_f + cb * RW;
     const int b0 = (int)blockIdx.x * a.per_wg;
     const int b1 = b0 + a.per_wg < a.total ? b0 + a.per_wg : a.total;
     const __amdgpu_buffer_rsrc_t wres = band_rsrc(a.wt, (uint32_t)((size_t)a.k * C * FH * FW * 4));
@@ -304,9 +303,13 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
 #endif
         }
     };
-    // Fused: the rrows input rows of band bid (rows m0*sh - ph .. , zero
-    // outside the image) of the C channels into raw buffer buf, one row per
-    // copy (16-byte pieces, or 4-byte ones when rows are not whole vectors).
+    // Fused: the rrows input rows of band bid (rows m0*sh - ph .., zero
+    // outside the image) of the C channels into raw buffer buf, columns
+    // 0..W-1 at rlpad, one row per copy (16-byte pieces, or 4-byte ones when
+    // rows are not whole vectors).  The pad columns around them were zeroed
+    // once and are never written.  With them the raw rows hold every window
+    // element of the band at a fixed offset from the window's start, so the
+    // k-steps read them as they read the window tensor's strips.
     auto issue_raw = [&](int bid, int buf) {
         const BandTile t = smallc_tile(a, bid);
         const __amdgpu_buffer_rsrc_t sres = band_rsrc(a.src + (size_t)t.img * img_elems, (uint32_t)(img_elems * 4));
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             const int xx = pr * 64 * per + lane * per;   // first column of this lane
             if (xx < a.w) {
                 const uint32_t voff = yy >= 0 && yy < a.h ? (uint32_t)(((c * a.h + yy) * a.w + xx) * 4) : kBandOutside;
-                char* dst = reinterpret_cast<char*>(L) + (buf_f + buf * rb_f + row * a.rpitch + pr * 64 * per) * 4;
+                char* dst = reinterpret_cast<char*>(L) + (buf * buf_f + row * a.rpitch + a.rlpad + pr * 64 * per) * 4;
 #if defined(__HIP_DEVICE_COMPILE__)
                 if (a.rawwide)
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
@@ -328,33 +331,15 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             }
         }
     };
-    // Fused: where strip position tid + 256*q of a channel comes from in the
-    // raw rows of its band (raw row ml*sh + u, column k - pw), or -1 for the
-    // zero columns of the padding; the same for every band.
-    int exo[GATHER ? kSmallCExpand : 1];
     if constexpr (GATHER) {
-#pragma unroll
-        for (int q = 0; q < kSmallCExpand; ++q) {
-            const int pos = tid + 256 * q;
-            const int ml = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - ml * a.row_len;
-            const int k = rem / FH, u = rem - k * FH, xx = k - a.pw;
-            exo[q] = xx >= 0 && xx < a.w ? (ml * a.sh + u) * a.rpitch + xx : -1;
+        // the pad columns (rlpad before each raw row, rpitch - rlpad - W after)
+        // of every raw row of both buffers
+        const int padc = a.rpitch - a.w;
+        for (int i = tid; i < 2 * C * a.rrows * padc; i += kBandThreads) {
+            const int row = i / padc, k = i - row * padc;
+            L[row * a.rpitch + (k < a.rlpad ? k : a.w + k)] = 0.0f;
         }
     }
-    // Fused: the band's strips from raw buffer buf into the strip buffer
-    // (the window tensor's own positions, as the unfused variant copies them).
-    auto expand = [&](int buf, int len) {
-        const float* raw = L + buf_f + buf * rb_f;
-#pragma unroll
-        for (int q = 0; q < kSmallCExpand; ++q) {
-            const int pos = tid + 256 * q;
-            if (pos < len) {
-#pragma unroll
-                for (int c = 0; c < C; ++c)
-                    L[c * a.slotf + pos] = exo[q] >= 0 ? raw[c * a.rrows * a.rpitch + exo[q]] : 0.0f;
-            }
-        }
-    };
     // Filter values of this wave's k-steps q = ks*SW + i = (c, u, v) for the
     // output channels of group kt: slot 0 row u, slot 1 row u + Fh - HU (zero
     // where that row is also slot 0's, and past the last step).  (q, c, u, v)
@@ -414,11 +399,6 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         __builtin_amdgcn_s_waitcnt(0x0F70);
         __syncthreads();
         const BandTile tile = smallc_tile(a, bid);
-        if constexpr (GATHER) {
-            expand(cur, tile.nrows * a.row_len);
-            __builtin_amdgcn_s_waitcnt(0xC07F);   // this wave's LDS writes (the copies stay in flight)
-            asm volatile("s_barrier" ::: "memory");
-        }
         if (tile.kt != kt_loaded) {   // wave-uniform; waited for here, before the next copies are issued
             kt_loaded = tile.kt;
             load_filter(kt_loaded, fa);
@@ -430,12 +410,18 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             else
                 issue_strips(bid + 1, cur ^ 1);
         }
-        uint32_t bb[C][NB];
+        // byte offset of each block's window: per channel (unfused), or of
+        // channel 0 (fused, the channel and filter row add a uniform offset)
+        uint32_t bb[GATHER ? 1 : C][NB];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const uint32_t w0 = smallc_window(a, tile, FH, lane, b) + (GATHER ? 0u : (uint32_t)(cur * buf_f) * 4u);
+            if constexpr (GATHER) {
+                bb[0][b] = smallc_raw_window(a, tile, FH, lane, b) + (uint32_t)(cur * buf_f) * 4u;
+            } else {
+                const uint32_t w0 = smallc_window(a, tile, FH, lane, b) + (uint32_t)(cur * buf_f) * 4u;
 #pragma unroll
-            for (int c = 0; c < C; ++c) bb[c][b] = w0 + (uint32_t)(c * a.slotf) * 4u;
+                for (int c = 0; c < C; ++c) bb[c][b] = w0 + (uint32_t)(c * a.slotf) * 4u;
+            }
         }
 #pragma unroll
         for (int b = 0; b < NB; ++b)
@@ -451,9 +437,17 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             float bv[2][NB];
             auto read_step = [&](int i, float (&dst)[NB]) {
                 const int q = Q0 + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
+                const char* Lb = reinterpret_cast<const char*>(L);
+                if constexpr (GATHER) {
+                    const int cu = (c * a.rrows + u) * a.rpitch * 4;
 #pragma unroll
-                for (int b = 0; b < NB; ++b)
-                    dst[b] = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(L) + bb[c][b] + (v * FH + u) * 4);
+                    for (int b = 0; b < NB; ++b)
+                        dst[b] = *reinterpret_cast<const float*>(Lb + bb[0][b] + cu + v * 4);
+                } else {
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+                        dst[b] = *reinterpret_cast<const float*>(Lb + bb[c][b] + (v * FH + u) * 4);
+                }
             };
             read_step(0, bv[0]);
 #pragma unroll
@@ -679,10 +673,16 @@ void launch_small_c_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
 // alignment shift and the rounding of the copies to whole 256-element parts.
 int64_t small_c_slot(const Geometry& g, int64_t rows) { return (rows * g.row_len + 3 + 255) / 256 * 256; }
 
-// Raw input rows of a band (fused): (rows - 1)*sh + Fh rows of W floats, the
-// pitch rounded up to whole 16-byte vectors, per channel.
+// Raw input rows of a band (fused): (rows - 1)*sh + Fh rows per channel,
+// each with zero columns before (rlpad >= pw, whole 16-byte vectors so the
+// data starts aligned) and after (to the last column a window reaches), the
+// pitch whole vectors.
 int64_t small_c_rrows(const Geometry& g, int64_t rows) { return (rows - 1) * g.sh + g.fh; }
-int64_t small_c_rpitch(const Geometry& g) { return (g.w + 3) / 4 * 4; }
+int64_t small_c_rlpad(const Geometry& g) { return (g.pw + 3) / 4 * 4; }
+int64_t small_c_rpitch(const Geometry& g) {
+    const int64_t reach = std::max(g.w, (g.wo - 1) * g.sw + g.fw - g.pw);   // columns 0 .. reach-1
+    return (small_c_rlpad(g) + reach + 3) / 4 * 4;
+}
 int64_t small_c_raw(const Geometry& g, int64_t rows) {
     return kSmallCChannels * small_c_rrows(g, rows) * small_c_rpitch(g);
 }
@@ -704,13 +704,10 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
     for (int64_t rows = 1; rows <= g.ho; ++rows) {
         const int64_t nb = (rows * g.wo + 31) / 32;
         if (nb < 4 || nb > 7) continue;
-        // the fused expansion covers a strip with kSmallCExpand positions per thread
-        if (rows * g.row_len > 256 * kSmallCExpand) continue;
-        // unfused: two strip buffers; fused: one, and two buffers of raw input
-        // rows; both followed by the partial sums of the two channel blocks
+        // two strip buffers (unfused) or two buffers of raw input rows
+        // (fused), followed by the partial sums of the two channel blocks
         const int64_t slot = small_c_slot(g, rows), red = 2 * 32 * nb * 32 * 4;
-        const int64_t lds = std::max(2 * kSmallCChannels * slot * 4,
-                                     kSmallCChannels * slot * 4 + 2 * small_c_raw(g, rows) * 4) + red;
+        const int64_t lds = std::max(2 * kSmallCChannels * slot, 2 * small_c_raw(g, rows)) * 4 + red;
         if (lds > kConvLdsMaxBytes) continue;
         const int64_t nbands = (g.ho + rows - 1) / rows;
         const int64_t total = g.n * nbands * (g.k / 64);
@@ -743,6 +740,7 @@ F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool 
     a.xcd_remap = 0;   // each workgroup walks its own run of bands
     a.rrows = (int)small_c_rrows(g, p.rows);
     a.rpitch = (int)small_c_rpitch(g);
+    a.rlpad = (int)small_c_rlpad(g);
     // raw rows by 16-byte copies when every row of x starts on a 16-byte boundary
     a.rawwide = (g.w % 4 == 0 && ((uintptr_t)src & 15) == 0) ? 1 : 0;
     a.rparts = a.rawwide ? (a.w + 255) / 256 : (a.w + 63) / 64;
