@@ -944,11 +944,13 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
             r.fail("fp32 small-C band conv: output %zu of an image stored %d times", i, (int)out[i]);
             return;
         }
-    // outputs go through a buffer resource over y: valid offsets inside it,
-    // the dropped-store offset (plus any channel) past its end, no wrap
-    const uint64_t y_bytes = (uint64_t)g.n * g.k * g.ho * g.wo * 4;
+    // outputs go through a buffer resource over one image of y: valid
+    // offsets inside it, the dropped-store offset (plus any channel) past its
+    // end, no wrap
+    const uint64_t y_bytes = (uint64_t)g.k * g.ho * g.wo * 4;
     if (y_bytes > kBandOutside || (uint64_t)kBandOutside + 31ull * g.ho * g.wo * 4 >= (uint64_t(1) << 32))
-        r.fail("fp32 small-C band conv: y of %llu bytes against the dropped-store offset", (unsigned long long)y_bytes);
+        r.fail("fp32 small-C band conv: y image of %llu bytes against the dropped-store offset",
+               (unsigned long long)y_bytes);
     // every (filter row, column) of every channel is multiplied exactly once
     // per output: slot 0 rows u < HU, slot 1 rows u + Fh - HU >= HU
     std::vector<int> used((size_t)C * T, 0);

@@ -243,13 +243,17 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
     }
 }
 
-// Layers with few input channels (the 7x7 stem layers, C = 3): the whole
-// reduction of a band is C*Fh*Fw elements, so a band's C strips are staged at
-// once.  The kernel is persistent: one workgroup per CU walks through a run
-// of consecutive bands (same output channels and image, neighbouring rows),
-// with the strips of band b + 1 copied into a second LDS buffer while band b
-// is multiplied, and band b - 1's outputs stored from registers between
-// band b's MFMAs, so that no phase of a band waits for memory.  The filter
+// Layers with few input channels (C = 3: the 7x7 stride-2 stems, the 11x11
+// stride-4 and 3x3 first layers): the whole reduction of a band is C*Fh*Fw
+// elements, so a band's C strips are staged at once.  The kernel is
+// persistent: one workgroup per CU walks through a run of consecutive bands
+// (same output channels and image, neighbouring rows), with the strips of
+// band b + 1 copied into a second LDS buffer while band b is multiplied, and
+// band b - 1's outputs stored from registers between band b's MFMAs, so that
+// no phase of a band waits for memory.  Fused, the band's zero-padded input
+// rows take the strips' place: window element (u, v) of output pixel (m, n)
+// is input row m*sh + u, column n*sw + v - pw, a fixed offset from the
+// window's start, as in the window tensor.  The filter
 // values stay in registers across the run; they are reloaded only where the
 // run crosses into the next group of output channels.  The MFMA's
 // two k-slots take filter rows u and u + Fh - ceil(Fh/2) of one channel and
@@ -368,10 +372,11 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             load_filter_half(std::integral_constant<int, 1>(), kt, f);
     };
 
-    // y through a buffer resource: a store whose offset lies past the end
-    // (pixels past the band, or no previous band yet) is dropped
+    // y through a buffer resource over the previous band's image: a store
+    // whose offset lies past its end (pixels past the band, or no previous
+    // band yet) is dropped
     const size_t hw = (size_t)a.ho * a.wo;
-    const __amdgpu_buffer_rsrc_t yres = band_rsrc(a.y, (uint32_t)((size_t)a.n * a.k * hw * 4));
+    __amdgpu_buffer_rsrc_t yres = band_rsrc(a.y, 0u);
     float fa[SW];
     f32x16 acc[NB], out[NB];
     // byte offset in y of the previous band's channel 0, pixel (lane, block);
@@ -497,8 +502,8 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
                     const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
                     out[b][r] = acc[b][r] + R[ch * RP + b * 32 + col];
                 }
-            const uint32_t y0 = (uint32_t)((((size_t)tile.img * a.k + (size_t)(tile.kt * 2 + cb) * 32 + slot * 4) * hw +
-                                            (size_t)tile.m0 * a.wo) * 4);
+            yres = band_rsrc(a.y + (size_t)tile.img * a.k * hw, (uint32_t)((size_t)a.k * hw * 4));
+            const uint32_t y0 = (uint32_t)((((size_t)(tile.kt * 2 + cb) * 32 + slot * 4) * hw + (size_t)tile.m0 * a.wo) * 4);
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int p = b * 32 + col;
@@ -649,24 +654,34 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
 
 namespace {
 
-template <int NB, int MODE>
+template <int FH, int NB, int MODE>
 void launch_small_c_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
     constexpr int C = kSmallCChannels;
     if (lds > 64 * 1024)
-        (void)hipFuncSetAttribute((const void*)conv_f32_band_small_c_kernel<C, 7, 7, NB, MODE>,
+        (void)hipFuncSetAttribute((const void*)conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL((conv_f32_band_small_c_kernel<C, 7, 7, NB, MODE>), dim3((unsigned)a.grid),
+    hipLaunchKernelGGL((conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE>), dim3((unsigned)a.grid),
                        dim3(kBandThreads), (size_t)lds, stream, a);
 }
 
-template <int NB>
+template <int FH, int NB>
 void launch_small_c_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
     if (a.mode == kBandGather)
-        launch_small_c_v<NB, kBandGather>(a, lds, stream);
+        launch_small_c_v<FH, NB, kBandGather>(a, lds, stream);
     else if (a.mode == kBandNarrow)
-        launch_small_c_v<NB, kBandNarrow>(a, lds, stream);
+        launch_small_c_v<FH, NB, kBandNarrow>(a, lds, stream);
     else
-        launch_small_c_v<NB, kBandWide>(a, lds, stream);
+        launch_small_c_v<FH, NB, kBandWide>(a, lds, stream);
+}
+
+template <int FH>
+void launch_small_c_fh(const F32BandArgs& a, int nb, int64_t lds, hipStream_t stream) {
+    switch (nb) {
+        case 4: launch_small_c_nb<FH, 4>(a, lds, stream); break;
+        case 5: launch_small_c_nb<FH, 5>(a, lds, stream); break;
+        case 6: launch_small_c_nb<FH, 6>(a, lds, stream); break;
+        default: launch_small_c_nb<FH, 7>(a, lds, stream); break;
+    }
 }
 
 // LDS floats per channel slot of a band of `rows` rows: the strip, its
@@ -691,13 +706,14 @@ int64_t small_c_raw(const Geometry& g, int64_t rows) {
 
 F32BandPlan plan_band_small_c_f32(const Geometry& g) {
     F32BandPlan best;
-    if (g.elem != 4 || g.c != kSmallCChannels || g.fh != 7 || g.fw != 7 || g.k % 64) return best;
+    if (g.elem != 4 || g.c != kSmallCChannels || g.fh != g.fw || g.k % 64) return best;
+    if (g.fh != 3 && g.fh != 7 && g.fh != 11) return best;   // the compiled filter sizes
     // 32-bit buffer offsets; y (stored through a buffer resource) below the
     // dropped-store offset
     if (g.c * g.h * g.w * 4 >= (int64_t(1) << 30) || g.c * g.ho * g.row_len * 4 >= (int64_t(1) << 30) ||
-        g.k * g.c * g.taps * 4 >= (int64_t(1) << 31) || g.n * g.k * g.ho * g.wo * 4 >= (int64_t(1) << 30))
+        g.k * g.c * g.taps * 4 >= (int64_t(1) << 31) || g.k * g.ho * g.wo * 4 >= (int64_t(1) << 30))
         return best;
-    constexpr int HU = 4, S = kSmallCChannels * HU * 7, SW = (S + 1) / 2;
+    const int HU = (int)(g.fh + 1) / 2, S = kSmallCChannels * HU * (int)g.fw, SW = (S + 1) / 2;
     // useful MFMA k-steps (pairs of reduction elements) over those the launch
     // occupies: whole workgroups per CU, each 4 waves of NB blocks x SW steps
     const double useful = (double)g.n * (g.k / 32) * (double)(g.ho * g.wo) / 32.0 * (g.c * g.taps / 2.0);
@@ -723,7 +739,7 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
             best.lds_bytes = lds;
         }
     }
-    if (best.eff < 0.75) return F32BandPlan();
+    if (best.eff < 0.7) return F32BandPlan();
     best.ok = true;
     return best;
 }
@@ -750,12 +766,12 @@ F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool 
 int launch_conv_f32_band_small_c(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
                                  const void* w, float* y, hipStream_t stream) {
     const F32BandArgs a = band_args_small_c_f32(g, p, fused, src, w, y);
-    switch (p.nb) {
-        case 4: launch_small_c_nb<4>(a, p.lds_bytes, stream); break;
-        case 5: launch_small_c_nb<5>(a, p.lds_bytes, stream); break;
-        case 6: launch_small_c_nb<6>(a, p.lds_bytes, stream); break;
-        default: launch_small_c_nb<7>(a, p.lds_bytes, stream); break;
-    }
+    if (g.fh == 3)
+        launch_small_c_fh<3>(a, p.nb, p.lds_bytes, stream);
+    else if (g.fh == 7)
+        launch_small_c_fh<7>(a, p.nb, p.lds_bytes, stream);
+    else
+        launch_small_c_fh<11>(a, p.nb, p.lds_bytes, stream);
     return 0;
 }
 

@@ -221,6 +221,10 @@ F32_BANDS_SMALL_C = [
     (4, 3, 64, 64, 512, 7, 7, 2, 2, 3, 3),     # stem-like: stride 2, padding 3, bands of 7 rows
     (8, 3, 70, 70, 64, 7, 7, 1, 1, 0, 0),      # stride 1, 64 x 64 outputs
     (2, 3, 48, 48, 512, 7, 7, 1, 1, 0, 0),     # ragged last band
+    (1, 3, 62, 62, 512, 3, 3, 1, 1, 1, 1),     # 3x3: the middle filter row in both k-slots
+    (4, 3, 63, 63, 512, 3, 3, 2, 2, 0, 0),
+    (16, 3, 59, 59, 512, 11, 11, 4, 4, 2, 2),  # 11x11 stride 4, input rows not whole 16-byte vectors
+    (1, 3, 56, 56, 512, 11, 11, 1, 1, 5, 5),
 ]
 
 
