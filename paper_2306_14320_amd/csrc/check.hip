@@ -769,7 +769,7 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
         p.lds_bytes != std::max(2 * C * slot_bytes, 2 * rb_f * 4) + (int64_t)2 * 32 * nb * 32 * 4 ||
         a.rrows != (a.rows - 1) * g.sh + g.fh || a.rlpad < g.pw || a.rlpad % 4 || a.rpitch < a.rlpad + g.w ||
         a.rpitch % 4 || (a.rawwide && g.w % 4) || a.rparts * 64 * (a.rawwide ? 4 : 1) < g.w || nb * 32 < a.rows * a.wo ||
-        (nb - 1) * 32 >= a.rows * a.wo || g.k % 64 || a.nkt * 64 != g.k || (int64_t)g.n * a.nbands * a.nkt != a.total ||
+        (nb - 1) * 32 >= a.rows * a.wo || g.k % 32 || a.nkt != (g.k + 63) / 64 || (int64_t)g.n * a.nbands * a.nkt != a.total ||
         (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho || a.per_wg < 1 ||
         (int64_t)a.grid * a.per_wg < a.total || (int64_t)(a.grid - 1) * a.per_wg >= a.total) {
         r.fail("fp32 small-C band conv: plan (%d rows, nb %d, slot %d floats, %lld bytes of LDS, %d x %d bands)", a.rows,
@@ -932,11 +932,21 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
                     }
                 }
         }
+        // blocks of output channels past K store nothing; their filter
+        // offsets lie past the filter, so they read zeros
         for (int kt = 0; kt < a.nkt; ++kt)
-            for (int cb = 0; cb < 2; ++cb)
+            for (int cb = 0; cb < 2; ++cb) {
+                if ((kt * 2 + cb) * 32 >= g.k) {
+                    if ((uint64_t)(kt * 2 + cb) * 32 * C * T * 4 < (uint64_t)g.k * C * T * 4) {
+                        r.fail("fp32 small-C band conv: idle channel block %d reads the filter", kt * 2 + cb);
+                        return;
+                    }
+                    continue;
+                }
                 for (int p2 = 0; p2 < t.npix; ++p2)
                     for (int ch = 0; ch < 32; ++ch)
                         ++out[(size_t)((kt * 2 + cb) * 32 + ch) * g.ho * g.wo + (size_t)t.m0 * g.wo + p2];
+            }
     }
     if (r.violations) return;
     for (size_t i = 0; i < out.size(); ++i)

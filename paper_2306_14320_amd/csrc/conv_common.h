@@ -566,11 +566,11 @@ __host__ __device__ inline int smallc_parts(const F32BandArgs& a, const BandTile
 }
 
 // The plan of the small-C band kernel, or !ok (fp32; C = 3; 3x3, 7x7 or
-// 11x11 filter; K a multiple of 64; a band of rows whose pixels fill 4-7
-// blocks of 32 and whose three strips (or raw input rows), twice, fit with
-// the partial sums in LDS; at least 70% of the occupied matrix-core work
-// useful, counting ceil(bands / 256) bands per workgroup).  Independent of
-// fusion.
+// 11x11 filter; K a multiple of 32, in groups of 64; a band of rows whose
+// pixels fill 4-7 blocks of 32 and whose three strips (or raw input rows),
+// twice, fit with the partial sums in LDS; at least 55% of the occupied
+// matrix-core work useful, counting ceil(bands / 256) bands per workgroup
+// and the idle half of a last group of 32 channels).  Independent of fusion.
 F32BandPlan plan_band_small_c_f32(const Geometry& g);
 F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
                                   const void* w, float* y);

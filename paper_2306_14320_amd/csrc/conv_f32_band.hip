@@ -288,50 +288,61 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
     const size_t img_elems = (size_t)C * a.plane_src;
 
     // Unfused: the C strips of band bid (runs of the window tensor) into
-    // strip buffer buf, parts of 256 (wide) or 64 elements spread over the 4
-    // waves; copies past the strip read zeros.
+    // strip buffer buf, parts of 256 (wide) or 64 elements; copy c*np + sp
+    // goes to wave (c*np + sp) mod 4.  Copies past the strip read zeros.
     auto issue_strips = [&](int bid, int buf) {
         const BandTile t = smallc_tile(a, bid);
         const __amdgpu_buffer_rsrc_t sres = band_rsrc(a.src + (size_t)t.img * img_elems, (uint32_t)(img_elems * 4));
         const int np = smallc_parts(a, t);
-        for (int j = wv; j < C * np; j += 4) {
-            const int c = j / np, sp = j - c * np;
-            const uint32_t off = band_source(a, t, MODE, FH, sp, lane);
-            char* dst = reinterpret_cast<char*>(L) + (buf * buf_f + c * a.slotf + sp * (MODE == kBandWide ? 256 : 64)) * 4;
-            const uint32_t voff = off == kBandOutside ? off : off + (uint32_t)(c * a.plane_src * 4);
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            for (int sp = (wv - c * np) & 3; sp < np; sp += 4) {
+                const uint32_t off = band_source(a, t, MODE, FH, sp, lane);
+                char* dst =
+                    reinterpret_cast<char*>(L) + (buf * buf_f + c * a.slotf + sp * (MODE == kBandWide ? 256 : 64)) * 4;
+                const uint32_t voff = off == kBandOutside ? off : off + (uint32_t)(c * a.plane_src * 4);
 #if defined(__HIP_DEVICE_COMPILE__)   // (16-byte LDS copies exist on gfx950 only; the host pass checks them too)
-            if constexpr (MODE == kBandWide)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
-            else
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
+                if constexpr (MODE == kBandWide)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
 #endif
+            }
         }
     };
     // Fused: the rrows input rows of band bid (rows m0*sh - ph .., zero
     // outside the image) of the C channels into raw buffer buf, columns
-    // 0..W-1 at rlpad, one row per copy (16-byte pieces, or 4-byte ones when
-    // rows are not whole vectors).  The pad columns around them were zeroed
-    // once and are never written.  With them the raw rows hold every window
-    // element of the band at a fixed offset from the window's start, so the
-    // k-steps read them as they read the window tensor's strips.
+    // 0..W-1 at rlpad, in rparts copies per row (16-byte pieces, or 4-byte
+    // ones when rows are not whole vectors); row c*rrows + r goes to wave
+    // (c*rrows + r) mod 4.  The pad columns around them were zeroed once and
+    // are never written.  With them the raw rows hold every window element
+    // of the band at a fixed offset from the window's start, so the k-steps
+    // read them as they read the window tensor's strips.
     auto issue_raw = [&](int bid, int buf) {
         const BandTile t = smallc_tile(a, bid);
         const __amdgpu_buffer_rsrc_t sres = band_rsrc(a.src + (size_t)t.img * img_elems, (uint32_t)(img_elems * 4));
         const int y0 = t.m0 * a.sh - a.ph;
         const int per = a.rawwide ? 4 : 1;
-        for (int j = wv; j < C * a.rrows * a.rparts; j += 4) {
-            const int row = j / a.rparts, pr = j - row * a.rparts;
-            const int c = row / a.rrows, r = row - c * a.rrows, yy = y0 + r;
-            const int xx = pr * 64 * per + lane * per;   // first column of this lane
-            if (xx < a.w) {
-                const uint32_t voff = yy >= 0 && yy < a.h ? (uint32_t)(((c * a.h + yy) * a.w + xx) * 4) : kBandOutside;
-                char* dst = reinterpret_cast<char*>(L) + (buf * buf_f + row * a.rpitch + a.rlpad + pr * 64 * per) * 4;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            for (int r = (wv - c * a.rrows) & 3; r < a.rrows; r += 4) {
+                const int yy = y0 + r;   // wave-uniform
+                const uint32_t rowoff = (uint32_t)((c * a.h + yy) * a.w) * 4u;
+                const bool in = yy >= 0 && yy < a.h;
+                const int dst0 = (buf * buf_f + (c * a.rrows + r) * a.rpitch + a.rlpad) * 4;
+                for (int pr = 0; pr < a.rparts; ++pr) {
+                    const int xx = pr * 64 * per + lane * per;   // first column of this lane
+                    if (xx < a.w) {
+                        const uint32_t voff = in ? rowoff + (uint32_t)xx * 4u : kBandOutside;
+                        char* dst = reinterpret_cast<char*>(L) + dst0 + pr * 256 * per;
 #if defined(__HIP_DEVICE_COMPILE__)
-                if (a.rawwide)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
-                else
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
+                        if (a.rawwide)
+                            __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 16, voff, 0, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, 4, voff, 0, 0, 0);
 #endif
+                    }
+                }
             }
         }
     };
@@ -346,7 +357,8 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
     }
     // Filter values of this wave's k-steps q = ks*SW + i = (c, u, v) for the
     // output channels of group kt: slot 0 row u, slot 1 row u + Fh - HU (zero
-    // where that row is also slot 0's, and past the last step).  (q, c, u, v)
+    // where that row is also slot 0's, past the last step, and for output
+    // channels past K, whose offsets lie past the filter).  (q, c, u, v)
     // are compile-time per half, so each load is a per-lane base plus an
     // immediate, and the zero-weight duplicate row a select.
     auto load_filter_half = [&](auto ks_tag, int kt, float (&f)[SW]) {
@@ -504,10 +516,13 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
                 }
             yres = band_rsrc(a.y + (size_t)tile.img * a.k * hw, (uint32_t)((size_t)a.k * hw * 4));
             const uint32_t y0 = (uint32_t)((((size_t)(tile.kt * 2 + cb) * 32 + slot * 4) * hw + (size_t)tile.m0 * a.wo) * 4);
+            // (a block of output channels past K, K = 32 mod 64, has zero
+            // weights and stores nothing)
+            const bool kin = (tile.kt * 2 + cb) * 32 < a.k;
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int p = b * 32 + col;
-                ybase[b] = p < tile.npix ? y0 + (uint32_t)p * 4u : kBandOutside;
+                ybase[b] = kin && p < tile.npix ? y0 + (uint32_t)p * 4u : kBandOutside;
             }
         }
     }
@@ -706,7 +721,7 @@ int64_t small_c_raw(const Geometry& g, int64_t rows) {
 
 F32BandPlan plan_band_small_c_f32(const Geometry& g) {
     F32BandPlan best;
-    if (g.elem != 4 || g.c != kSmallCChannels || g.fh != g.fw || g.k % 64) return best;
+    if (g.elem != 4 || g.c != kSmallCChannels || g.fh != g.fw || g.k % 32) return best;
     if (g.fh != 3 && g.fh != 7 && g.fh != 11) return best;   // the compiled filter sizes
     // 32-bit buffer offsets; y (stored through a buffer resource) below the
     // dropped-store offset
@@ -726,7 +741,7 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
         const int64_t lds = std::max(2 * kSmallCChannels * slot, 2 * small_c_raw(g, rows)) * 4 + red;
         if (lds > kConvLdsMaxBytes) continue;
         const int64_t nbands = (g.ho + rows - 1) / rows;
-        const int64_t total = g.n * nbands * (g.k / 64);
+        const int64_t total = g.n * nbands * ((g.k + 63) / 64);
         if (total > 0x7fffffff) continue;
         const int64_t per_wg = (total + 255) / 256;
         const double eff = useful / ((double)per_wg * 256.0 * 4.0 * nb * SW);
@@ -739,7 +754,7 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
             best.lds_bytes = lds;
         }
     }
-    if (best.eff < 0.7) return F32BandPlan();
+    if (best.eff < 0.55) return F32BandPlan();
     best.ok = true;
     return best;
 }
@@ -747,7 +762,7 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
 F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
                                   const void* w, float* y) {
     F32BandArgs a = band_args_f32(g, p, fused, src, w, y);
-    a.nkt = (int)(g.k / 64);
+    a.nkt = (int)((g.k + 63) / 64);   // K = 32 mod 64: the last group's second block idles
     a.nchunks = 1;
     a.slotf = (int)small_c_slot(g, p.rows);
     a.total = (int)(g.n * a.nbands * a.nkt);

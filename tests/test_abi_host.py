@@ -219,6 +219,10 @@ F32_BANDS_SMALL_C = [
     (4, 3, 63, 63, 512, 3, 3, 2, 2, 0, 0),
     (16, 3, 59, 59, 512, 11, 11, 4, 4, 2, 2),   # 11x11 stride 4, rows not whole 16-byte vectors
     (1, 3, 56, 56, 512, 11, 11, 1, 1, 5, 5),
+    (128, 3, 227, 227, 96, 11, 11, 4, 4, 0, 0),   # Table 1 Conv1: K = 96, the last group's second block idle
+    (128, 3, 231, 231, 96, 11, 11, 4, 4, 0, 0),   # Table 1 Conv2
+    (4, 3, 64, 64, 96, 3, 3, 1, 1, 1, 1),
+    (8, 3, 83, 83, 96, 7, 7, 2, 2, 3, 3),
 ]
 
 
@@ -293,9 +297,9 @@ def test_filter_scratch_sizes_on_workloads():
     name = "single_3x3_f32"
     assert kcft[name] * 4 <= got[name] <= 2 * kcft[name] * 4 + (1 << 16), (name, got[name])
     st = workloads.BY_NAME["stem_7x7_s2_f32"]
-    stem2 = P.im2win_desc(2, st.c, st.h, st.w, st.k, st.fh, st.fw, st.sh, st.sw, st.ph, st.pw, P.IM2WIN_F32)
-    assert P.im2win_conv_kernel(stem2, False) == "f32_tiles"
-    assert kcft["stem_7x7_s2_f32"] * 4 <= P.im2win_filter_scratch_bytes(stem2) <= 2 * kcft["stem_7x7_s2_f32"] * 4 + (1 << 16)
+    stem1 = P.im2win_desc(1, st.c, st.h, st.w, st.k, st.fh, st.fw, st.sh, st.sw, st.ph, st.pw, P.IM2WIN_F32)
+    assert P.im2win_conv_kernel(stem1, False) == "f32_tiles"
+    assert kcft["stem_7x7_s2_f32"] * 4 <= P.im2win_filter_scratch_bytes(stem1) <= 2 * kcft["stem_7x7_s2_f32"] * 4 + (1 << 16)
 
 
 def test_short_or_missing_scratch_rejected():

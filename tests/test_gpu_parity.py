@@ -225,6 +225,9 @@ F32_BANDS_SMALL_C = [
     (4, 3, 63, 63, 512, 3, 3, 2, 2, 0, 0),
     (16, 3, 59, 59, 512, 11, 11, 4, 4, 2, 2),  # 11x11 stride 4, input rows not whole 16-byte vectors
     (1, 3, 56, 56, 512, 11, 11, 1, 1, 5, 5),
+    (4, 3, 64, 64, 96, 3, 3, 1, 1, 1, 1),      # K = 96: the last group's second block of channels idle
+    (8, 3, 83, 83, 96, 7, 7, 2, 2, 3, 3),
+    (32, 3, 53, 53, 224, 11, 11, 4, 4, 5, 5),
 ]
 
 
