@@ -281,43 +281,42 @@ __global__ __launch_bounds__(kImgThreads, 1) void conv_bf16_image_kernel(ImgArgs
 // The filter K x C x Fh x Fw rewritten in fragment order: fragment
 // ((kp*nchunks + ch)*T + t)*2 + i holds, for lane l, the 8 channels
 // 32*ch + 8*(l/16) .. +7 of tap t = v*Fh + u of output channel
-// 32*kp + 16*i + l%16, as one 16-byte piece.  A workgroup rewrites 16 output
-// channels x one chunk: the 16 filter rows of the chunk (32*T elements each,
-// 16-byte aligned) come in with every 16-byte load in flight at once, then
-// each thread gathers pieces from LDS and writes them out whole.
-__global__ __launch_bounds__(256) void pack_filter_frag_kernel(const uint16_t* __restrict__ w,
-                                                               uint16_t* __restrict__ wf, int c, int fh,
-                                                               int fw, int nchunks) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int T = fh * fw, run = kImgChunk * T, vrun = run / 8;   // 16-byte pieces per row
-    u32x4* Lv = reinterpret_cast<u32x4*>(smem);
-    const uint16_t* Ls = reinterpret_cast<const uint16_t*>(smem);
-    const int ch = blockIdx.x % nchunks, kb = blockIdx.x / nchunks;   // kb: block of 16 output channels
-    const int nv = 16 * vrun;
-    u32x4 v[kPackFragLoads];
+// 32*kp + 16*i + l%16, as one 16-byte piece.  One wave per (16 output
+// channels, chunk): each lane loads the contiguous run of its output
+// channel's 8 channels x T taps (16*T bytes, T 16-byte loads, all in flight
+// at once), picks each tap's 8 values out of it with byte permutes and
+// stores the T pieces; a store instruction writes one whole fragment.
+template <int FH, int FW>
+__global__ __launch_bounds__(64) void pack_filter_frag_kernel(const uint16_t* __restrict__ w,
+                                                              uint16_t* __restrict__ wf, int c, int nchunks) {
+    constexpr int T = FH * FW;
+    const int lane = threadIdx.x;
+    const int ch = (int)blockIdx.x % nchunks, kb = (int)blockIdx.x / nchunks;   // kb: block of 16 output channels
+    const int k = kb * 16 + (lane & 15), g = lane >> 4;
+    const u32x4* run = reinterpret_cast<const u32x4*>(w + ((size_t)k * c + kImgChunk * ch + 8 * g) * T);
+    uint32_t d[4 * T];   // run element e (channel e / T, natural tap e % T) in half e & 1 of word e / 2
 #pragma unroll
-    for (int k = 0; k < kPackFragLoads; ++k) {
-        const int idx = threadIdx.x + k * 256;
-        const int r = idx / vrun, q = idx - r * vrun;
-        if (idx < nv)
-            v[k] = reinterpret_cast<const u32x4*>(w + ((size_t)(kb * 16 + r) * c + kImgChunk * ch) * T)[q];
-    }
+    for (int q = 0; q < T; ++q) {
+        const u32x4 v = run[q];
 #pragma unroll
-    for (int k = 0; k < kPackFragLoads; ++k) {
-        const int idx = threadIdx.x + k * 256;
-        if (idx < nv) Lv[idx] = v[k];
+        for (int e = 0; e < 4; ++e) d[4 * q + e] = v[e];
     }
-    __syncthreads();
     const int kp = kb >> 1, i = kb & 1;
-    for (int pc = threadIdx.x; pc < 64 * T; pc += 256) {
-        const int l = pc & 63, t = pc >> 6;
-        const int vv = t / fh, u = t - vv * fh, nat = u * fw + vv;
-        const uint16_t* s = Ls + (l & 15) * run + 8 * (l >> 4) * T + nat;
+    u32x4* out = reinterpret_cast<u32x4*>(wf) + (((size_t)kp * nchunks + ch) * T * 2 + i) * 64 + lane;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const int vv = t / FH, u = t - vv * FH, nat = u * FW + vv;
         u32x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = uint32_t(s[(2 * e) * T]) | (uint32_t(s[(2 * e + 1) * T]) << 16);
-        const size_t frag = (((size_t)kp * nchunks + ch) * T + t) * 2 + i;
-        reinterpret_cast<u32x4*>(wf)[frag * 64 + l] = o;
+        for (int j = 0; j < 4; ++j) {
+            const int e0 = (2 * j) * T + nat, e1 = (2 * j + 1) * T + nat;
+            // bytes 0-1: half e0 & 1 of word e0 / 2 (second operand); bytes
+            // 2-3: half e1 & 1 of word e1 / 2 (first operand, selectors 4-7)
+            const uint32_t sel = (uint32_t)((e0 & 1) * 2) | (uint32_t)((e0 & 1) * 2 + 1) << 8 |
+                                 (uint32_t)(4 + (e1 & 1) * 2) << 16 | (uint32_t)(4 + (e1 & 1) * 2 + 1) << 24;
+            o[j] = __builtin_amdgcn_perm(d[e1 >> 1], d[e0 >> 1], sel);
+        }
+        out[(size_t)t * 2 * 64] = o;
     }
 }
 
@@ -396,9 +395,8 @@ ImgArgs image_args(const Geometry& g, const ImgPlan& p, const void* src, const v
 int launch_conv_bf16_image(const Geometry& g, const ImgPlan& p, bool fused, const void* src,
                            const void* w, void* scratch, float* y, hipStream_t stream) {
     const int nchunks = (int)(g.c / kImgChunk);
-    hipLaunchKernelGGL(pack_filter_frag_kernel, dim3((unsigned)(g.k / 16 * nchunks)), dim3(256),
-                       (size_t)16 * kImgChunk * g.taps * 2, stream, static_cast<const uint16_t*>(w),
-                       static_cast<uint16_t*>(scratch), (int)g.c, (int)g.fh, (int)g.fw, nchunks);
+    hipLaunchKernelGGL((pack_filter_frag_kernel<3, 3>), dim3((unsigned)(g.k / 16 * nchunks)), dim3(64), 0, stream,
+                       static_cast<const uint16_t*>(w), static_cast<uint16_t*>(scratch), (int)g.c, nchunks);
     const ImgArgs a = image_args(g, p, src, scratch, y);
     launch_image<3, 3, kImgNPB>(a, fused, p.lds_bytes, stream);
     return 0;

@@ -342,7 +342,6 @@ constexpr int kImgThreads = 512;     // 8 waves: 4 groups of 32 output channels 
 constexpr int kImgChunk = 32;        // input channels per chunk (one MFMA per tap)
 constexpr int kImgNPB = 7;           // 16-pixel blocks per wave (193 to 224 output pixels per image)
 constexpr int kImgStripItems = 2;    // unfused staging items per thread (4 positions x 8 channels)
-constexpr int kPackFragLoads = 5;    // filter pack: 16-byte loads per thread (16 rows of 32*9 elements)
 constexpr int kImgBRing = 4;         // B fragments in flight + 1 (LDS reads issued ahead of their MFMAs)
 constexpr int kImgFusedItems = 2;    // fused staging items per thread (2 input elements x 8 channels)
 

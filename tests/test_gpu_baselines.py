@@ -133,9 +133,8 @@ def test_peak_memory_probe(name):
     ws_bytes = P.im2win_workspace_bytes(d)
     sc = P.im2win_filter_scratch_bytes(d)
     sc_bytes = max(sc, 16) if sc else 0
-    if name == "resnet_3x3_f32":
-        assert sc == 0
-    else:
+    # (which kernels repack the filter is pinned on the CPU; bf16 always does)
+    if wl.dtype == "bf16":
         assert sc > 0
     paths = line["paths"]
     # the caching allocator rounds each block up to a multiple of 512 bytes

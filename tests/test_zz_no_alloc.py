@@ -21,7 +21,9 @@ U32 = 2.0 ** -24
 # (dtype, (n, c, h, w, k, fh, fw, sh, sw, ph, pw)): larger first, then smaller
 SEQUENCES = [
     ("bf16", [(8, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1), (2, 64, 10, 12, 128, 3, 3, 1, 1, 1, 1)]),
-    ("f32", [(4, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3), (1, 3, 40, 36, 64, 7, 7, 2, 2, 3, 3)]),
+    # (five input channels: the three-channel band kernel, which reads the
+    # filter as it is, does not take the first)
+    ("f32", [(4, 5, 224, 224, 64, 7, 7, 2, 2, 3, 3), (1, 3, 40, 36, 64, 7, 7, 2, 2, 3, 3)]),
 ]
 
 
