@@ -606,8 +606,18 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                (long long)p.lds_bytes);
         return;
     }
-    if (a.mode != (fused ? kBandGather : (g.ho * g.row_len) % 4 == 0 ? kBandWide : kBandNarrow))
+    F32BandArgs raw_probe = a;
+    const bool raw = fused && band_raw_mode(g, a.rows, nullptr, &raw_probe);
+    if (a.mode != (fused ? (raw ? kBandRaw : kBandGather) : (g.ho * g.row_len) % 4 == 0 ? kBandWide : kBandNarrow))
         r.fail("fp32 band conv: copy mode %d", a.mode);
+    if (raw && (a.rlpad < g.pw || a.rlpad % 4 || a.rpitch != 4 * a.rlanes || a.rlanes > 64 || a.rrpi != 64 / a.rlanes ||
+                a.rpitch < a.rlpad + std::max(g.w, (g.wo - 1) * g.sw + g.fw - g.pw) ||
+                a.rrows != (a.rows - 1) * g.sh + g.fh || a.rgroups * a.rrpi < a.rrows ||
+                a.rgroups > kBandRawGroups || (int64_t)a.rgroups * a.rrpi * a.rpitch > kBandSlot || g.w % 4)) {
+        r.fail("fp32 band conv: raw rows (pitch %d, pad %d, %d rows per copy, %d copies)", a.rpitch, a.rlpad, a.rrpi,
+               a.rgroups);
+        return;
+    }
     std::vector<uint8_t> seen_wg(a.grid, 0);
     for (int b = 0; b < a.grid; ++b) {
         const int bid = a.xcd_remap ? (b & 7) * (a.grid >> 3) + (b >> 3) : b;
@@ -617,7 +627,7 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
         }
     }
     const int nj = band_copies(a.mode);
-    const int per = a.mode == kBandWide ? 4 : 1;      // floats per lane and copy
+    const int per = a.mode == kBandWide || a.mode == kBandRaw ? 4 : 1;   // floats per lane and copy
     const uint64_t slab = (uint64_t)g.c * a.plane_src * 4;
     const uint64_t plane_bytes = (uint64_t)a.plane_src * 4;
     if (slab >= kBandOutside) r.fail("fp32 band conv: image slab of %llu bytes", (unsigned long long)slab);
@@ -639,9 +649,11 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
         for (int wv = 0; wv < kBandThreads / 64; ++wv)
             for (int j = 0; j < nj; ++j)
                 for (int lane = 0; lane < 64; ++lane) {
+                    // raw mode: copies past rgroups and lanes past rrpi whole rows are skipped
+                    if (a.mode == kBandRaw && ((j >> 1) >= a.rgroups || lane >= a.rrpi * a.rlanes)) continue;
                     const int cc = 2 * wv + (j & 1);
                     const uint32_t off = band_source(a, t, a.mode, FH, j >> 1, lane);
-                    const int64_t dst = band_dest(a.mode, wv, j) + (int64_t)lane * per * 4;
+                    const int64_t dst = band_dest(a, a.mode, wv, j) + (int64_t)lane * per * 4;
                     if (dst < (int64_t)cc * kBandSlot * 4 || dst + per * 4 > (int64_t)(cc + 1) * kBandSlot * 4) {
                         r.fail("fp32 band conv: copy %d of wave %d lane %d writes LDS byte %lld outside slot %d", j,
                                wv, lane, (long long)dst, cc);
@@ -656,6 +668,28 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                         r.fail("fp32 band conv: copy %d of wave %d lane %d reads byte %llu of a %llu-byte slab", j,
                                wv, lane, (unsigned long long)last, (unsigned long long)slab);
                         return;
+                    }
+                    if (a.mode == kBandRaw) {
+                        // raw row r, column xx .. xx+3 of the band (x row
+                        // m0*sh - ph + r), or zeros outside the image and the row
+                        const int r2 = (j >> 1) * a.rrpi + lane / a.rlanes, li = lane % a.rlanes;
+                        const int64_t yy = (int64_t)t.m0 * g.sh - g.ph + r2, xx = 4 * li - a.rlpad;
+                        const bool in = r2 < a.rrows && yy >= 0 && yy < g.h && xx >= 0 && xx + 4 <= g.w;
+                        if ((off != kBandOutside) != in || (in && off != (uint32_t)(yy * g.w + xx) * 4u) ||
+                            dst / 4 != (int64_t)cc * kBandSlot + (int64_t)r2 * a.rpitch + 4 * li) {
+                            r.fail("fp32 band conv: raw copy %d of wave %d lane %d: source %u, LDS float %lld", j, wv,
+                                   lane, off, (long long)(dst / 4));
+                            return;
+                        }
+                        for (int e = 0; e < 4; ++e) {
+                            const int64_t f = dst / 4 + e;
+                            if (holds[f] != -1) {
+                                r.fail("fp32 band conv: LDS float %lld written twice", (long long)f);
+                                return;
+                            }
+                            holds[f] = in ? ((int64_t)cc << 24) + yy * g.w + xx + e : kZero;
+                        }
+                        continue;
                     }
                     for (int e = 0; e < per; ++e) {
                         const int64_t f = dst / 4 + e;
@@ -703,12 +737,17 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                         for (int tap = 0; tap < T; ++tap) {
                             const int u = tap / FW, v = tap % FW;
                             const int64_t f = band_window(a, t, FH, 2 * ks * PP + (lane >> 5), lane, b) / 4 +
-                                              (int64_t)pp * 2 * kBandSlot + (int64_t)v * FH + u;
-                            const int64_t elem = m * g.row_len + (n * g.sw + v) * FH + u;
+                                              (int64_t)pp * 2 * kBandSlot +
+                                              (a.mode == kBandRaw ? (int64_t)u * a.rpitch + v : (int64_t)v * FH + u);
                             const int64_t yy = m * g.sh + u - g.ph, xx = n * g.sw + v - g.pw;
                             const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
+                            // window-tensor element (raw mode: the x element)
+                            const int64_t elem =
+                                a.mode == kBandRaw ? yy * g.w + xx : m * g.row_len + (n * g.sw + v) * FH + u;
                             const bool ok = f >= 0 && f < stage_f &&
-                                            (holds[f] == ((int64_t)cc << 24) + elem || (fused && pad && holds[f] == kZero));
+                                            (a.mode == kBandRaw ? holds[f] == (pad ? kZero : ((int64_t)cc << 24) + elem)
+                                                                : (holds[f] == ((int64_t)cc << 24) + elem ||
+                                                                   (fused && pad && holds[f] == kZero)));
                             if (!ok) {
                                 r.fail("fp32 band conv: band %d wave %d lane %d block %d pair %d tap %d reads LDS float "
                                        "%lld holding %lld, wants element %lld of slot %d", band, wv, lane, b, pp, tap,
@@ -774,6 +813,10 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
         (int64_t)a.grid * a.per_wg < a.total || (int64_t)(a.grid - 1) * a.per_wg >= a.total) {
         r.fail("fp32 small-C band conv: plan (%d rows, nb %d, slot %d floats, %lld bytes of LDS, %d x %d bands)", a.rows,
                nb, a.slotf, (long long)p.lds_bytes, a.grid, a.per_wg);
+        return;
+    }
+    if (fused ? a.mode != kBandGather : (a.mode != kBandWide && a.mode != kBandNarrow)) {
+        r.fail("fp32 small-C band conv: copy mode %d", a.mode);
         return;
     }
     // workgroup w walks bands [w*per_wg, min((w+1)*per_wg, total)): every

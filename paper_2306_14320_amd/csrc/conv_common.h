@@ -396,6 +396,8 @@ constexpr int kBandStageBytes = kBandChunk * kBandSlot * 4;   // one chunk of st
 constexpr int kBandWide = 0;     // window-tensor rows, 16-byte copies (16-byte aligned planes)
 constexpr int kBandNarrow = 1;   // window-tensor rows, 4-byte copies
 constexpr int kBandGather = 2;   // fused: each strip position gathered from x
+constexpr int kBandRaw = 3;      // fused: the band's input rows, zero-padded, 16-byte copies
+constexpr int kBandRawGroups = 6;   // raw mode: copies (groups of rows) per channel slot, at most
 
 // Offset that no staging buffer reaches (image slabs are below 2^30 bytes):
 // a buffer load from it reads zero.
@@ -415,13 +417,15 @@ struct F32BandArgs {
     int nchunks;           // C / 8
     int grid;              // workgroups (N * nbands * nkt)
     int xcd_remap;         // place consecutive workgroups on one XCD
-    int mode;              // kBandWide, kBandNarrow or kBandGather
+    int mode;              // kBandWide, kBandNarrow, kBandGather or kBandRaw
     int slotf;             // small-C kernel: LDS floats per channel slot
     int total;             // small-C kernel: bands (x channel groups) of the layer
     int per_wg;            // small-C kernel: consecutive bands per workgroup
     int rrows, rpitch;     // small-C fused: raw input rows per band, LDS floats per raw row
     int rlpad;             // small-C fused: LDS floats before column 0 of a raw row (zero, >= pw)
     int rawwide, rparts;   // small-C fused: raw rows by 16-byte copies; copies per row
+    int rlanes, rrpi;      // band raw mode: 16-byte lanes per raw row (rpitch / 4), rows per copy
+    int rgroups;           // band raw mode: copies per channel slot
     FastDiv div_row, div_wo;   // by L, by Wo
 };
 
@@ -448,11 +452,15 @@ __host__ __device__ inline BandTile band_tile(const F32BandArgs& a, int bid) {
 // LDS byte address, in stage 0, of the window start of the pixel of `lane`
 // in pixel block b, in channel slot `slot`; pixels past the band are
 // clamped to its last pixel (computed, never stored).
+// Raw mode: the window starts at raw row ml*sh, column n*sw - pw of the
+// slot; tap (u, v) adds u*rpitch + v.
 __host__ __device__ inline uint32_t band_window(const F32BandArgs& a, const BandTile& t, int fh, int slot, int lane,
                                                 int b) {
     int p = b * 32 + (lane & 31);
     if (p > t.npix - 1) p = t.npix - 1;
     const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
+    if (a.mode == kBandRaw)
+        return (uint32_t)(slot * kBandSlot + ml * a.sh * a.rpitch + a.rlpad - a.pw + n * a.sw) * 4u;
     return (uint32_t)(slot * kBandSlot + t.shift + ml * a.row_len + n * a.sw * fh) * 4u;
 }
 
@@ -466,6 +474,15 @@ __host__ __device__ inline uint32_t band_window(const F32BandArgs& a, const Band
 // (zero in the padding).
 __host__ __device__ inline uint32_t band_source(const F32BandArgs& a, const BandTile& t, int mode, int fh, int s,
                                                 int lane) {
+    if (mode == kBandRaw) {
+        // copy s: raw rows s*rrpi .. of the band (input rows m0*sh - ph + r),
+        // rlanes lanes of 4 floats per row, columns 4*li - rlpad; the pad
+        // columns, rows outside the image and rows past rrows read zero
+        const int r = s * a.rrpi + lane / a.rlanes, li = lane - (lane / a.rlanes) * a.rlanes;
+        const int yy = t.m0 * a.sh - a.ph + r, xx = 4 * li - a.rlpad;
+        const bool inside = r < a.rrows && yy >= 0 && yy < a.h && xx >= 0 && xx + 4 <= a.w;
+        return inside ? (uint32_t)(yy * a.w + xx) * 4u : kBandOutside;
+    }
     const int len = t.nrows * a.row_len;
     if (mode == kBandWide) {
         const int e = s * 256 + lane * 4;
@@ -481,15 +498,25 @@ __host__ __device__ inline uint32_t band_source(const F32BandArgs& a, const Band
 }
 
 // LDS byte offset, within a stage, of copy j of wave wv: channel slot
-// 2*wv + (j & 1), part j / 2 (256 elements wide, 64 otherwise).
-__host__ __device__ inline uint32_t band_dest(int mode, int wv, int j) {
-    return (uint32_t)(((2 * wv + (j & 1)) * kBandSlot) * 4 + (j >> 1) * (mode == kBandWide ? 1024 : 256));
+// 2*wv + (j & 1), part j / 2 (256 elements wide, 64 otherwise, rrpi raw
+// rows in raw mode).
+__host__ __device__ inline uint32_t band_dest(const F32BandArgs& a, int mode, int wv, int j) {
+    const int part = mode == kBandWide ? 1024 : mode == kBandRaw ? a.rrpi * a.rpitch * 4 : 256;
+    return (uint32_t)(((2 * wv + (j & 1)) * kBandSlot) * 4 + (j >> 1) * part);
 }
 
 // Copies per wave and chunk (two channel slots).
 __host__ __device__ constexpr int band_copies(int mode) {
-    return mode == kBandWide ? 2 * (kBandMaxSeg / 4) : 2 * kBandMaxSeg;
+    return mode == kBandWide ? 2 * (kBandMaxSeg / 4) : mode == kBandRaw ? 2 * kBandRawGroups : 2 * kBandMaxSeg;
 }
+
+// Raw mode for a fused band convolution of this shape and input, or not:
+// rows of x whole 16-byte vectors (W a multiple of 4, x 16-byte aligned),
+// a raw row of rlanes 16-byte lanes holding rlpad >= pw zero columns, the
+// row and the columns a window reaches, and the band's rows in at most
+// kBandRawGroups copies of 64 / rlanes rows each, inside one slot.  Fills
+// rrows, rpitch, rlpad, rlanes, rrpi and rgroups.
+bool band_raw_mode(const Geometry& g, int rows, const void* x, F32BandArgs* a);
 
 struct F32BandPlan {
     bool ok = false;

@@ -20,18 +20,23 @@
 //     Unfused, each channel's strip is one contiguous run of the window
 //     tensor, copied by LDS DMA (buffer_load ... lds, no register round
 //     trip) in 16-byte pieces, or 4-byte ones when the planes are not
-//     16-byte aligned.  Fused, every strip element is gathered from x by
-//     4-byte LDS DMA with per-lane source offsets computed once per kernel;
-//     padding positions carry an offset past the end of the buffer, which
-//     the hardware reads as zero;
+//     16-byte aligned.  Fused, the slot holds the band's input rows instead
+//     (raw mode), each with zero columns on both sides, copied in 16-byte
+//     pieces several rows per copy: the window of pixel (m, n) then starts at
+//     raw row (m - m0)*sh, column n*sw - pw, and tap (u, v) lies u rows and
+//     v columns further, a fixed offset as in the window tensor.  Where the
+//     input rows are not whole 16-byte vectors, every strip element is
+//     gathered from x by 4-byte LDS DMA instead.  Per-lane source offsets
+//     are computed once per kernel; padding positions carry an offset past
+//     the end of the buffer, which the hardware reads as zero;
 //   - the filter does not go through LDS: each lane loads its own filter
 //     rows (one output channel, one input channel per pair, Fh*Fw taps) of
 //     the next chunk into registers while the current chunk is multiplied;
 //   - the copies of the next chunk are spread over the taps of the current
 //     one, and the windows of the next tap are read before the MFMAs of the
 //     current tap, so both latencies hide behind matrix-core work.
-// Both variants stage the same values into the same strip positions and run
-// the same matrix-core sequence, so their outputs are bitwise identical.
+// Both variants multiply the same values in the same matrix-core sequence,
+// so their outputs are bitwise identical.
 // Consecutive workgroups (the output-channel groups and bands of one image)
 // are placed on the same XCD (the hardware hands consecutive workgroup ids
 // to the 8 XCDs in turn), so they share the image in that XCD's L2.
@@ -112,14 +117,20 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
     // Copy j of chunk ch into stage ST: channel slot 2*wv + (j & 1), part
     // j >> 1.  A chunk past the last one reads only zeros (harmless: that
     // stage is not read again).
+    // Raw mode: copies past the band's rgroups are skipped, and so are the
+    // lanes past rrpi whole rows.
     auto copy = [&](int j, int ch, auto st_tag) {
         constexpr int ST = decltype(st_tag)::value;
+        if (MODE == kBandRaw && (j >> 1) >= a.rgroups) return;
         const uint32_t cbytes = (uint32_t)((ch * kBandChunk + 2 * wv + (j & 1)) * plane_bytes);
-        char* dst = reinterpret_cast<char*>(S) + ST * kBandStageBytes + band_dest(MODE, wv, j);
+        char* dst = reinterpret_cast<char*>(S) + ST * kBandStageBytes + band_dest(a, MODE, wv, j);
+        if (MODE != kBandRaw || lane < a.rrpi * a.rlanes) {
 #if defined(__HIP_DEVICE_COMPILE__)   // (16-byte LDS copies exist on gfx950 only; the host pass checks them too)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst, MODE == kBandWide ? 16 : 4,
-                                                 sofs[j >> 1] + cbytes, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst,
+                                                     MODE == kBandWide || MODE == kBandRaw ? 16 : 4,
+                                                     sofs[j >> 1] + cbytes, 0, 0, 0);
 #endif
+        }
     };
 
     float fa0[STEPS], fa1[STEPS];
@@ -147,7 +158,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
         auto read_step = [&](int q, float (&dst)[NB]) {
             const int pp = q / T, t = q - pp * T;
             const int u = t / FW, v = t - u * FW;
-            const int off = pp * PAIR_B + (v * FH + u) * 4;
+            const int off = pp * PAIR_B + (MODE == kBandRaw ? (u * a.rpitch + v) * 4 : (v * FH + u) * 4);
 #pragma unroll
             for (int b = 0; b < NB; ++b) dst[b] = *reinterpret_cast<const float*>(base + bb[b] + off);
         };
@@ -549,7 +560,9 @@ void launch_band_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
 
 template <int FH, int FW, int NB, int KS>
 void launch_band_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
-    if (a.mode == kBandGather)
+    if (a.mode == kBandRaw)
+        launch_band_v<FH, FW, NB, kBandRaw, KS>(a, lds, stream);
+    else if (a.mode == kBandGather)
         launch_band_v<FH, FW, NB, kBandGather, KS>(a, lds, stream);
     else if (a.mode == kBandNarrow)
         launch_band_v<FH, FW, NB, kBandNarrow, KS>(a, lds, stream);
@@ -635,11 +648,33 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
     a.xcd_remap = (p.grid % 8 == 0 && p.grid > 8) ? 1 : 0;
     // 16-byte copies need 16-byte aligned planes
     const bool aligned = ((uintptr_t)src & 15) == 0 && (g.ho * g.row_len) % 4 == 0;
-    a.mode = fused ? kBandGather : aligned ? kBandWide : kBandNarrow;
+    a.rrows = a.rpitch = a.rlpad = a.rlanes = a.rrpi = a.rgroups = 0;
+    a.rawwide = a.rparts = 0;
+    a.mode = fused ? (band_raw_mode(g, p.rows, src, &a) ? kBandRaw : kBandGather) : aligned ? kBandWide : kBandNarrow;
     a.slotf = 0;
     a.total = a.grid;
     a.per_wg = 1;
     return a;
+}
+
+bool band_raw_mode(const Geometry& g, int rows, const void* x, F32BandArgs* a) {
+    if (g.w % 4 || ((uintptr_t)x & 15)) return false;
+    const int64_t rlpad = (g.pw + 3) / 4 * 4;
+    const int64_t reach = std::max(g.w, (g.wo - 1) * g.sw + g.fw - g.pw);   // columns 0 .. reach-1
+    int64_t rlanes = (rlpad + reach + 3) / 4;
+    // consecutive output rows of a block (sh raw rows apart) in other banks
+    if ((rlanes * 4 * g.sh) % 64 == 0) ++rlanes;
+    if (rlanes > 64) return false;
+    const int64_t rrpi = 64 / rlanes, rrows = (rows - 1) * g.sh + g.fh;
+    const int64_t rgroups = (rrows + rrpi - 1) / rrpi;
+    if (rgroups > kBandRawGroups || rgroups * rrpi * rlanes * 4 > kBandSlot) return false;
+    a->rrows = (int)rrows;
+    a->rpitch = (int)(rlanes * 4);
+    a->rlpad = (int)rlpad;
+    a->rlanes = (int)rlanes;
+    a->rrpi = (int)rrpi;
+    a->rgroups = (int)rgroups;
+    return true;
 }
 
 int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
@@ -762,6 +797,8 @@ F32BandPlan plan_band_small_c_f32(const Geometry& g) {
 F32BandArgs band_args_small_c_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src,
                                   const void* w, float* y) {
     F32BandArgs a = band_args_f32(g, p, fused, src, w, y);
+    if (fused) a.mode = kBandGather;   // (this kernel's fused staging is its own raw-row copy)
+    a.rlanes = a.rrpi = a.rgroups = 0;
     a.nkt = (int)((g.k + 63) / 64);   // K = 32 mod 64: the last group's second block idles
     a.nchunks = 1;
     a.slotf = (int)small_c_slot(g, p.rows);
