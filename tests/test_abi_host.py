@@ -202,6 +202,9 @@ F32_BANDS = [
     (2, 16, 56, 56, 1024, 3, 3, 1, 1, 1, 1),
     (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),
     (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),
+    (8, 16, 52, 52, 1024, 3, 3, 2, 2, 1, 1),     # fused from raw rows, stride 2
+    (4, 16, 112, 112, 512, 3, 3, 2, 2, 1, 1),
+    (2, 16, 28, 32, 4096, 3, 5, 2, 2, 1, 4),     # raw rows with 8 zero columns in front
 ]
 
 
@@ -223,6 +226,7 @@ F32_BANDS_SMALL_C = [
     (128, 3, 231, 231, 96, 11, 11, 4, 4, 0, 0),   # Table 1 Conv2
     (4, 3, 64, 64, 96, 3, 3, 1, 1, 1, 1),
     (8, 3, 83, 83, 96, 7, 7, 2, 2, 3, 3),
+    (16, 3, 45, 45, 160, 7, 7, 2, 2, 3, 3),
 ]
 
 

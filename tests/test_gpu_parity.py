@@ -213,6 +213,8 @@ F32_BANDS = [
     (2, 16, 56, 56, 1024, 3, 3, 1, 1, 1, 1),   # two-way split: 7-row bands of 56 columns
     (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),   # two-way split: bands of 14 and 12 rows
     (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2
+    (8, 16, 52, 52, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2, fused from raw rows
+    (2, 16, 28, 32, 4096, 3, 5, 2, 2, 1, 4),   # raw rows with 8 zero columns in front (pw = 4)
 ]
 
 
@@ -228,6 +230,7 @@ F32_BANDS_SMALL_C = [
     (4, 3, 64, 64, 96, 3, 3, 1, 1, 1, 1),      # K = 96: the last group's second block of channels idle
     (8, 3, 83, 83, 96, 7, 7, 2, 2, 3, 3),
     (32, 3, 53, 53, 224, 11, 11, 4, 4, 5, 5),
+    (16, 3, 45, 45, 160, 7, 7, 2, 2, 3, 3),    # K = 160: three groups, the last half idle
 ]
 
 
