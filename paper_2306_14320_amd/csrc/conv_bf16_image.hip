@@ -217,11 +217,10 @@ __global__ __launch_bounds__(kImgThreads, 1) void conv_bf16_image_kernel(ImgArgs
     store_strips(0);
     __syncthreads();
 
-    // The loop body has no branch: after the last chunk it reloads that
-    // chunk's strips and filter (harmless reads) and writes the stage no one
-    // reads any more.
-    for (int ch = 0; ch < a.nchunks; ++ch) {
-        const int nx = ch + 1 < a.nchunks ? ch + 1 : ch;
+    // Every chunk but the last: the next chunk's strips and filter are loaded
+    // while this one is multiplied.
+    for (int ch = 0; ch + 1 < a.nchunks; ++ch) {
+        const int nx = ch + 1;
         IMG_PIN_VMEM();
         load_strips(nx);
         IMG_PIN_VMEM();
@@ -261,19 +260,43 @@ __global__ __launch_bounds__(kImgThreads, 1) void conv_bf16_image_kernel(ImgArgs
         __syncthreads();
     }
 
-    // D[row][col]: col = lane % 16 (pixel), row = 4*(lane/16) + v (output channel)
+    // The last chunk runs pixel block by pixel block (taps inner), and each
+    // block's outputs are stored as soon as its last MFMAs are issued, so
+    // the stores of the first blocks drain while the later ones multiply.
+    // D[row][col]: col = lane % 16 (pixel), row = 4*(lane/16) + v (output
+    // channel).
     float* yimg = a.y + (size_t)img * a.k * a.npix;
+    {
+        const u32x4* S = L + ((a.nchunks - 1) & 1) * a.stage_pos;
+        constexpr int NS = T * NPB, R = kImgBRing;
+        u32x4 bq[R];
 #pragma unroll
-    for (int q = 0; q < NPB; ++q) {
-        const int p = (half * NPB + q) * 16 + (lane & 15);
-        if (p < a.npix) {
+        for (int s0 = 0; s0 < R - 1; ++s0) bq[s0] = S[posb[s0 / T] + s0 % T];
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            const int q = st / T, t = st % T;
+            if (st + R - 1 < NS) {
+                const int s1 = st + R - 1;
+                bq[s1 % R] = S[posb[s1 / T] + s1 % T];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            const bf16x8 bv = __builtin_bit_cast(bf16x8, bq[st % R]);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
+                acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[t][i]), bv,
+                                                                    acc[i][q], 0, 0, 0);
+            if (t == T - 1) {
+                const int p = (half * NPB + q) * 16 + (lane & 15);
+                if (p < a.npix) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int j = kt * 128 + kp * 32 + i * 16 + 4 * g + v;
-                    yimg[(size_t)j * a.npix + p] = acc[i][q][v];
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const int j = kt * 128 + kp * 32 + i * 16 + 4 * g + v;
+                            yimg[(size_t)j * a.npix + p] = acc[i][q][v];
+                        }
                 }
+            }
         }
     }
 }
