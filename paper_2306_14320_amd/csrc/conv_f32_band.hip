@@ -264,15 +264,15 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
 // no phase of a band waits for memory.  Fused, the band's zero-padded input
 // rows take the strips' place: window element (u, v) of output pixel (m, n)
 // is input row m*sh + u, column n*sw + v - pw, a fixed offset from the
-// window's start, as in the window tensor.  The filter
-// values stay in registers across the run; they are reloaded only where the
-// run crosses into the next group of output channels.  The MFMA's
-// two k-slots take filter rows u and u + Fh - ceil(Fh/2) of one channel and
-// tap column (one LDS read: the second slot is the first plus
-// Fh - ceil(Fh/2) positions), u < ceil(Fh/2); for odd Fh the middle row
-// comes up in both slots and the second slot's copy gets zero weights, so
-// every read stays inside the pixel's window.  Waves (cb, ks): 2 blocks of 32
-// output channels x 2 halves of the C*ceil(Fh/2)*Fw k-steps.
+// window's start, as in the window tensor.  The filter values stay in
+// registers across the run; they are reloaded only where the run crosses
+// into the next group of output channels.  The MFMA's two k-slots take
+// filter rows u and u + Fh - ceil(Fh/2) of one channel and tap column (one
+// LDS read: the second slot is the first plus Fh - ceil(Fh/2) rows),
+// u < ceil(Fh/2); for odd Fh the middle row comes up in both slots and the
+// second slot's copy gets zero weights, so every read stays inside the
+// pixel's window.  Waves (cb, ks): 2 blocks of 32 output channels x 2
+// halves of the C*ceil(Fh/2)*Fw k-steps.
 template <int C, int FH, int FW, int NB, int MODE>
 __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(F32BandArgs a) {
     constexpr int HU = (FH + 1) / 2;
@@ -421,9 +421,9 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         issue_strips(b0, 0);
     for (int bid = b0; bid < b1; ++bid) {
         const int cur = (bid - b0) & 1;
-        // band bid's strips (raw rows) have landed, and the stores of band
-        // bid - 2; every wave is done with the buffers band bid - 1 read and
-        // with R
+        // band bid's strips (raw rows) have landed, and the stores issued
+        // during band bid - 1; every wave is done with the buffers band
+        // bid - 1 read and with R
         __builtin_amdgcn_s_waitcnt(0x0F70);
         __syncthreads();
         const BandTile tile = smallc_tile(a, bid);
