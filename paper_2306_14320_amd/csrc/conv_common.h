@@ -497,13 +497,21 @@ __host__ __device__ inline uint32_t band_source(const F32BandArgs& a, const Band
     return inside ? (uint32_t)(yy * a.w + xx) * 4u : kBandOutside;
 }
 
-// LDS byte offset, within a stage, of copy j of wave wv: channel slot
-// 2*wv + (j & 1), part j / 2 (256 elements wide, 64 otherwise, rrpi raw
-// rows in raw mode).
-__host__ __device__ inline uint32_t band_dest(const F32BandArgs& a, int mode, int wv, int j) {
-    const int part = mode == kBandWide ? 1024 : mode == kBandRaw ? a.rrpi * a.rpitch * 4 : 256;
-    return (uint32_t)(((2 * wv + (j & 1)) * kBandSlot) * 4 + (j >> 1) * part);
+// LDS byte offset, within a stage, of part `part` of channel slot `slot`
+// (256 elements wide, 64 otherwise, rrpi raw rows in raw mode).
+__host__ __device__ inline uint32_t band_dest_slot(const F32BandArgs& a, int mode, int slot, int part) {
+    const int bytes = mode == kBandWide ? 1024 : mode == kBandRaw ? a.rrpi * a.rpitch * 4 : 256;
+    return (uint32_t)(slot * kBandSlot * 4 + part * bytes);
 }
+
+// Copy j of wave wv (one wave per SIMD): channel slot 2*wv + (j & 1), part
+// j / 2.  (Two waves per SIMD: copy j of wave wv is slot wv, part j.)
+__host__ __device__ inline uint32_t band_dest(const F32BandArgs& a, int mode, int wv, int j) {
+    return band_dest_slot(a, mode, 2 * wv + (j & 1), j >> 1);
+}
+
+// The two-way split runs two waves per SIMD (conv_f32_band8_kernel).
+constexpr bool kBandTwoWavesPerSimd = true;
 
 // Copies per wave and chunk (two channel slots).
 __host__ __device__ constexpr int band_copies(int mode) {

@@ -254,6 +254,153 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
     }
 }
 
+// The two-way split (KS = 2, 3x3, 64 output channels) with two waves per
+// SIMD: waves w and w + 4 take the same 32 output channels and half of the
+// chunk's pairs, for the band's first ceil(NB/2) pixel blocks (w < 4) or the
+// other NB - ceil(NB/2) (w >= 4), so each SIMD always has a second wave to
+// issue while one waits.  Every wave stages one channel slot per chunk.
+// Otherwise as conv_f32_band_kernel (same staging modes, same LDS layout,
+// same matrix-core sequence per output, P0 + P1 in the same order), so its
+// outputs are bitwise those of the one-wave-per-SIMD kernel.
+template <int FH, int FW, int NB, int MODE>
+__global__ __launch_bounds__(2 * kBandThreads, 1) void conv_f32_band8_kernel(F32BandArgs a) {
+    constexpr int T = FH * FW;
+    constexpr int PP = 2;                            // channel pairs of a chunk per wave
+    constexpr int STEPS = PP * T;                    // k-steps of a chunk per wave
+    constexpr int NJ = band_copies(MODE) / 2;        // copies per wave per chunk: one slot
+    constexpr int DPT = (NJ + STEPS - 1) / STEPS;    // copies issued after each k-step
+    constexpr int PAIR_B = 2 * kBandSlot * 4;        // LDS bytes from one pair's slots to the next
+    constexpr int NB0 = (NB + 1) / 2;                // pixel blocks of the waves 0-3
+    extern __shared__ __align__(16) float S[];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // 0 .. 7
+    const int ph = wv >> 2, cb = (wv >> 1) & 1, ks = wv & 1;
+    const int bid = a.xcd_remap ? (int)(blockIdx.x & 7) * (a.grid >> 3) + (int)(blockIdx.x >> 3)
+                                : (int)blockIdx.x;
+    const BandTile tile = band_tile(a, bid);
+    const int slot = lane >> 5, col = lane & 31;
+    const int kout = (tile.kt * 2 + cb) * 32 + col;
+    const __amdgpu_buffer_rsrc_t wres = band_rsrc(a.wt, (uint32_t)((size_t)a.k * a.c * T * 4));
+    const int wlane = ((kout * a.c) + 2 * ks * PP + slot) * T * 4;
+    const size_t img_elems = (size_t)a.c * a.plane_src;
+    const __amdgpu_buffer_rsrc_t sres =
+        band_rsrc(a.src + (size_t)tile.img * img_elems, (uint32_t)(img_elems * 4));
+    const int plane_bytes = a.plane_src * 4;
+    uint32_t sofs[NJ];
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) sofs[s] = band_source(a, tile, MODE, FH, s, lane);
+
+    // Copy j of chunk ch into stage ST: channel slot wv, part j.
+    auto copy = [&](int j, int ch, auto st_tag) {
+        constexpr int ST = decltype(st_tag)::value;
+        if (MODE == kBandRaw && j >= a.rgroups) return;
+        const uint32_t cbytes = (uint32_t)((ch * kBandChunk + wv) * plane_bytes);
+        char* dst = reinterpret_cast<char*>(S) + ST * kBandStageBytes + band_dest_slot(a, MODE, wv, j);
+        if (MODE != kBandRaw || lane < a.rrpi * a.rlanes) {
+#if defined(__HIP_DEVICE_COMPILE__)   // (16-byte LDS copies exist on gfx950 only; the host pass checks them too)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sres, (lds_void*)dst,
+                                                     MODE == kBandWide || MODE == kBandRaw ? 16 : 4,
+                                                     sofs[j] + cbytes, 0, 0, 0);
+#endif
+        }
+    };
+    auto load_filter = [&](int ch, int q) {   // k-step q = pp*T + t
+        const int pp = q / T, t = q - pp * T;
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                             wres, wlane + (2 * pp * T + t) * 4, ch * kBandChunk * T * 4, 0));
+    };
+    auto land = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+    };
+
+    // The whole kernel for NBW pixel blocks starting at block B0.
+    auto body = [&](auto nbw_tag) {
+        constexpr int NBW = decltype(nbw_tag)::value;
+        const int B0 = ph * NB0;
+        uint32_t bb[NBW];
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) bb[b] = band_window(a, tile, FH, 2 * ks * PP + slot, lane, B0 + b);
+        float fa0[STEPS], fa1[STEPS];
+        f32x16 acc[NBW];
+#pragma unroll
+        for (int b = 0; b < NBW; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
+        auto chunk = [&](auto st_tag, const float (&fa)[STEPS], float (&fn)[STEPS], int ch) {
+            constexpr int ST = decltype(st_tag)::value;
+            const char* base = reinterpret_cast<const char*>(S) + ST * kBandStageBytes;
+            float bv[2][NBW];
+            auto read_step = [&](int q, float (&dst)[NBW]) {
+                const int pp = q / T, t = q - pp * T;
+                const int u = t / FW, v = t - u * FW;
+                const int off = pp * PAIR_B + (MODE == kBandRaw ? (u * a.rpitch + v) * 4 : (v * FH + u) * 4);
+#pragma unroll
+                for (int b = 0; b < NBW; ++b) dst[b] = *reinterpret_cast<const float*>(base + bb[b] + off);
+            };
+            read_step(0, bv[0]);
+#pragma unroll
+            for (int q = 0; q < STEPS; ++q) {
+                if (q + 1 < STEPS) read_step(q + 1, bv[(q + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int b = 0; b < NBW; ++b)
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[q], bv[q & 1][b], acc[b], 0, 0, 0);
+                BAND_PIN_VMEM();
+#pragma unroll
+                for (int d = 0; d < DPT; ++d)
+                    if (q * DPT + d < NJ) copy(q * DPT + d, ch + 1, std::integral_constant<int, 1 - ST>());
+                fn[q] = load_filter(ch + 1, q);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) copy(j, 0, std::integral_constant<int, 0>());
+#pragma unroll
+        for (int q = 0; q < STEPS; ++q) fa0[q] = load_filter(0, q);
+        land();
+        for (int ch = 0; ch < a.nchunks; ch += 2) {   // nchunks is even
+            chunk(std::integral_constant<int, 0>(), fa0, fa1, ch);
+            land();
+            chunk(std::integral_constant<int, 1>(), fa1, fa0, ch + 1);
+            land();
+        }
+        // P0 + P1 through LDS, R[block][channel][pixel], as the one-wave kernel
+        constexpr int RP = NB * 32;
+        constexpr int RW = 32 * RP;
+        float* R = S + cb * RW;
+        if (ks > 0) {
+#pragma unroll
+            for (int b = 0; b < NBW; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    R[ch * RP + (B0 + b) * 32 + col] = acc[b][r];
+                }
+        }
+        __syncthreads();
+        if (ks == 0) {
+            const size_t hw = (size_t)a.ho * a.wo;
+            float* yo = a.y + ((size_t)tile.img * a.k + (size_t)(tile.kt * 2 + cb) * 32) * hw + (size_t)tile.m0 * a.wo;
+#pragma unroll
+            for (int b = 0; b < NBW; ++b) {
+                const int p = (B0 + b) * 32 + col;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
+                    const float v = acc[b][r] + R[ch * RP + p];
+                    if (p < tile.npix) yo[(size_t)ch * hw + p] = v;
+                }
+            }
+        }
+    };
+    if (ph == 0)
+        body(std::integral_constant<int, NB0>());
+    else
+        body(std::integral_constant<int, NB - NB0>());
+}
+
 // Layers with few input channels (C = 3: the 7x7 stride-2 stems, the 11x11
 // stride-4 and 3x3 first layers): the whole reduction of a band is C*Fh*Fw
 // elements, so a band's C strips are staged at once.  The kernel is
@@ -558,6 +705,27 @@ void launch_band_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
                        (size_t)lds, stream, a);
 }
 
+template <int FH, int FW, int NB, int MODE>
+void launch_band8_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)conv_f32_band8_kernel<FH, FW, NB, MODE>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL((conv_f32_band8_kernel<FH, FW, NB, MODE>), dim3((unsigned)a.grid), dim3(2 * kBandThreads),
+                       (size_t)lds, stream, a);
+}
+
+template <int FH, int FW, int NB>
+void launch_band8_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
+    if (a.mode == kBandRaw)
+        launch_band8_v<FH, FW, NB, kBandRaw>(a, lds, stream);
+    else if (a.mode == kBandGather)
+        launch_band8_v<FH, FW, NB, kBandGather>(a, lds, stream);
+    else if (a.mode == kBandNarrow)
+        launch_band8_v<FH, FW, NB, kBandNarrow>(a, lds, stream);
+    else
+        launch_band8_v<FH, FW, NB, kBandWide>(a, lds, stream);
+}
+
 template <int FH, int FW, int NB, int KS>
 void launch_band_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
     if (a.mode == kBandRaw)
@@ -682,8 +850,13 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
     const F32BandArgs a = band_args_f32(g, p, fused, src, w, y);
     const int64_t lds = p.lds_bytes;
     if (p.ks == 2) {
-        if (p.nb == 12) launch_band_nb<3, 3, 12, 2>(a, lds, stream);
-        else launch_band_nb<3, 3, 13, 2>(a, lds, stream);
+        if (kBandTwoWavesPerSimd) {
+            if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
+            else launch_band8_nb<3, 3, 13>(a, lds, stream);
+        } else {
+            if (p.nb == 12) launch_band_nb<3, 3, 12, 2>(a, lds, stream);
+            else launch_band_nb<3, 3, 13, 2>(a, lds, stream);
+        }
         return 0;
     }
 #define BAND_NB4(FW_)                                                   \
