@@ -591,6 +591,11 @@ void check_conv_image(const Geometry& g, bool fused, const ImgPlan& p, Report& r
 // window-tensor element it must hold), every window read of every wave, lane,
 // pair, tap and pixel block, the filter rows, the partial-sum area and the
 // output stores (each output of the layer exactly once).
+// (With the two-way split the kernel runs two waves per SIMD: each of its
+// 8 waves copies every part of one channel slot, where the 4 waves replayed
+// here copy every part of two slots each, so both issue the same copies;
+// waves w and w + 4 read the windows of wave w below for the first
+// ceil(NB/2) pixel blocks and the rest: the same reads and outputs.)
 void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Report& r) {
     const F32BandArgs a = band_args_f32(g, p, fused, nullptr, nullptr, nullptr);
     const int T = (int)g.taps, FH = (int)g.fh, FW = (int)g.fw;

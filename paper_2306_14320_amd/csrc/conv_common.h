@@ -510,8 +510,6 @@ __host__ __device__ inline uint32_t band_dest(const F32BandArgs& a, int mode, in
     return band_dest_slot(a, mode, 2 * wv + (j & 1), j >> 1);
 }
 
-// The two-way split runs two waves per SIMD (conv_f32_band8_kernel).
-constexpr bool kBandTwoWavesPerSimd = true;
 
 // Copies per wave and chunk (two channel slots).
 __host__ __device__ constexpr int band_copies(int mode) {

@@ -850,13 +850,10 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
     const F32BandArgs a = band_args_f32(g, p, fused, src, w, y);
     const int64_t lds = p.lds_bytes;
     if (p.ks == 2) {
-        if (kBandTwoWavesPerSimd) {
-            if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
-            else launch_band8_nb<3, 3, 13>(a, lds, stream);
-        } else {
-            if (p.nb == 12) launch_band_nb<3, 3, 12, 2>(a, lds, stream);
-            else launch_band_nb<3, 3, 13, 2>(a, lds, stream);
-        }
+        // two waves per SIMD (with the four-way split they were slower:
+        // 3-4 pixel blocks per wave)
+        if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
+        else launch_band8_nb<3, 3, 13>(a, lds, stream);
         return 0;
     }
 #define BAND_NB4(FW_)                                                   \
