@@ -553,6 +553,7 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
 // two waves per block of 32 output channels splitting the k-steps; one
 // persistent workgroup per CU walks through per_wg consecutive bands.
 constexpr int kSmallCChannels = 3;          // C the kernels are built for
+constexpr int kSmallCWavesPerSimd = 2;      // 8 waves, each half of the band's pixel blocks
 
 // Band bid of the small-C kernel: output-channel group slowest, so that a
 // workgroup's run of consecutive bands shares one filter.

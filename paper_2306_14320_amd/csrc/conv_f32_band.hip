@@ -419,22 +419,24 @@ __global__ __launch_bounds__(2 * kBandThreads, 1) void conv_f32_band8_kernel(F32
 // u < ceil(Fh/2); for odd Fh the middle row comes up in both slots and the
 // second slot's copy gets zero weights, so every read stays inside the
 // pixel's window.  Waves (cb, ks): 2 blocks of 32 output channels x 2
-// halves of the C*ceil(Fh/2)*Fw k-steps.
-template <int C, int FH, int FW, int NB, int MODE>
-__global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(F32BandArgs a) {
+// halves of the C*ceil(Fh/2)*Fw k-steps; with WPS = 2 waves w and w + 4 take
+// wave w's share for the first ceil(NB/2) pixel blocks and the rest, two
+// waves per SIMD, and the staging copies go round the 8 waves.
+template <int C, int FH, int FW, int NB, int MODE, int WPS>
+__global__ __launch_bounds__(WPS * kBandThreads, 1) void conv_f32_band_small_c_kernel(F32BandArgs a) {
     constexpr int HU = (FH + 1) / 2;
     constexpr int S = C * HU * FW;      // k-steps of the whole reduction
     constexpr int SW = (S + 1) / 2;     // k-steps of the first half (the second takes S - SW)
     constexpr int RP = NB * 32;
     constexpr int RW = 32 * RP;         // floats of one block's partial sums
-    constexpr int NOUT = NB * 16;       // output registers per lane
-    constexpr int SPS = (2 * NOUT + SW - 1) / SW;   // stores issued per k-step (done halfway through)
     constexpr bool GATHER = MODE == kBandGather;
+    constexpr int NT = WPS * kBandThreads, NWV = 4 * WPS;   // threads, waves
+    constexpr int NB0 = (NB + WPS - 1) / WPS;   // pixel blocks of the waves 0-3 (the rest: waves 4-7)
     extern __shared__ __align__(16) float L[];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int cb = wv >> 1, ks = wv & 1;
+    const int ph = wv >> 2, cb = (wv >> 1) & 1, ks = wv & 1;
     const int slot = lane >> 5, col = lane & 31;
     // LDS: two strip buffers (unfused) or two buffers of zero-padded raw
     // input rows (fused), then the partial sums of the two blocks
@@ -454,7 +456,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         const int np = smallc_parts(a, t);
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            for (int sp = (wv - c * np) & 3; sp < np; sp += 4) {
+            for (int sp = (wv - c * np) & (NWV - 1); sp < np; sp += NWV) {
                 const uint32_t off = band_source(a, t, MODE, FH, sp, lane);
                 char* dst =
                     reinterpret_cast<char*>(L) + (buf * buf_f + c * a.slotf + sp * (MODE == kBandWide ? 256 : 64)) * 4;
@@ -483,7 +485,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         const int per = a.rawwide ? 4 : 1;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            for (int r = (wv - c * a.rrows) & 3; r < a.rrows; r += 4) {
+            for (int r = (wv - c * a.rrows) & (NWV - 1); r < a.rrows; r += NWV) {
                 const int yy = y0 + r;   // wave-uniform
                 const uint32_t rowoff = (uint32_t)((c * a.h + yy) * a.w) * 4u;
                 const bool in = yy >= 0 && yy < a.h;
@@ -508,7 +510,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         // the pad columns (rlpad before each raw row, rpitch - rlpad - W after)
         // of every raw row of both buffers
         const int padc = a.rpitch - a.w;
-        for (int i = tid; i < 2 * C * a.rrows * padc; i += kBandThreads) {
+        for (int i = tid; i < 2 * C * a.rrows * padc; i += NT) {
             const int row = i / padc, k = i - row * padc;
             L[row * a.rpitch + (k < a.rlpad ? k : a.w + k)] = 0.0f;
         }
@@ -542,18 +544,24 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             load_filter_half(std::integral_constant<int, 1>(), kt, f);
     };
 
+    // The rest for NBW pixel blocks from block B0 (this wave's share).
+    auto body = [&](auto nbw_tag) {
+    constexpr int NBW = decltype(nbw_tag)::value;
+    constexpr int NOUT = NBW * 16;       // output registers per lane
+    constexpr int SPS = (2 * NOUT + SW - 1) / SW;   // stores issued per k-step (done halfway through)
+    const int B0 = ph * NB0;
     // y through a buffer resource over the previous band's image: a store
     // whose offset lies past its end (pixels past the band, or no previous
     // band yet) is dropped
     const size_t hw = (size_t)a.ho * a.wo;
     __amdgpu_buffer_rsrc_t yres = band_rsrc(a.y, 0u);
     float fa[SW];
-    f32x16 acc[NB], out[NB];
+    f32x16 acc[NBW], out[NBW];
     // byte offset in y of the previous band's channel 0, pixel (lane, block);
     // the channel adds ch*hw*4 (scalar)
-    uint32_t ybase[NB];
+    uint32_t ybase[NBW];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
+    for (int b = 0; b < NBW; ++b) {
         ybase[b] = kBandOutside;
 #pragma unroll
         for (int r = 0; r < 16; ++r) out[b][r] = 0.0f;
@@ -587,19 +595,19 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         }
         // byte offset of each block's window: per channel (unfused), or of
         // channel 0 (fused, the channel and filter row add a uniform offset)
-        uint32_t bb[GATHER ? 1 : C][NB];
+        uint32_t bb[GATHER ? 1 : C][NBW];
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
+        for (int b = 0; b < NBW; ++b) {
             if constexpr (GATHER) {
-                bb[0][b] = smallc_raw_window(a, tile, FH, lane, b) + (uint32_t)(cur * buf_f) * 4u;
+                bb[0][b] = smallc_raw_window(a, tile, FH, lane, B0 + b) + (uint32_t)(cur * buf_f) * 4u;
             } else {
-                const uint32_t w0 = smallc_window(a, tile, FH, lane, b) + (uint32_t)(cur * buf_f) * 4u;
+                const uint32_t w0 = smallc_window(a, tile, FH, lane, B0 + b) + (uint32_t)(cur * buf_f) * 4u;
 #pragma unroll
                 for (int c = 0; c < C; ++c) bb[c][b] = w0 + (uint32_t)(c * a.slotf) * 4u;
             }
         }
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
+        for (int b = 0; b < NBW; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
 
@@ -609,18 +617,18 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         auto run = [&](auto ks_tag) {
             constexpr int KSI = decltype(ks_tag)::value;
             constexpr int Q0 = KSI * SW, NQ = KSI == 0 ? SW : S - SW;
-            float bv[2][NB];
-            auto read_step = [&](int i, float (&dst)[NB]) {
+            float bv[2][NBW];
+            auto read_step = [&](int i, float (&dst)[NBW]) {
                 const int q = Q0 + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
                 const char* Lb = reinterpret_cast<const char*>(L);
                 if constexpr (GATHER) {
                     const int cu = (c * a.rrows + u) * a.rpitch * 4;
 #pragma unroll
-                    for (int b = 0; b < NB; ++b)
+                    for (int b = 0; b < NBW; ++b)
                         dst[b] = *reinterpret_cast<const float*>(Lb + bb[0][b] + cu + v * 4);
                 } else {
 #pragma unroll
-                    for (int b = 0; b < NB; ++b)
+                    for (int b = 0; b < NBW; ++b)
                         dst[b] = *reinterpret_cast<const float*>(Lb + bb[c][b] + (v * FH + u) * 4);
                 }
             };
@@ -630,7 +638,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
                 if (i + 1 < NQ) read_step(i + 1, bv[(i + 1) & 1]);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int b = 0; b < NB; ++b)
+                for (int b = 0; b < NBW; ++b)
                     acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i], bv[i & 1][b], acc[b], 0, 0, 0);
                 if constexpr (KSI == 0) {
 #pragma unroll
@@ -655,22 +663,22 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
         // this band's stores stay in flight.
         if (ks > 0) {
 #pragma unroll
-            for (int b = 0; b < NB; ++b)
+            for (int b = 0; b < NBW; ++b)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
-                    R[ch * RP + b * 32 + col] = acc[b][r];
+                    R[ch * RP + (B0 + b) * 32 + col] = acc[b][r];
                 }
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);
         asm volatile("s_barrier" ::: "memory");
         if (ks == 0) {
 #pragma unroll
-            for (int b = 0; b < NB; ++b)
+            for (int b = 0; b < NBW; ++b)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
-                    out[b][r] = acc[b][r] + R[ch * RP + b * 32 + col];
+                    out[b][r] = acc[b][r] + R[ch * RP + (B0 + b) * 32 + col];
                 }
             yres = band_rsrc(a.y + (size_t)tile.img * a.k * hw, (uint32_t)((size_t)a.k * hw * 4));
             const uint32_t y0 = (uint32_t)((((size_t)(tile.kt * 2 + cb) * 32 + slot * 4) * hw + (size_t)tile.m0 * a.wo) * 4);
@@ -678,8 +686,8 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             // weights and stores nothing)
             const bool kin = (tile.kt * 2 + cb) * 32 < a.k;
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int p = b * 32 + col;
+            for (int b = 0; b < NBW; ++b) {
+                const int p = (B0 + b) * 32 + col;
                 ybase[b] = kin && p < tile.npix ? y0 + (uint32_t)p * 4u : kBandOutside;
             }
         }
@@ -693,6 +701,15 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_small_c_kernel(
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(elem(out[b], r)), yres, ybase[b],
                                                   (int)(chs * hw * 4), 0);
         }
+    }
+    };
+    if constexpr (WPS == 1) {
+        body(std::integral_constant<int, NB>());
+    } else {
+        if (ph == 0)
+            body(std::integral_constant<int, NB0>());
+        else
+            body(std::integral_constant<int, NB - NB0>());
     }
 }
 
@@ -876,12 +893,12 @@ namespace {
 
 template <int FH, int NB, int MODE>
 void launch_small_c_v(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
-    constexpr int C = kSmallCChannels;
+    constexpr int C = kSmallCChannels, WPS = kSmallCWavesPerSimd;
     if (lds > 64 * 1024)
-        (void)hipFuncSetAttribute((const void*)conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE>,
+        (void)hipFuncSetAttribute((const void*)conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE, WPS>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL((conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE>), dim3((unsigned)a.grid),
-                       dim3(kBandThreads), (size_t)lds, stream, a);
+    hipLaunchKernelGGL((conv_f32_band_small_c_kernel<C, FH, FH, NB, MODE, WPS>), dim3((unsigned)a.grid),
+                       dim3(WPS * kBandThreads), (size_t)lds, stream, a);
 }
 
 template <int FH, int NB>
