@@ -217,9 +217,10 @@ int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void*
  * the process), one of:
  *   "f32_bands"          fp32, a band of output rows of one image x 32 or 64
  *                        output channels per workgroup
- *   "f32_bands_small_c"  fp32 with 3 input channels and a 7x7 filter: a band
- *                        of rows x 64 output channels, the whole reduction
- *                        staged at once
+ *   "f32_bands_small_c"  fp32 with 3 input channels and a 3x3, 7x7 or 11x11
+ *                        filter: runs of bands of rows x 64 output channels
+ *                        per workgroup, each band's whole reduction staged
+ *                        at once
  *   "f32_tiles"          fp32, tiles of output channels x pixels
  *   "bf16_one_image"     bf16, one image x 128 output channels per workgroup
  *   "bf16_tiles"         bf16, tiles of output channels x pixels
