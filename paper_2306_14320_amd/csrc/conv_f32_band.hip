@@ -1,8 +1,8 @@
 // fp32 im2win convolution by bands of output rows: a workgroup computes a
-// band of rows of one image for 32 or 64 output channels, with all 4 waves
-// busy on the same amount of matrix-core work, so that a layer of a few
-// hundred workgroups fills the chip without the quantization of fixed
-// pixel tiles.
+// band of rows of one image for 32 or 64 output channels, with every SIMD
+// busy on the same amount of matrix-core work (one wave each, or two for the
+// two-way split), so that a layer of a few hundred workgroups fills the chip
+// without the quantization of fixed pixel tiles.
 //
 // The same implicit GEMM as the other convolution kernels (Alg. 2: the
 // window of output pixel (m, n) is the run [n*sw*Fh, (n*sw + Fw)*Fh) of
