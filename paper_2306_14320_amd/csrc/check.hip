@@ -601,18 +601,23 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
     const int T = (int)g.taps, FH = (int)g.fh, FW = (int)g.fw;
     const int KS = p.ks, PP = 4 / KS, CB = 4 / KS, nb = p.nb;
     const int64_t stage_f = kBandStageBytes / 4;
+    // several whole images per band: a run of ipb*Ho rows
+    const bool multi = a.ipb > 1;
+    const int64_t brows = multi ? (int64_t)a.ipb * g.ho : a.rows;
+    const int64_t groups = multi ? (g.n + a.ipb - 1) / a.ipb : g.n * a.nbands;
     if (2 * (int64_t)kBandStageBytes > p.lds_bytes ||
         (int64_t)(KS == 4 ? 4 : 2) * 32 * nb * 32 * 4 > p.lds_bytes || p.lds_bytes > kConvLdsMaxBytes ||
-        (KS != 4 && KS != 2) || a.rows < 1 || nb * 32 < a.rows * a.wo || (nb - 1) * 32 >= a.rows * a.wo ||
-        (int64_t)a.rows * g.row_len + 3 > 64 * kBandMaxSeg || g.c % (2 * kBandChunk) || g.k % (32 * CB) ||
+        (KS != 4 && KS != 2) || a.rows < 1 || nb * 32 < brows * a.wo || (nb - 1) * 32 >= brows * a.wo ||
+        brows * g.row_len + 3 > 64 * kBandMaxSeg || g.c % (2 * kBandChunk) || g.k % (32 * CB) ||
         (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho ||
-        (int64_t)g.n * a.nbands * a.nkt != a.grid) {
-        r.fail("fp32 band conv: plan (ks %d, %d rows, nb %d, %lld bytes of LDS)", KS, a.rows, nb,
+        (multi && (a.rows != g.ho || a.nbands != 1 || a.ipb > g.n || a.mode == kBandRaw)) ||
+        groups * a.nkt != a.grid) {
+        r.fail("fp32 band conv: plan (ks %d, %d rows, %d images, nb %d, %lld bytes of LDS)", KS, a.rows, a.ipb, nb,
                (long long)p.lds_bytes);
         return;
     }
     F32BandArgs raw_probe = a;
-    const bool raw = fused && band_raw_mode(g, a.rows, nullptr, &raw_probe);
+    const bool raw = fused && !multi && band_raw_mode(g, a.rows, nullptr, &raw_probe);
     if (a.mode != (fused ? (raw ? kBandRaw : kBandGather) : (g.ho * g.row_len) % 4 == 0 ? kBandWide : kBandNarrow))
         r.fail("fp32 band conv: copy mode %d", a.mode);
     if (raw && (a.rlpad < g.pw || a.rlpad % 4 || a.rpitch != 4 * a.rlanes || a.rlanes > 64 || a.rrpi != 64 / a.rlanes ||
@@ -635,19 +640,39 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
     const int per = a.mode == kBandWide || a.mode == kBandRaw ? 4 : 1;   // floats per lane and copy
     const uint64_t slab = (uint64_t)g.c * a.plane_src * 4;
     const uint64_t plane_bytes = (uint64_t)a.plane_src * 4;
-    if (slab >= kBandOutside) r.fail("fp32 band conv: image slab of %llu bytes", (unsigned long long)slab);
+    if ((uint64_t)a.ipb * slab >= kBandOutside)
+        r.fail("fp32 band conv: source of %d image slabs of %llu bytes", a.ipb, (unsigned long long)slab);
     const int64_t kZero = -2;
+    const int64_t hw = g.ho * g.wo;
     std::vector<int64_t> holds(stage_f);
-    std::vector<uint8_t> out((size_t)g.k * g.ho * g.wo, 0);
-    for (int band = 0; band < a.nbands && r.violations == 0; ++band) {
-        // (image 0, channel group 0 of the band: the staging and the reads
-        // do not depend on either)
+    // outputs: of image 0 (bands of one image: every band of it), or of the
+    // band's images (several images: each band checked on its own)
+    std::vector<uint8_t> out((size_t)g.k * hw * (multi ? a.ipb : 1), 0);
+    // bands checked: every band of image 0, or (several images) the first
+    // band and the last, which may hold fewer images
+    std::vector<int> checked;
+    if (multi) {
+        checked.push_back(0);
+        if (groups > 1) checked.push_back((int)groups - 1);
+    } else {
+        for (int band = 0; band < a.nbands; ++band) checked.push_back(band);
+    }
+    for (int band : checked) {
+        if (r.violations) break;
+        // (channel group 0 of the band: the staging and the reads do not
+        // depend on it)
         const BandTile t = band_tile(a, band * a.nkt);
-        if (t.band != band || t.img != 0 || t.kt != 0 || t.m0 != band * a.rows || t.nrows < 1 ||
+        const int want_img = multi ? band * a.ipb : 0;
+        const int want_nimg = multi ? (int)std::min<int64_t>(a.ipb, g.n - want_img) : 1;
+        if (t.band != (multi ? 0 : band) || t.img != want_img || t.nimg != want_nimg || t.kt != 0 ||
+            t.m0 != (multi ? 0 : band * a.rows) || t.nrows < 1 || (multi && t.nrows != want_nimg * g.ho) ||
             t.npix > nb * 32 || (a.mode == kBandWide && t.shift + (int64_t)t.nrows * g.row_len > 64 * kBandMaxSeg)) {
-            r.fail("fp32 band conv: band %d (rows %d + %d, shift %d)", band, t.m0, t.nrows, t.shift);
+            r.fail("fp32 band conv: band %d (rows %d + %d, image %d + %d, shift %d)", band, t.m0, t.nrows, t.img,
+                   t.nimg, t.shift);
             return;
         }
+        if (multi) std::fill(out.begin(), out.end(), 0);
+        const uint64_t src_bytes = (uint64_t)t.nimg * slab;   // the copies' buffer: the band's image slabs
         // staging: holds[float of a stage] = slot << 24 | window-tensor
         // element of the plane, or kZero (a copy wrote zero), or -1
         std::fill(holds.begin(), holds.end(), -1);
@@ -665,13 +690,18 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                         return;
                     }
                     // the last real chunk reads inside the slab; the one past
-                    // it (issued, never used) reads only zeros; no offset wraps
+                    // it (issued, never used) reads only zeros (several
+                    // images: or the next image's first planes, inside the
+                    // source); no offset wraps.  (Several images: off lies
+                    // in the channel-0 plane of one of the band's images.)
                     const uint64_t last = ((uint64_t)(a.nchunks - 1) * kBandChunk + cc) * plane_bytes + off;
                     const uint64_t past = ((uint64_t)a.nchunks * kBandChunk + cc) * plane_bytes + off;
-                    if (past >= (uint64_t(1) << 32) || past < slab ||
-                        (off != kBandOutside && (off + per * 4 > plane_bytes || last + per * 4 > slab))) {
-                        r.fail("fp32 band conv: copy %d of wave %d lane %d reads byte %llu of a %llu-byte slab", j,
-                               wv, lane, (unsigned long long)last, (unsigned long long)slab);
+                    if (past >= (uint64_t(1) << 32) || (!multi && past < src_bytes) ||
+                        (off != kBandOutside &&
+                         ((off % slab) + per * 4 > plane_bytes || off / slab >= (uint64_t)t.nimg ||
+                          last + per * 4 > src_bytes))) {
+                        r.fail("fp32 band conv: copy %d of wave %d lane %d reads byte %llu of %llu source bytes", j,
+                               wv, lane, (unsigned long long)last, (unsigned long long)src_bytes);
                         return;
                     }
                     if (a.mode == kBandRaw) {
@@ -703,17 +733,22 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                                                      : (int64_t)(j >> 1) * 256 + lane * 4 + e - t.shift;
                         int64_t v = kZero;
                         if (off != kBandOutside) {
-                            const int64_t elem = (int64_t)t.m0 * g.row_len + pos;   // element of the plane
-                            if (!fused && (int64_t)off / 4 + e != elem) {
+                            // element of the band's run of rows (several
+                            // images: row m of the run is row m % Ho of image
+                            // m / Ho of the band, C planes further per image)
+                            const int64_t elem = (int64_t)t.m0 * g.row_len + pos;
+                            const int64_t q = multi ? elem / g.row_len / g.ho : 0;
+                            if (!fused && (int64_t)off / 4 + e != elem + q * (g.c - 1) * a.plane_src) {
                                 r.fail("fp32 band conv: strip position %lld copied from element %u", (long long)pos,
                                        off / 4 + e);
                                 return;
                             }
                             if (fused) {   // the x element of window-tensor element elem (transform's definition)
-                                const int64_t m = elem / g.row_len, k = (elem % g.row_len) / FH, u = elem % FH;
+                                const int64_t m = elem / g.row_len - q * g.ho, k = (elem % g.row_len) / FH,
+                                              u = elem % FH;
                                 const int64_t yy = m * g.sh + u - g.ph, xx = k - g.pw;
                                 if (pos < 0 || pos >= (int64_t)t.nrows * g.row_len || yy < 0 || yy >= g.h ||
-                                    xx < 0 || xx >= g.w || (int64_t)off / 4 != yy * g.w + xx) {
+                                    xx < 0 || xx >= g.w || (int64_t)off / 4 != q * g.c * a.plane_src + yy * g.w + xx) {
                                     r.fail("fp32 band conv: strip position %lld gathered from x element %u",
                                            (long long)pos, off / 4);
                                     return;
@@ -736,7 +771,8 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                 for (int b = 0; b < nb; ++b) {
                     int pix = b * 32 + (lane & 31);
                     if (pix > t.npix - 1) pix = t.npix - 1;
-                    const int64_t m = t.m0 + pix / g.wo, n = pix % g.wo;
+                    const int64_t m = t.m0 + pix / g.wo, n = pix % g.wo;   // row of the band's run
+                    const int64_t mi = multi ? m % g.ho : m;                   // row of its image
                     for (int pp = 0; pp < PP; ++pp) {
                         const int cc = 2 * (ks * PP + pp) + (lane >> 5);
                         for (int tap = 0; tap < T; ++tap) {
@@ -744,7 +780,7 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                             const int64_t f = band_window(a, t, FH, 2 * ks * PP + (lane >> 5), lane, b) / 4 +
                                               (int64_t)pp * 2 * kBandSlot +
                                               (a.mode == kBandRaw ? (int64_t)u * a.rpitch + v : (int64_t)v * FH + u);
-                            const int64_t yy = m * g.sh + u - g.ph, xx = n * g.sw + v - g.pw;
+                            const int64_t yy = mi * g.sh + u - g.ph, xx = n * g.sw + v - g.pw;
                             const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
                             // window-tensor element (raw mode: the x element)
                             const int64_t elem =
@@ -774,16 +810,31 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
                     for (int ch = 0; ch < 32; ++ch) {
                         const int64_t j = (int64_t)(kt * CB + cb) * 32 + ch;
                         if (j >= g.k) { r.fail("fp32 band conv: output channel %lld", (long long)j); return; }
-                        ++out[(size_t)j * g.ho * g.wo + (size_t)t.m0 * g.wo + p2];
+                        // the kernel's store offset from the band's first
+                        // pixel of channel j
+                        const int64_t at = (int64_t)t.m0 * g.wo + p2 + band_image_skip(a, p2);
+                        const int64_t q = multi ? p2 / hw : 0;
+                        if (at != q * g.k * hw + p2 - q * hw + (int64_t)t.m0 * g.wo) {
+                            r.fail("fp32 band conv: pixel %d of band %d stored at %lld", p2, band, (long long)at);
+                            return;
+                        }
+                        ++out[(size_t)(j * hw + at)];
                     }
+                }
+        if (multi)
+            for (size_t i = 0; i < (size_t)t.nimg * g.k * hw; ++i)
+                if (out[i] != 1) {
+                    r.fail("fp32 band conv: output %zu of band %d stored %d times", i, band, (int)out[i]);
+                    return;
                 }
     }
     if (r.violations) return;
-    for (size_t i = 0; i < out.size(); ++i)
-        if (out[i] != 1) {
-            r.fail("fp32 band conv: output %zu of an image stored %d times", i, (int)out[i]);
-            return;
-        }
+    if (!multi)
+        for (size_t i = 0; i < out.size(); ++i)
+            if (out[i] != 1) {
+                r.fail("fp32 band conv: output %zu of an image stored %d times", i, (int)out[i]);
+                return;
+            }
     // filter rows: the last chunk's pair of the last channel group
     const int64_t wmax = (((int64_t)(a.nkt - 1) * CB * 32 + CB * 32 - 1) * g.c + (a.nchunks - 1) * kBandChunk + 7) * T + T - 1;
     if (wmax >= g.k * g.c * T)

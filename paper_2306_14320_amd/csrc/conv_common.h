@@ -426,27 +426,48 @@ struct F32BandArgs {
     int rawwide, rparts;   // small-C fused: raw rows by 16-byte copies; copies per row
     int rlanes, rrpi;      // band raw mode: 16-byte lanes per raw row (rpitch / 4), rows per copy
     int rgroups;           // band raw mode: copies per channel slot
-    FastDiv div_row, div_wo;   // by L, by Wo
+    int ipb;               // whole images per band (bands of several images), else 1
+    FastDiv div_row, div_wo, div_ho;   // by L, by Wo, by Ho
 };
 
 // The band of output rows, image and output-channel group of one workgroup.
+// A band of several whole images (ipb > 1) is a run of rows [0, nrows) that
+// goes on from one image's last row to the next image's first: the images'
+// strips sit back to back in a channel slot exactly as consecutive rows do,
+// so window reads need no change; copies and stores skip the other channels
+// of each image (band_image_skip).
 struct BandTile {
-    int img, band, kt;
+    int img, band, kt;     // first image, band of that image (0 for several images)
     int m0, nrows, npix;   // output rows [m0, m0 + nrows), npix = nrows * Wo
     int shift;             // wide copies: strip element 0 sits at slot position shift
+    int nimg;              // images the band covers (1, or up to ipb)
 };
 
 __host__ __device__ inline BandTile band_tile(const F32BandArgs& a, int bid) {
     BandTile t;
     t.kt = bid % a.nkt;
     const int ib = bid / a.nkt;
-    t.band = ib % a.nbands;
-    t.img = ib / a.nbands;
-    t.m0 = t.band * a.rows;
-    t.nrows = a.ho - t.m0 < a.rows ? a.ho - t.m0 : a.rows;
+    if (a.ipb > 1) {
+        t.band = 0;
+        t.img = ib * a.ipb;
+        t.nimg = a.n - t.img < a.ipb ? a.n - t.img : a.ipb;
+        t.m0 = 0;
+        t.nrows = t.nimg * a.ho;
+    } else {
+        t.band = ib % a.nbands;
+        t.img = ib / a.nbands;
+        t.nimg = 1;
+        t.m0 = t.band * a.rows;
+        t.nrows = a.ho - t.m0 < a.rows ? a.ho - t.m0 : a.rows;
+    }
     t.npix = t.nrows * a.wo;
     t.shift = a.mode == kBandWide ? (t.m0 * a.row_len) & 3 : 0;
     return t;
+}
+
+// Image (from the band's first) of band row m (0 for bands of one image).
+__host__ __device__ inline int band_row_image(const F32BandArgs& a, int m) {
+    return a.ipb > 1 ? (int)fast_div((uint32_t)m, a.div_ho) : 0;
 }
 
 // LDS byte address, in stage 0, of the window start of the pixel of `lane`
@@ -483,18 +504,40 @@ __host__ __device__ inline uint32_t band_source(const F32BandArgs& a, const Band
         const bool inside = r < a.rrows && yy >= 0 && yy < a.h && xx >= 0 && xx + 4 <= a.w;
         return inside ? (uint32_t)(yy * a.w + xx) * 4u : kBandOutside;
     }
+    // (several images: run element e of image q lies q images of C planes
+    // further in the source, i.e. e + q*(C-1)*plane elements)
     const int len = t.nrows * a.row_len;
+    const uint32_t skip = (uint32_t)(a.c - 1) * (uint32_t)a.plane_src;
     if (mode == kBandWide) {
         const int e = s * 256 + lane * 4;
-        return e < t.shift + len ? (uint32_t)(t.m0 * a.row_len - t.shift + e) * 4u : kBandOutside;
+        if (e >= t.shift + len) return kBandOutside;
+        const int el = t.m0 * a.row_len - t.shift + e;
+        const int q = band_row_image(a, (int)fast_div((uint32_t)el, a.div_row));
+        return ((uint32_t)el + (uint32_t)q * skip) * 4u;
     }
     const int pos = s * 64 + lane;
-    if (mode == kBandNarrow) return pos < len ? (uint32_t)(t.m0 * a.row_len + pos) * 4u : kBandOutside;
+    if (mode == kBandNarrow) {
+        if (pos >= len) return kBandOutside;
+        const int el = t.m0 * a.row_len + pos;
+        const int q = band_row_image(a, (int)fast_div((uint32_t)el, a.div_row));
+        return ((uint32_t)el + (uint32_t)q * skip) * 4u;
+    }
     const int ml = (int)fast_div((uint32_t)pos, a.div_row), rem = pos - ml * a.row_len;
     const int k = rem / fh, u = rem - k * fh;
-    const int yy = (t.m0 + ml) * a.sh + u - a.ph, xx = k - a.pw;
+    const int q = band_row_image(a, t.m0 + ml), mi = t.m0 + ml - q * a.ho;
+    const int yy = mi * a.sh + u - a.ph, xx = k - a.pw;
     const bool inside = pos < len && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w;
-    return inside ? (uint32_t)(yy * a.w + xx) * 4u : kBandOutside;
+    return inside ? ((uint32_t)(yy * a.w + xx) + (uint32_t)q * (uint32_t)a.c * (uint32_t)a.plane_src) * 4u
+                  : kBandOutside;
+}
+
+// Elements of y between pixel p of a band's output-channel plane and where
+// it is stored, beyond p itself: the other channels of the images before
+// p's (0 for bands of one image).
+__host__ __device__ inline uint32_t band_image_skip(const F32BandArgs& a, int p) {
+    if (a.ipb == 1) return 0;
+    const int q = (int)fast_div(fast_div((uint32_t)p, a.div_wo), a.div_ho);
+    return (uint32_t)q * (uint32_t)(a.k - 1) * (uint32_t)(a.ho * a.wo);
 }
 
 // LDS byte offset, within a stage, of part `part` of channel slot `slot`
@@ -529,17 +572,19 @@ struct F32BandPlan {
     int ks = 0;            // reduction split (4: 32 output channels per workgroup; 2: 64)
     int rows = 0;          // output rows per band
     int nb = 0;            // 32-pixel blocks per band
+    int ipb = 1;           // whole images per band (rows = Ho), or 1
     int64_t lds_bytes = 0, grid = 0;
     double eff = 0;        // useful share of the matrix-core work the launch occupies
 };
 
 // The plan of the band kernel, or !ok when the shape is not one it takes
 // (fp32; 3x3 or 3x5 filter; C a multiple of 16, K of 32 (of 64 with the
-// two-way split, 3x3 only); a band of rows whose strips fit a slot and whose
-// pixels fill 4-7 blocks of 32 (12-13 with the two-way split); at most 4
-// rounds of 256 workgroups, and at least 85% of the occupied matrix-core
-// work useful after rounding the grid to whole rounds).  The plan does not depend on fusion, so both
-// variants take a shape or neither.
+// two-way split, 3x3 only); a band of rows, or of several whole images,
+// whose strips fit a slot and whose pixels fill 4-7 blocks of 32 (12-13 with
+// the two-way split); at most 4 rounds of 256 workgroups, and at least 85%
+// of the occupied matrix-core work useful after rounding the grid to whole
+// rounds).  The plan does not depend on fusion, so both variants take a
+// shape or neither.
 F32BandPlan plan_band_f32(const Geometry& g);
 F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
                           float* y);

@@ -1,5 +1,6 @@
 // fp32 im2win convolution by bands of output rows: a workgroup computes a
-// band of rows of one image for 32 or 64 output channels, with every SIMD
+// band of rows of one image (or, for feature maps smaller than a band,
+// several whole images) for 32 or 64 output channels, with every SIMD
 // busy on the same amount of matrix-core work (one wave each, or two for the
 // two-way split), so that a layer of a few hundred workgroups fills the chip
 // without the quantization of fixed pixel tiles.
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
     // image's input planes.
     const size_t img_elems = (size_t)a.c * a.plane_src;
     const __amdgpu_buffer_rsrc_t sres =
-        band_rsrc(a.src + (size_t)tile.img * img_elems, (uint32_t)(img_elems * 4));
+        band_rsrc(a.src + (size_t)tile.img * img_elems, (uint32_t)(tile.nimg * img_elems * 4));
     const int plane_bytes = a.plane_src * 4;
 
     // Per-lane source byte offset (within one channel plane) of each copy of
@@ -215,10 +216,11 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
         const size_t hw = (size_t)a.ho * a.wo;
         float* yo = a.y + ((size_t)tile.img * a.k + (size_t)tile.kt * 32) * hw + (size_t)tile.m0 * a.wo;
         for (int p = tid; p < tile.npix; p += kBandThreads) {
+            float* yp = yo + p + band_image_skip(a, p);
 #pragma unroll 4
             for (int ch = 0; ch < 32; ++ch) {
                 const int e = ch * RP + p;
-                yo[(size_t)ch * hw + p] = ((S[e] + S[e + RW]) + S[e + 2 * RW]) + S[e + 3 * RW];
+                yp[(size_t)ch * hw] = ((S[e] + S[e + RW]) + S[e + 2 * RW]) + S[e + 3 * RW];
             }
         }
     } else {
@@ -243,11 +245,12 @@ __global__ __launch_bounds__(kBandThreads, 1) void conv_f32_band_kernel(F32BandA
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int p = b * 32 + col;
+                float* yp = yo + p + band_image_skip(a, p);
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
                     const float v = acc[b][r] + R[ch * RP + p];
-                    if (p < tile.npix) yo[(size_t)ch * hw + p] = v;
+                    if (p < tile.npix) yp[(size_t)ch * hw] = v;
                 }
             }
         }
@@ -285,7 +288,7 @@ __global__ __launch_bounds__(2 * kBandThreads, 1) void conv_f32_band8_kernel(F32
     const int wlane = ((kout * a.c) + 2 * ks * PP + slot) * T * 4;
     const size_t img_elems = (size_t)a.c * a.plane_src;
     const __amdgpu_buffer_rsrc_t sres =
-        band_rsrc(a.src + (size_t)tile.img * img_elems, (uint32_t)(img_elems * 4));
+        band_rsrc(a.src + (size_t)tile.img * img_elems, (uint32_t)(tile.nimg * img_elems * 4));
     const int plane_bytes = a.plane_src * 4;
     uint32_t sofs[NJ];
 #pragma unroll
@@ -386,11 +389,12 @@ __global__ __launch_bounds__(2 * kBandThreads, 1) void conv_f32_band8_kernel(F32
 #pragma unroll
             for (int b = 0; b < NBW; ++b) {
                 const int p = (B0 + b) * 32 + col;
+                float* yp = yo + p + band_image_skip(a, p);
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int ch = (r >> 2) * 8 + slot * 4 + (r & 3);
                     const float v = acc[b][r] + R[ch * RP + p];
-                    if (p < tile.npix) yo[(size_t)ch * hw + p] = v;
+                    if (p < tile.npix) yp[(size_t)ch * hw] = v;
                 }
             }
         }
@@ -796,6 +800,28 @@ F32BandPlan plan_band_f32(const Geometry& g) {
                 best.ks = ks;
                 best.rows = (int)rows;
                 best.nb = (int)nb;
+                best.ipb = 1;
+                best.grid = grid;
+                best.eff = eff;
+            }
+        }
+        // bands of several whole images, for feature maps smaller than a
+        // band (their strips back to back in a slot, within 2^30 bytes of
+        // source per band)
+        for (int64_t ipb = 2; ipb <= g.n; ++ipb) {
+            if (ipb * g.ho * g.row_len + 3 > 64 * kBandMaxSeg) break;
+            const int64_t nb = (ipb * g.ho * g.wo + 31) / 32;
+            if (ipb * g.c * std::max(g.h * g.w, g.ho * g.row_len) * 4 >= (int64_t(1) << 30)) break;
+            if (!band_shape_ok(g, ks, (int)nb)) continue;
+            const int64_t grid = (g.n + ipb - 1) / ipb * (g.k / (32 * (4 / ks)));
+            const int64_t rounds = (grid + 255) / 256;
+            if (rounds > kBandMaxRounds) continue;
+            const double eff = useful / ((double)rounds * 1024.0 * nb * pp);
+            if (eff > best.eff + 1e-9) {
+                best.ks = ks;
+                best.rows = (int)g.ho;
+                best.nb = (int)nb;
+                best.ipb = (int)ipb;
                 best.grid = grid;
                 best.eff = eff;
             }
@@ -823,9 +849,11 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
     a.row_len = (int)g.row_len;
     a.div_row = make_fastdiv((uint32_t)g.row_len);
     a.div_wo = make_fastdiv((uint32_t)g.wo);
+    a.div_ho = make_fastdiv((uint32_t)g.ho);
     a.plane_src = fused ? (int)(g.h * g.w) : (int)(g.ho * g.row_len);
     a.rows = p.rows;
-    a.nbands = (int)((g.ho + p.rows - 1) / p.rows);
+    a.ipb = p.ipb;
+    a.nbands = p.ipb > 1 ? 1 : (int)((g.ho + p.rows - 1) / p.rows);
     a.ks = p.ks;
     a.nkt = (int)(g.k / (32 * (4 / p.ks)));
     a.nchunks = (int)(g.c / kBandChunk);
@@ -835,7 +863,8 @@ F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, c
     const bool aligned = ((uintptr_t)src & 15) == 0 && (g.ho * g.row_len) % 4 == 0;
     a.rrows = a.rpitch = a.rlpad = a.rlanes = a.rrpi = a.rgroups = 0;
     a.rawwide = a.rparts = 0;
-    a.mode = fused ? (band_raw_mode(g, p.rows, src, &a) ? kBandRaw : kBandGather) : aligned ? kBandWide : kBandNarrow;
+    a.mode = fused ? (p.ipb == 1 && band_raw_mode(g, p.rows, src, &a) ? kBandRaw : kBandGather)
+                   : aligned ? kBandWide : kBandNarrow;
     a.slotf = 0;
     a.total = a.grid;
     a.per_wg = 1;

@@ -186,9 +186,16 @@ def test_launch_plans_in_bounds_on_paper_layers():
 # Shapes that the fp32 band kernel takes (n, c, h, w, k, fh, fw, sh, sw, ph,
 # pw): C a multiple of 16, K of 32 (64 with the two-way reduction split), a
 # band of output rows of 97-224 pixels (four-way split) or 353-416 (two-way),
-# at most 4 rounds of 256 workgroups with at least 85% of them useful.
+# or of several whole images of fewer pixels, at most 4 rounds of 256
+# workgroups with at least 85% of them useful.
 F32_BANDS = [
     (64, 128, 28, 28, 128, 3, 5, 2, 2, 1, 2),   # the rectangular-window layer: whole images
+    (128, 512, 7, 7, 512, 3, 3, 1, 1, 0, 0),    # Table 1 Conv12: bands of 8 images of 25 pixels
+    (128, 256, 12, 12, 512, 3, 3, 1, 1, 0, 0),  # Table 1 Conv6: bands of 4 images of 100 pixels
+    (124, 16, 7, 7, 512, 3, 3, 1, 1, 0, 0),     # several images, the last band of 4
+    (126, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),   # several images, the last band of 2
+    (128, 16, 5, 5, 512, 3, 3, 1, 1, 1, 1),     # several padded images
+    (128, 16, 7, 9, 512, 3, 5, 1, 1, 0, 0),     # several images, 3x5
     (32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1),     # the ResNet-style layer: 7-row bands, two-way split
     (128, 64, 56, 56, 64, 3, 3, 1, 1, 0, 0),    # Table 1 Conv9: ragged last band
     (128, 128, 28, 28, 128, 3, 3, 1, 1, 0, 0),  # Table 1 Conv10

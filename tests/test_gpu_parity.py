@@ -215,6 +215,12 @@ F32_BANDS = [
     (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2
     (8, 16, 52, 52, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2, fused from raw rows
     (2, 16, 28, 32, 4096, 3, 5, 2, 2, 1, 4),   # raw rows with 8 zero columns in front (pw = 4)
+    (128, 16, 7, 7, 512, 3, 3, 1, 1, 0, 0),    # bands of 8 whole images of 25 pixels (4-byte copies)
+    (124, 16, 7, 7, 512, 3, 3, 1, 1, 0, 0),    # the same, the last band of 4 images
+    (128, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),  # two-way split, bands of 4 images of 100 pixels (16-byte copies)
+    (126, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),  # the same, the last band of 2 images
+    (128, 16, 5, 5, 512, 3, 3, 1, 1, 1, 1),    # several padded images: the fused gather's zeros
+    (128, 16, 7, 9, 512, 3, 5, 1, 1, 0, 0),    # several images, 3x5
 ]
 
 
