@@ -761,13 +761,15 @@ void launch_band_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
 
 // Pixel blocks per band that the kernels are built for.
 constexpr int kBandNb4Min = 4, kBandNb4Max = 7;     // four-way split
-constexpr int kBandNb2Min = 12, kBandNb2Max = 13;   // two-way split (3x3)
+constexpr int kBandNb2Min = 12, kBandNb2Max = 13;   // two-way split (3x3), and:
+constexpr int kBandNb2Pair = 9;                      // two whole images of 144 pixels
 
 constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups
 
 bool band_shape_ok(const Geometry& g, int ks, int nb) {
     if (ks == 4) return nb >= kBandNb4Min && nb <= kBandNb4Max && g.fh == 3 && (g.fw == 3 || g.fw == 5);
-    return nb >= kBandNb2Min && nb <= kBandNb2Max && g.fh == 3 && g.fw == 3 && g.k % 64 == 0;
+    return (nb == kBandNb2Pair || (nb >= kBandNb2Min && nb <= kBandNb2Max)) && g.fh == 3 && g.fw == 3 &&
+           g.k % 64 == 0;
 }
 
 }  // namespace
@@ -898,7 +900,8 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
     if (p.ks == 2) {
         // two waves per SIMD (with the four-way split they were slower:
         // 3-4 pixel blocks per wave)
-        if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
+        if (p.nb == kBandNb2Pair) launch_band8_nb<3, 3, kBandNb2Pair>(a, lds, stream);
+        else if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
         else launch_band8_nb<3, 3, 13>(a, lds, stream);
         return 0;
     }

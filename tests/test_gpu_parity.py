@@ -221,6 +221,8 @@ F32_BANDS = [
     (126, 16, 12, 12, 512, 3, 3, 1, 1, 0, 0),  # the same, the last band of 2 images
     (128, 16, 5, 5, 512, 3, 3, 1, 1, 1, 1),    # several padded images: the fused gather's zeros
     (128, 16, 7, 9, 512, 3, 5, 1, 1, 0, 0),    # several images, 3x5
+    (128, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # two-way split, bands of 2 images of 144 pixels (9 blocks)
+    (127, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # the same, the last band of 1 image
 ]
 
 
