@@ -761,10 +761,11 @@ void launch_band_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
 
 // Pixel blocks per band that the kernels are built for.
 constexpr int kBandNb4Min = 4, kBandNb4Max = 7;     // four-way split
-constexpr int kBandNb2Min = 12, kBandNb2Max = 13;   // two-way split (3x3), and:
+constexpr int kBandNb2Min = 12, kBandNb2Max = 14;   // two-way split (3x3), and:
 constexpr int kBandNb2Pair = 9;                      // two whole images of 144 pixels
 
-constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups
+constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups, unless a workgroup's work is long:
+constexpr double kBandLongMacs = 12e6;   // multiply-adds per workgroup
 
 bool band_shape_ok(const Geometry& g, int ks, int nb) {
     if (ks == 4) return nb >= kBandNb4Min && nb <= kBandNb4Max && g.fh == 3 && (g.fw == 3 || g.fw == 5);
@@ -796,7 +797,9 @@ F32BandPlan plan_band_f32(const Geometry& g) {
             const int64_t rounds = (grid + 255) / 256;
             // many short rounds: the tile kernels, which overlap one
             // workgroup's staging with another's multiplies, do better
-            if (rounds > kBandMaxRounds) continue;
+            // (with long ones, staging a band is a small share of its work)
+            const double wg_macs = (double)(4 / ks) * 32 * nb * 32 * g.c * g.taps;
+            if (rounds > kBandMaxRounds && wg_macs < kBandLongMacs) continue;
             const double eff = useful / ((double)rounds * 1024.0 * nb * pp);
             if (eff > best.eff + 1e-9) {
                 best.ks = ks;
@@ -817,7 +820,8 @@ F32BandPlan plan_band_f32(const Geometry& g) {
             if (!band_shape_ok(g, ks, (int)nb)) continue;
             const int64_t grid = (g.n + ipb - 1) / ipb * (g.k / (32 * (4 / ks)));
             const int64_t rounds = (grid + 255) / 256;
-            if (rounds > kBandMaxRounds) continue;
+            const double wg_macs = (double)(4 / ks) * 32 * nb * 32 * g.c * g.taps;
+            if (rounds > kBandMaxRounds && wg_macs < kBandLongMacs) continue;
             const double eff = useful / ((double)rounds * 1024.0 * nb * pp);
             if (eff > best.eff + 1e-9) {
                 best.ks = ks;
@@ -902,7 +906,8 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
         // 3-4 pixel blocks per wave)
         if (p.nb == kBandNb2Pair) launch_band8_nb<3, 3, kBandNb2Pair>(a, lds, stream);
         else if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
-        else launch_band8_nb<3, 3, 13>(a, lds, stream);
+        else if (p.nb == 13) launch_band8_nb<3, 3, 13>(a, lds, stream);
+        else launch_band8_nb<3, 3, 14>(a, lds, stream);
         return 0;
     }
 #define BAND_NB4(FW_)                                                   \

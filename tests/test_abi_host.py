@@ -197,6 +197,8 @@ F32_BANDS = [
     (128, 16, 5, 5, 512, 3, 3, 1, 1, 1, 1),     # several padded images
     (128, 16, 7, 9, 512, 3, 5, 1, 1, 0, 0),     # several images, 3x5
     (127, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),   # two-way split, 2 images of 144 pixels, the last band of 1
+    (128, 64, 112, 112, 128, 3, 3, 1, 1, 0, 0), # Table 1 Conv8: 4-row bands in 14 blocks, 28 rounds of long work
+    (9, 16, 112, 112, 128, 3, 3, 1, 1, 0, 0),
     (32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1),     # the ResNet-style layer: 7-row bands, two-way split
     (128, 64, 56, 56, 64, 3, 3, 1, 1, 0, 0),    # Table 1 Conv9: ragged last band
     (128, 128, 28, 28, 128, 3, 3, 1, 1, 0, 0),  # Table 1 Conv10

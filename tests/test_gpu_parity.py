@@ -223,6 +223,7 @@ F32_BANDS = [
     (128, 16, 7, 9, 512, 3, 5, 1, 1, 0, 0),    # several images, 3x5
     (128, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # two-way split, bands of 2 images of 144 pixels (9 blocks)
     (127, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # the same, the last band of 1 image
+    (9, 16, 112, 112, 128, 3, 3, 1, 1, 0, 0),  # two-way split, 4-row bands of 110 pixels in 14 blocks
 ]
 
 
