@@ -840,7 +840,8 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
     if (wmax >= g.k * g.c * T)
         r.fail("fp32 band conv: filter element %lld of %lld", (long long)wmax, (long long)(g.k * g.c * T));
     // stage 1, the farthest pair and tap stay inside one LDS read's reach
-    if (kBandStageBytes + (PP - 1) * 2 * kBandSlot * 4 + T * 4 >= 65536)
+    const int64_t tap_reach = a.mode == kBandRaw ? (int64_t)(FH - 1) * a.rpitch + FW : T;
+    if (kBandStageBytes + (PP - 1) * 2 * kBandSlot * 4 + tap_reach * 4 >= 65536)
         r.fail("fp32 band conv: LDS read offsets exceed 16 bits");
     if (conv_scratch_bytes(g, fused) != 0)
         r.fail("fp32 band conv: scratch of %lld bytes requested", (long long)conv_scratch_bytes(g, fused));

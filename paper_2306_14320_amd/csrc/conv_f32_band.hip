@@ -768,7 +768,9 @@ constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups, unless a workgr
 constexpr double kBandLongMacs = 12e6;   // multiply-adds per workgroup
 
 bool band_shape_ok(const Geometry& g, int ks, int nb) {
-    if (ks == 4) return nb >= kBandNb4Min && nb <= kBandNb4Max && g.fh == 3 && (g.fw == 3 || g.fw == 5);
+    if (ks == 4)
+        return nb >= kBandNb4Min && nb <= kBandNb4Max &&
+               ((g.fh == 3 && (g.fw == 3 || g.fw == 5)) || (g.fh == 5 && g.fw == 5));
     return (nb == kBandNb2Pair || (nb >= kBandNb2Min && nb <= kBandNb2Max)) && g.fh == 3 && g.fw == 3 &&
            g.k % 64 == 0;
 }
@@ -910,17 +912,19 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
         else launch_band8_nb<3, 3, 14>(a, lds, stream);
         return 0;
     }
-#define BAND_NB4(FW_)                                                   \
-    switch (p.nb) {                                                     \
-        case 4: launch_band_nb<3, FW_, 4, 4>(a, lds, stream); break;    \
-        case 5: launch_band_nb<3, FW_, 5, 4>(a, lds, stream); break;    \
-        case 6: launch_band_nb<3, FW_, 6, 4>(a, lds, stream); break;    \
-        default: launch_band_nb<3, FW_, 7, 4>(a, lds, stream); break;   \
+#define BAND_NB4(FH_, FW_)                                                \
+    switch (p.nb) {                                                       \
+        case 4: launch_band_nb<FH_, FW_, 4, 4>(a, lds, stream); break;    \
+        case 5: launch_band_nb<FH_, FW_, 5, 4>(a, lds, stream); break;    \
+        case 6: launch_band_nb<FH_, FW_, 6, 4>(a, lds, stream); break;    \
+        default: launch_band_nb<FH_, FW_, 7, 4>(a, lds, stream); break;   \
     }
-    if (g.fw == 3) {
-        BAND_NB4(3)
+    if (g.fh == 5) {
+        BAND_NB4(5, 5)
+    } else if (g.fw == 3) {
+        BAND_NB4(3, 3)
     } else {
-        BAND_NB4(5)
+        BAND_NB4(3, 5)
     }
 #undef BAND_NB4
     return 0;

@@ -199,6 +199,8 @@ F32_BANDS = [
     (127, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),   # two-way split, 2 images of 144 pixels, the last band of 1
     (128, 64, 112, 112, 128, 3, 3, 1, 1, 0, 0), # Table 1 Conv8: 4-row bands in 14 blocks, 28 rounds of long work
     (9, 16, 112, 112, 128, 3, 3, 1, 1, 0, 0),
+    (128, 96, 24, 24, 256, 5, 5, 1, 1, 0, 0),   # Table 1 Conv5: 5x5, 11-row bands, 8 rounds of long work
+    (16, 16, 20, 20, 256, 5, 5, 1, 1, 2, 2),
     (32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1),     # the ResNet-style layer: 7-row bands, two-way split
     (128, 64, 56, 56, 64, 3, 3, 1, 1, 0, 0),    # Table 1 Conv9: ragged last band
     (128, 128, 28, 28, 128, 3, 3, 1, 1, 0, 0),  # Table 1 Conv10
@@ -284,10 +286,11 @@ def test_fp32_bands_decline_unsupported_shapes():
         return P.im2win_conv_kernel(P.im2win_desc(*c.values(), P.IM2WIN_F32), False)
     assert name() == "f32_bands"
     assert name(n=56) != "f32_bands"            # 224 workgroups: 77% of one round
-    assert name(n=1100) != "f32_bands"          # more than 4 rounds
+    assert name(n=1100, c=16) != "f32_bands"    # more than 4 rounds of short work per workgroup
+    assert name(n=1088) == "f32_bands"          # 17 rounds of long work (13.8M multiply-adds each)
     assert name(c=120) != "f32_bands"           # C not a multiple of 16
     assert name(k=112) != "f32_bands"           # K not a multiple of 32
-    assert name(fh=5, ph=2) != "f32_bands"      # 5x5 filter
+    assert name(fh=5, fw=3, ph=2, pw=1) != "f32_bands"   # 5x3 filter (5x5 is taken: Conv5 above)
     assert name(h=12, w=12, ph=0, pw=0) != "f32_bands"   # 5x4 = 20 pixels
 
 

@@ -224,6 +224,8 @@ F32_BANDS = [
     (128, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # two-way split, bands of 2 images of 144 pixels (9 blocks)
     (127, 16, 14, 14, 256, 3, 3, 1, 1, 0, 0),  # the same, the last band of 1 image
     (9, 16, 112, 112, 128, 3, 3, 1, 1, 0, 0),  # two-way split, 4-row bands of 110 pixels in 14 blocks
+    (16, 16, 24, 24, 256, 5, 5, 1, 1, 0, 0),   # 5x5: bands of 11 and 9 rows of 20 pixels
+    (16, 16, 20, 20, 256, 5, 5, 1, 1, 2, 2),   # 5x5 with padding 2: the raw rows' zero columns
 ]
 
 
