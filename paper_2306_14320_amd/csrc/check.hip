@@ -858,7 +858,7 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
 void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPlan& p, Report& r) {
     const F32BandArgs a = band_args_small_c_f32(g, p, fused, nullptr, nullptr, nullptr);
     const int C = (int)g.c, FH = (int)g.fh, FW = (int)g.fw, T = FH * FW;
-    const int HU = (FH + 1) / 2, S = C * HU * FW, SW = (S + 1) / 2, nb = p.nb;
+    const int HU = (FH + 1) / 2, S = smallc_steps(C, FH, FW), SW = (S + 1) / 2, nb = p.nb;
     const int64_t slot_bytes = (int64_t)a.slotf * 4;
     const int64_t rb_f = (int64_t)C * a.rrows * a.rpitch;   // floats of one raw-row buffer (fused)
     if (C != kSmallCChannels || p.ks != 2 || p.lds_bytes > kConvLdsMaxBytes ||
@@ -1010,11 +1010,21 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
                     const int64_t m = t.m0 + pix / g.wo, n = pix % g.wo;
                     const int sl = lane >> 5;
                     for (int i = 0; i < nq; ++i) {
-                        const int q = ks * SW + i, c = q / (HU * FW), rr = q % (HU * FW), u = rr / FW, v = rr % FW;
-                        const int uu = u + sl * (FH - HU);   // the filter row this slot multiplies
+                        const int q = ks * SW + i;
+                        // the element this slot multiplies, and the kernel's read:
+                        // the slot's base (one channel further in the pair
+                        // steps, Fh - HU rows in the last channel's) plus
+                        // slot 0's element offset
+                        const SmallCStep st = smallc_step(C, FH, FW, q, sl), s0 = smallc_step(C, FH, FW, q, 0);
+                        const int c = st.c, uu = st.u, v = st.v;
                         const int64_t f =
-                            fused ? smallc_raw_window(a, t, FH, lane, b) / 4 + ((int64_t)c * a.rrows + u) * a.rpitch + v
-                                  : (int64_t)c * a.slotf + smallc_window(a, t, FH, lane, b) / 4 + (int64_t)v * FH + u;
+                            fused ? smallc_raw_window(a, t, FH, lane, b) / 4 +
+                                        (st.pair ? (int64_t)sl * a.rrows : (int64_t)(C - 1) * a.rrows + sl * (FH - HU)) *
+                                            a.rpitch +
+                                        ((st.pair ? (int64_t)s0.c * a.rrows : 0) + s0.u) * a.rpitch + s0.v
+                                  : smallc_window(a, t, FH, lane, b) / 4 +
+                                        (st.pair ? (int64_t)sl * a.slotf : (int64_t)(C - 1) * a.slotf + sl * (FH - HU)) +
+                                        (st.pair ? (int64_t)s0.c * a.slotf : 0) + (int64_t)s0.v * FH + s0.u;
                         const std::vector<int64_t>& src = fused ? raw : holds;
                         const int64_t yy = m * g.sh + uu - g.ph, xx = n * g.sw + v - g.pw;
                         const bool pad = yy < 0 || yy >= g.h || xx < 0 || xx >= g.w;
@@ -1062,12 +1072,17 @@ void check_conv_band_small_c_f32(const Geometry& g, bool fused, const F32BandPla
         r.fail("fp32 small-C band conv: y image of %llu bytes against the dropped-store offset",
                (unsigned long long)y_bytes);
     // every (filter row, column) of every channel is multiplied exactly once
-    // per output: slot 0 rows u < HU, slot 1 rows u + Fh - HU >= HU
+    // per output (the repeated middle row's second copy has zero weight)
     std::vector<int> used((size_t)C * T, 0);
     for (int q = 0; q < S; ++q)
         for (int sl = 0; sl < 2; ++sl) {
-            const int c = q / (HU * FW), rr = q % (HU * FW), u = rr / FW, v = rr % FW, uu = u + sl * (FH - HU);
-            if (sl == 0 || uu >= HU) ++used[(size_t)(c * FH + uu) * FW + v];
+            const SmallCStep st = smallc_step(C, FH, FW, q, sl);
+            if (st.c < 0 || st.c >= C || st.u < 0 || st.u >= FH || st.v < 0 || st.v >= FW) {
+                r.fail("fp32 small-C band conv: step %d slot %d multiplies channel %d row %d column %d", q, sl, st.c,
+                       st.u, st.v);
+                return;
+            }
+            if (!st.zero) ++used[(size_t)(st.c * FH + st.u) * FW + st.v];
         }
     for (size_t i = 0; i < used.size(); ++i)
         if (used[i] != 1) {

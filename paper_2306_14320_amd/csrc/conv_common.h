@@ -614,28 +614,55 @@ __host__ __device__ inline BandTile smallc_tile(const F32BandArgs& a, int bid) {
     t.nrows = a.ho - t.m0 < a.rows ? a.ho - t.m0 : a.rows;
     t.npix = t.nrows * a.wo;
     t.shift = a.mode == kBandWide ? (t.m0 * a.row_len) & 3 : 0;
+    t.nimg = 1;
     return t;
 }
 
+// The reduction of the small-C kernel in k-steps of two elements, one per
+// k-slot of the MFMA: first the channel pairs (2p, 2p + 1), slot 0 taking
+// channel 2p and slot 1 channel 2p + 1 at the same filter tap (u, v); then,
+// for odd C, the last channel with filter rows u and u + Fh - ceil(Fh/2) in
+// the two slots, u < ceil(Fh/2), where for odd Fh the middle row comes up in
+// both and slot 1's copy has zero weight.  Within a group the slots differ
+// by a fixed offset (one channel; Fh - ceil(Fh/2) rows), so one LDS read per
+// step serves both.
+struct SmallCStep {
+    int c, u, v;   // channel, filter row and column this k-slot multiplies
+    bool zero;     // zero weight (the repeated middle row)
+    bool pair;     // in the channel-pair group
+};
+__host__ __device__ constexpr int smallc_steps(int c, int fh, int fw) {
+    return (c / 2) * fh * fw + (c % 2) * ((fh + 1) / 2) * fw;
+}
+__host__ __device__ constexpr SmallCStep smallc_step(int c, int fh, int fw, int q, int slot) {
+    const int ga = (c / 2) * fh * fw;
+    if (q < ga) {
+        const int pr = q / (fh * fw), r = q - pr * (fh * fw);
+        return SmallCStep{2 * pr + slot, r / fw, r % fw, false, true};
+    }
+    const int hu = (fh + 1) / 2, r = q - ga, u = r / fw + slot * (fh - hu);
+    return SmallCStep{c - 1, u, r % fw, slot == 1 && u < hu, false};
+}
+
 // LDS byte offset, within a channel slot, of the window start of the pixel of
-// `lane` in pixel block b; k-slot lane / 32 starts Fh - ceil(Fh/2) filter rows
-// (positions) further.  Pixels past the band are clamped to its last pixel.
+// `lane` in pixel block b (the same for both k-slots; the step adds the
+// slots' offsets).  Pixels past the band are clamped to its last pixel.
 __host__ __device__ inline uint32_t smallc_window(const F32BandArgs& a, const BandTile& t, int fh, int lane, int b) {
     int p = b * 32 + (lane & 31);
     if (p > t.npix - 1) p = t.npix - 1;
     const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
-    return (uint32_t)(t.shift + ml * a.row_len + n * a.sw * fh + (lane >> 5) * (fh - (fh + 1) / 2)) * 4u;
+    return (uint32_t)(t.shift + ml * a.row_len + n * a.sw * fh) * 4u;
 }
 
 // Fused: byte offset, in a raw-row buffer, of the window that lane `lane`
-// of pixel block b reads (the zero-padded input row ml*sh + its slot's first
-// filter row, column n*sw - pw); filter tap (c, u, v) adds
-// ((c*rrows + u)*rpitch + v) floats.  Pixels past the band repeat the last.
+// of pixel block b reads (the zero-padded input row ml*sh, column
+// n*sw - pw); filter tap (c, u, v) adds ((c*rrows + u)*rpitch + v) floats.
+// Pixels past the band repeat the last.
 __host__ __device__ inline uint32_t smallc_raw_window(const F32BandArgs& a, const BandTile& t, int fh, int lane, int b) {
     int p = b * 32 + (lane & 31);
     if (p > t.npix - 1) p = t.npix - 1;
     const int ml = (int)fast_div((uint32_t)p, a.div_wo), n = p - ml * a.wo;
-    return (uint32_t)((ml * a.sh + (lane >> 5) * (fh - (fh + 1) / 2)) * a.rpitch + a.rlpad - a.pw + n * a.sw) * 4u;
+    return (uint32_t)(ml * a.sh * a.rpitch + a.rlpad - a.pw + n * a.sw) * 4u;
 }
 
 // Parts (copies of 256 elements wide, 64 otherwise) of one channel slot.

@@ -429,7 +429,7 @@ __global__ __launch_bounds__(2 * kBandThreads, 1) void conv_f32_band8_kernel(F32
 template <int C, int FH, int FW, int NB, int MODE, int WPS>
 __global__ __launch_bounds__(WPS * kBandThreads, 1) void conv_f32_band_small_c_kernel(F32BandArgs a) {
     constexpr int HU = (FH + 1) / 2;
-    constexpr int S = C * HU * FW;      // k-steps of the whole reduction
+    constexpr int S = smallc_steps(C, FH, FW);   // k-steps of the whole reduction
     constexpr int SW = (S + 1) / 2;     // k-steps of the first half (the second takes S - SW)
     constexpr int RP = NB * 32;
     constexpr int RW = 32 * RP;         // floats of one block's partial sums
@@ -519,25 +519,30 @@ __global__ __launch_bounds__(WPS * kBandThreads, 1) void conv_f32_band_small_c_k
             L[row * a.rpitch + (k < a.rlpad ? k : a.w + k)] = 0.0f;
         }
     }
-    // Filter values of this wave's k-steps q = ks*SW + i = (c, u, v) for the
-    // output channels of group kt: slot 0 row u, slot 1 row u + Fh - HU (zero
-    // where that row is also slot 0's, past the last step, and for output
-    // channels past K, whose offsets lie past the filter).  (q, c, u, v)
-    // are compile-time per half, so each load is a per-lane base plus an
-    // immediate, and the zero-weight duplicate row a select.
+    // Filter values of this wave's k-steps q = ks*SW + i for the output
+    // channels of group kt: the (channel, row, column) of each k-slot's
+    // element (smallc_step; zero for the repeated middle row, past the last
+    // step, and for output channels past K, whose offsets lie past the
+    // filter).  q is compile-time per half, so each load is a per-lane base
+    // plus an immediate, the k-slot a select.
     auto load_filter_half = [&](auto ks_tag, int kt, float (&f)[SW]) {
         constexpr int KSI = decltype(ks_tag)::value;
         const int kout = (kt * 2 + cb) * 32 + col;
-        const uint32_t base = (uint32_t)((kout * C * FH + slot * (FH - HU)) * FW * 4);
+        // slot 1's element lies one channel (pair steps) or Fh - HU rows (the
+        // last channel's steps) after slot 0's
+        const uint32_t base = (uint32_t)(kout * C * FH * FW * 4);
+        const uint32_t bpair = base + (uint32_t)(slot * FH * FW * 4), blast = base + (uint32_t)(slot * (FH - HU) * FW * 4);
 #pragma unroll
         for (int i = 0; i < SW; ++i) {
-            const int q = KSI * SW + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
+            const int q = KSI * SW + i;
             if (q >= S) {
                 f[i] = 0.0f;
                 continue;
             }
-            uint32_t off = base + (uint32_t)(((c * FH + u) * FW + v) * 4);
-            if (u + (FH - HU) < HU) off = slot ? kBandOutside : off;   // slot 1 would repeat a slot-0 row
+            const SmallCStep s0 = smallc_step(C, FH, FW, q, 0), s1 = smallc_step(C, FH, FW, q, 1);
+            const uint32_t imm = (uint32_t)(((s0.c * FH + s0.u) * FW + s0.v) * 4);
+            uint32_t off = (s0.pair ? bpair : blast) + imm;
+            if (s1.zero) off = slot ? kBandOutside : off;   // slot 1 would repeat a slot-0 row
             f[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, off, 0, 0));
         }
     };
@@ -597,17 +602,21 @@ __global__ __launch_bounds__(WPS * kBandThreads, 1) void conv_f32_band_small_c_k
             else
                 issue_strips(bid + 1, cur ^ 1);
         }
-        // byte offset of each block's window: per channel (unfused), or of
-        // channel 0 (fused, the channel and filter row add a uniform offset)
-        uint32_t bb[GATHER ? 1 : C][NBW];
+        // byte offset of each block's window for this lane's k-slot: in the
+        // channel-pair steps (slot 1 one channel further), and in the last
+        // channel's steps (slot 1 Fh - HU rows further); the step's channel
+        // and tap add a uniform offset
+        uint32_t bp[NBW], bl[NBW];
 #pragma unroll
         for (int b = 0; b < NBW; ++b) {
             if constexpr (GATHER) {
-                bb[0][b] = smallc_raw_window(a, tile, FH, lane, B0 + b) + (uint32_t)(cur * buf_f) * 4u;
+                const uint32_t r0 = smallc_raw_window(a, tile, FH, lane, B0 + b) + (uint32_t)(cur * buf_f) * 4u;
+                bp[b] = r0 + (uint32_t)(slot * a.rrows * a.rpitch) * 4u;
+                bl[b] = r0 + (uint32_t)(slot * (FH - HU) * a.rpitch) * 4u;
             } else {
                 const uint32_t w0 = smallc_window(a, tile, FH, lane, B0 + b) + (uint32_t)(cur * buf_f) * 4u;
-#pragma unroll
-                for (int c = 0; c < C; ++c) bb[c][b] = w0 + (uint32_t)(c * a.slotf) * 4u;
+                bp[b] = w0 + (uint32_t)(slot * a.slotf) * 4u;
+                bl[b] = w0 + (uint32_t)((C - 1) * a.slotf + slot * (FH - HU)) * 4u;
             }
         }
 #pragma unroll
@@ -623,18 +632,18 @@ __global__ __launch_bounds__(WPS * kBandThreads, 1) void conv_f32_band_small_c_k
             constexpr int Q0 = KSI * SW, NQ = KSI == 0 ? SW : S - SW;
             float bv[2][NBW];
             auto read_step = [&](int i, float (&dst)[NBW]) {
-                const int q = Q0 + i, c = q / (HU * FW), r = q - c * (HU * FW), u = r / FW, v = r - u * FW;
+                const SmallCStep s0 = smallc_step(C, FH, FW, Q0 + i, 0);   // slot 0's element
                 const char* Lb = reinterpret_cast<const char*>(L);
-                if constexpr (GATHER) {
-                    const int cu = (c * a.rrows + u) * a.rpitch * 4;
+                // uniform offset of slot 0's element from the slot's base
+                int off;
+                if constexpr (GATHER)
+                    off = ((s0.pair ? s0.c * a.rrows : 0) + s0.u) * a.rpitch * 4 + s0.v * 4;
+                else
+                    off = ((s0.pair ? s0.c * a.slotf : 0) + s0.v * FH + s0.u) * 4;
+                if (!s0.pair && GATHER) off += (C - 1) * a.rrows * a.rpitch * 4;
 #pragma unroll
-                    for (int b = 0; b < NBW; ++b)
-                        dst[b] = *reinterpret_cast<const float*>(Lb + bb[0][b] + cu + v * 4);
-                } else {
-#pragma unroll
-                    for (int b = 0; b < NBW; ++b)
-                        dst[b] = *reinterpret_cast<const float*>(Lb + bb[c][b] + (v * FH + u) * 4);
-                }
+                for (int b = 0; b < NBW; ++b)
+                    dst[b] = *reinterpret_cast<const float*>(Lb + (s0.pair ? bp[b] : bl[b]) + off);
             };
             read_step(0, bv[0]);
 #pragma unroll
