@@ -215,8 +215,9 @@ int im2win_conv2d_fused_noalloc(const im2win_desc* d, const void* x, const void*
  * im2win_conv2d_fused (fused != 0) launches for *d, for logs, profiles and
  * tests.  *name receives a string owned by the library (valid for the life of
  * the process), one of:
- *   "f32_bands"          fp32, a band of output rows of one image x 32 or 64
- *                        output channels per workgroup
+ *   "f32_bands"          fp32, a band of output rows of one image (or of
+ *                        several whole small images) x 32 or 64 output
+ *                        channels per workgroup
  *   "f32_bands_small_c"  fp32 with 3 input channels and a 3x3, 7x7 or 11x11
  *                        filter: runs of bands of rows x 64 output channels
  *                        per workgroup, each band's whole reduction staged
