@@ -580,7 +580,7 @@ struct F32BandPlan {
 // The plan of the band kernel, or !ok when the shape is not one it takes
 // (fp32; 3x3 or 3x5 filter; C a multiple of 16, K of 32 (of 64 with the
 // two-way split, 3x3 only); a band of rows, or of several whole images,
-// whose strips fit a slot and whose pixels fill 4-7 blocks of 32 (9 or 12-14
+// whose strips fit a slot and whose pixels fill 4-7 blocks of 32 (9 or 11-14
 // with the two-way split); at most 4 rounds of 256 workgroups unless each
 // workgroup has at least 12M multiply-adds to do, and at least 85% of the
 // occupied matrix-core work useful after rounding the grid to whole rounds).

@@ -770,7 +770,7 @@ void launch_band_nb(const F32BandArgs& a, int64_t lds, hipStream_t stream) {
 
 // Pixel blocks per band that the kernels are built for.
 constexpr int kBandNb4Min = 4, kBandNb4Max = 7;     // four-way split
-constexpr int kBandNb2Min = 12, kBandNb2Max = 14;   // two-way split (3x3), and:
+constexpr int kBandNb2Min = 11, kBandNb2Max = 14;   // two-way split (3x3), and:
 constexpr int kBandNb2Pair = 9;                      // two whole images of 144 pixels
 
 constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups, unless a workgroup's work is long:
@@ -916,6 +916,7 @@ int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, co
         // two waves per SIMD (with the four-way split they were slower:
         // 3-4 pixel blocks per wave)
         if (p.nb == kBandNb2Pair) launch_band8_nb<3, 3, kBandNb2Pair>(a, lds, stream);
+        else if (p.nb == 11) launch_band8_nb<3, 3, 11>(a, lds, stream);
         else if (p.nb == 12) launch_band8_nb<3, 3, 12>(a, lds, stream);
         else if (p.nb == 13) launch_band8_nb<3, 3, 13>(a, lds, stream);
         else launch_band8_nb<3, 3, 14>(a, lds, stream);

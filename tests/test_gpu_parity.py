@@ -211,7 +211,7 @@ F32_BANDS = [
     (4, 16, 13, 23, 2048, 3, 5, 1, 2, 0, 1),   # 121 pixels, rows of 75 (4-byte copies)
     (3, 32, 29, 15, 2720, 3, 3, 2, 1, 1, 0),   # 195 pixels, row stride 2, grid not a multiple of 8
     (2, 16, 56, 56, 1024, 3, 3, 1, 1, 1, 1),   # two-way split: 7-row bands of 56 columns
-    (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),   # two-way split: bands of 14 and 12 rows
+    (8, 16, 28, 28, 1024, 3, 3, 1, 1, 0, 0),   # two-way split: two bands of 13 rows in 11 blocks
     (8, 16, 55, 55, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2
     (8, 16, 52, 52, 1024, 3, 3, 2, 2, 1, 1),   # two-way split, stride 2, fused from raw rows
     (2, 16, 28, 32, 4096, 3, 5, 2, 2, 1, 4),   # raw rows with 8 zero columns in front (pw = 4)
