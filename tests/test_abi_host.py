@@ -264,6 +264,22 @@ def test_conv_kernel_names_on_workloads():
     assert P.im2win_conv_kernel(d, False) == "per_output"
 
 
+def test_conv_kernel_names_on_table1():
+    """The kernel family each of the paper's twelve layers takes at batch
+    128, both variants alike: three-channel layers on the persistent kernel,
+    Conv4 (7x7, rows longer than a band slot) on the tiles, the rest on bands
+    (Conv6, Conv11, Conv12 as bands of several whole images)."""
+    want = {1: "f32_bands_small_c", 2: "f32_bands_small_c", 3: "f32_bands_small_c", 4: "f32_tiles",
+            5: "f32_bands", 6: "f32_bands", 7: "f32_bands_small_c", 8: "f32_bands", 9: "f32_bands",
+            10: "f32_bands", 11: "f32_bands", 12: "f32_bands"}
+    assert len(workloads.TABLE1) == 12
+    for i, wl in enumerate(workloads.TABLE1, start=1):
+        d = _desc(_wl_shape(wl), P.IM2WIN_F32)
+        assert (P.im2win_conv_kernel(d, False), P.im2win_conv_kernel(d, True)) == (want[i],) * 2, wl.name
+        # the band kernels read w as it is; Conv4's tiles take repacked filter blocks
+        assert (P.im2win_filter_scratch_bytes(d) > 0) == (want[i] == "f32_tiles"), wl.name
+
+
 @pytest.mark.parametrize("layout", [0, 1], ids=["padded", "trimmed"])
 @pytest.mark.parametrize("case", F32_BANDS, ids=lambda c: "x".join(map(str, c)))
 def test_launch_plans_in_bounds_fp32_bands(case, layout):
