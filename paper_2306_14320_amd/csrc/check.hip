@@ -610,7 +610,7 @@ void check_conv_band_f32(const Geometry& g, bool fused, const F32BandPlan& p, Re
         (KS != 4 && KS != 2) || a.rows < 1 || nb * 32 < brows * a.wo || (nb - 1) * 32 >= brows * a.wo ||
         brows * g.row_len + 3 > 64 * kBandMaxSeg || g.c % (2 * kBandChunk) || g.k % (32 * CB) ||
         (int64_t)a.nbands * a.rows < g.ho || (int64_t)(a.nbands - 1) * a.rows >= g.ho ||
-        (multi && (a.rows != g.ho || a.nbands != 1 || a.ipb > g.n || a.mode == kBandRaw)) ||
+        (multi && (a.rows != g.ho || a.nbands != 1 || a.ipb > g.n || a.mode == kBandRaw)) || !band_nb_compiled(KS, nb) ||
         groups * a.nkt != a.grid) {
         r.fail("fp32 band conv: plan (ks %d, %d rows, %d images, nb %d, %lld bytes of LDS)", KS, a.rows, a.ipb, nb,
                (long long)p.lds_bytes);

@@ -587,6 +587,8 @@ struct F32BandPlan {
 // The plan does not depend on fusion, so both variants take a shape or
 // neither.
 F32BandPlan plan_band_f32(const Geometry& g);
+// Whether the band kernels are built for nb pixel blocks with the ks-way split.
+bool band_nb_compiled(int ks, int nb);
 F32BandArgs band_args_f32(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,
                           float* y);
 int launch_conv_f32_band(const Geometry& g, const F32BandPlan& p, bool fused, const void* src, const void* w,

@@ -777,14 +777,17 @@ constexpr int kBandMaxRounds = 4;   // rounds of 256 workgroups, unless a workgr
 constexpr double kBandLongMacs = 12e6;   // multiply-adds per workgroup
 
 bool band_shape_ok(const Geometry& g, int ks, int nb) {
-    if (ks == 4)
-        return nb >= kBandNb4Min && nb <= kBandNb4Max &&
-               ((g.fh == 3 && (g.fw == 3 || g.fw == 5)) || (g.fh == 5 && g.fw == 5));
-    return (nb == kBandNb2Pair || (nb >= kBandNb2Min && nb <= kBandNb2Max)) && g.fh == 3 && g.fw == 3 &&
-           g.k % 64 == 0;
+    if (!band_nb_compiled(ks, nb)) return false;
+    if (ks == 4) return (g.fh == 3 && (g.fw == 3 || g.fw == 5)) || (g.fh == 5 && g.fw == 5);
+    return g.fh == 3 && g.fw == 3 && g.k % 64 == 0;
 }
 
 }  // namespace
+
+bool band_nb_compiled(int ks, int nb) {
+    if (ks == 4) return nb >= kBandNb4Min && nb <= kBandNb4Max;
+    return ks == 2 && (nb == kBandNb2Pair || (nb >= kBandNb2Min && nb <= kBandNb2Max));
+}
 
 F32BandPlan plan_band_f32(const Geometry& g) {
     F32BandPlan best;
